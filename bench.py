@@ -1,0 +1,288 @@
+"""Benchmark of the SDQ decomposed linear layer on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+
+A step is one pass of the hot path over one batch of synthetic input: for
+every layer of the workload, per-token activation quantization
+(sdq_quantize_act) followed by the decomposed GEMM (sdq_gemm).  The weights
+were packed offline (sdq_pack, host); the packer's time is reported beside
+the line, never inside the step.  Every input is resident in HBM when the
+timed region starts, and distinct copies of the packed weights (>= 512 MB,
+twice the 256 MB Infinity Cache) are rotated so each launch streams its
+weights from HBM.
+
+Prints one JSON line: dense-equivalent TFLOP/s of the step (2*M*N*K per layer),
+the roofline object of the dominant kernel (the GEMM) measured with HIP events
+on the launch stream, and the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"fp8": 5033.0, "f16": 2516.6}
+
+WORKLOADS = {
+    # name: (workload id, layer indices, M)
+    "llama7b-attn-decode": (2, [0], 1),
+    "llama7b-mlp-prefill": (3, [0, 1, 2], 2048),
+    "opt6.7b-ffn-decode": (4, [0, 1], 64),
+    "tiny": (1, [0], 16),
+}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="llama7b-attn-decode",
+                   help="|".join(WORKLOADS) + "|sweep (with --layer/--M/--fmt)")
+    p.add_argument("--layer", type=int, default=0, help="block-sweep layer index (0..6)")
+    p.add_argument("--M", type=int, default=1, help="block-sweep token count")
+    p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
+    p.add_argument("--rotate-mb", type=float, default=512.0)
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2406_13868_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(name: str):
+    """HBM bytes per GEMM launch from committed counter runs, if they were taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{name}.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {a.gpus}); "
+              "the path shards by output rows with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2406_13868_amd as sdq
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    sdq._lib.lib()
+
+    if a.workload == "sweep":
+        wid = 5
+        fmt = synth.WORKLOADS[5].formats[a.fmt]
+        layers = [a.layer]
+        M = a.M
+        wl_name = f"llama7b block sweep {synth.WORKLOADS[5].layers[a.layer].name} M={M} {fmt.label}"
+    else:
+        wid, layers, M = WORKLOADS[a.workload]
+        fmt = synth.WORKLOADS[wid].formats[0]
+        wl_name = synth.WORKLOADS[wid].name
+    W_def = synth.WORKLOADS[wid]
+    cfg = sdq.Config.of(fmt)
+
+    # ---------------------------------------------------------------- inputs
+    Ls = [W_def.layers[i] for i in layers]
+    Ws, Xs, blobs_host = [], [], []
+    t_pack = t_pack1 = 0.0
+    for li, L in zip(layers, Ls):
+        W = synth.make_w(wid, li, L.N, L.K)
+        X = synth.make_x(wid, M, L.K)
+        t0 = time.perf_counter()
+        blob = sdq.pack(W, cfg)
+        t_pack += time.perf_counter() - t0
+        if li == layers[0]:
+            t0 = time.perf_counter()
+            sdq.pack(W, cfg, n_threads=1)
+            t_pack1 = time.perf_counter() - t0
+        Ws.append(W)
+        Xs.append(X)
+        blobs_host.append(blob)
+    phys = sum(b.nbytes for b in blobs_host)
+    logical = sum(sdq.logical_bytes(cfg, L.N, L.K) for L in Ls)
+    R = max(2, math.ceil(a.rotate_mb * 1e6 / phys))
+    x_dtype = torch.bfloat16 if W_def.x_dtype == "bf16" else torch.float32
+    blobs = [[torch.from_numpy(b).to(dev) for b in blobs_host] for _ in range(R)]
+    Xd = [[torch.from_numpy(X).to(dev).to(x_dtype) for X in Xs] for _ in range(R)]
+    Xq = [[torch.empty((M, L.K), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)]
+    sa = [[torch.empty((M,), dtype=torch.float32, device=dev) for _ in Ls] for _ in range(R)]
+    Y = [[torch.empty((M, L.N), dtype=torch.float32, device=dev) for L in Ls] for _ in range(R)]
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        r = i % R
+        for j, L in enumerate(Ls):
+            sdq.linear(Xd[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], xq=Xq[r][j],
+                       scales=sa[r][j])
+
+    def gemms(i):
+        r = i % R
+        for j, L in enumerate(Ls):
+            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j])
+
+    def gemms_hot(i):
+        for j, L in enumerate(Ls):
+            sdq.gemm(Xq[0][j], sa[0][j], blobs[0][j], L.N, L.K, cfg, out=Y[0][j])
+
+    def capture(fn, n, start):
+        """HIP graph of n calls of fn (launch-bound loops replay without host gaps)."""
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn(start)
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(g):
+            for i in range(n):
+                fn(start + i)
+        return g
+
+    def timed(g, n):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        st = torch.cuda.current_stream()
+        e0.record(st)
+        g.replay()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n  # ms per call
+
+    # ---------------------------------------------------------------- timed steps
+    for i in range(a.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    g_step = capture(step, a.steps, a.warmup)
+    timed(g_step, a.steps)  # first replay uploads the graph
+    ms_step = timed(g_step, a.steps)
+
+    # ---------------------------------------------- the GEMM kernel alone (dominant kernel)
+    n_g = max(a.steps, 2 * R)
+    g_gemm = capture(gemms, n_g, 0)
+    timed(g_gemm, n_g)
+    gemm_us = timed(g_gemm, n_g) * 1e3
+    g_hot = capture(gemms_hot, n_g, 0)
+    timed(g_hot, n_g)
+    gemm_hot_us = timed(g_hot, n_g) * 1e3
+    # eager launches (host launch rate included): context only
+    torch.cuda.synchronize()
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record(stream)
+    for i in range(n_g):
+        gemms(i)
+    b1.record(stream)
+    torch.cuda.synchronize()
+    gemm_b2b_us = b0.elapsed_time(b1) * 1e3 / n_g
+
+    flops = sum(2.0 * M * L.N * L.K for L in Ls)
+    alg_bytes = logical + sum(M * L.K + 4 * M + 4 * M * L.N for L in Ls)
+    paths = sorted({sdq.gemm_path(cfg, M, L.N, L.K) for L in Ls})
+    hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family == "mx" and M < 256)
+    if hbm_bound:
+        achieved = alg_bytes / (gemm_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = flops / (gemm_us * 1e-6) / 1e12
+        peak = MFMA_PEAK_TFLOPS["fp8" if cfg.family == "mx" else "f16"]
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4)}
+    tkey = a.workload if a.workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
+    roof["traffic"] = measured_traffic(tkey)
+    roof["kernel_us"] = round(gemm_us / len(Ls), 3)
+
+    # ---------------------------------------------------------------- CPU oracle
+    cpu = None
+    if not a.no_cpu_baseline:
+        cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds)
+
+    value = flops / (ms_step * 1e-3) / 1e12
+    line = {
+        "metric": "dense-equivalent TFLOP/s and % roofline of sdq_gemm, LLaMA-7B layer shapes",
+        "value": round(value, 4),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8" if cfg.family == "int" else "fp8",
+        "data": "synthetic (seeded generators shaped like the named layers; no weights or datasets)",
+        "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
+                   "formats": fmt.label, "gemm_path": ["decode", "mfma"][paths[-1] - 1] if paths else None,
+                   "parallelism": "none (one GPU)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "gemm_us_graph": round(gemm_us, 3),
+        "gemm_us_eager": round(gemm_b2b_us, 3),
+        "gemm_us_cache_resident": round(gemm_hot_us, 3),
+        "gemm_dense_equiv_tflops": round(flops / (gemm_us * 1e-6) / 1e12, 3),
+        "logical_bytes": int(logical),
+        "physical_bytes": int(phys),
+        "algorithmic_bytes_per_launch": int(alg_bytes),
+        "rotated_copies": R,
+        "packer_s_threaded": round(t_pack, 3),
+        "packer_s_one_thread_first_layer": round(t_pack1, 3),
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(line))
+
+
+def cpu_baseline(Ws, Xs, fmt, M, seconds):
+    """The oracle as it stands, on this host: activation quantization plus the
+    fp64 decomposed product of every layer, repeated for about `seconds`."""
+    from oracle import sdq as S
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    cfg_o = S.config_from(fmt)
+    # bound the sample: at most 64 tokens per layer
+    ms = min(M, 64)
+    packs = [S.pack_logical(W, cfg_o) for W in Ws]  # offline stage, not timed
+    reps, t, flops = 0, 0.0, 0.0
+    while t < seconds or reps == 0:
+        t0 = time.perf_counter()
+        for X, Lg in zip(Xs, packs):
+            Xq, s_a = S.quantize_act(X[:ms], cfg_o)
+            S.gemm_fp64(Xq, s_a, Lg)
+            flops += 2.0 * ms * Lg["N"] * Lg["K"]
+        t += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(flops / t / 1e12, 8), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reps} repetitions of numpy quantize_act + fp64 gemm over {len(Ws)} layer(s) "
+                      f"at {ms} token(s), {t:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,202 @@
+/*
+ * sdq.h -- C ABI of the SDQ decomposed linear-layer GEMM for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * SDQ (Sparse Decomposed Quantization; Jeong, Tsai, Keckler, Krishna) splits
+ * every weight matrix W[N,K] of a linear layer into two structured-sparse
+ * parts (Section 5, Stages 1-3):
+ *   W_o  n_o:m_o outliers ("local outliers" of Section 4) at 8 bits,
+ *   W_i  n_i:m_i inliers at 4 bits with per-vector (VS-Quant) scales,
+ * quantizes the activations per token, and computes the layer as the sum of
+ * the two sparse products (Section 5.1):
+ *   Y[m,n] = s_a[m] * sum_k Xq[m,k] * (deq W_o[n,k] + deq W_i[n,k]).
+ *
+ * Conventions shared by every entry point
+ *   - W is [N, K] row-major (row n = output feature, K = reduction), X and Xq
+ *     are [M, K] row-major, Y is [M, N] row-major fp32.
+ *   - N:M groups and scale blocks run along K inside one row of W.
+ *   - Every function returns an sdq_status (0 = SDQ_OK, negative = error).
+ *     Nothing throws, aborts or prints (unless SDQ_LOG=1 is set, which prints
+ *     the kernel chosen by sdq_gemm to stderr).
+ *   - Argument errors (NULL pointers, shapes, configurations, buffer sizes)
+ *     are detected before any GPU work and returned synchronously.
+ *   - The caller owns every buffer.  Device entry points allocate no memory
+ *     (host or device) and can be captured in a HIP graph; the host packer
+ *     uses only its worker threads and K floats of scratch per thread.  The
+ *     library keeps no mutable global state.
+ *   - Device entry points take device pointers and a stream (a hipStream_t
+ *     passed as void*; NULL = the default stream), enqueue their kernels on
+ *     that stream and return without synchronizing.  A launch failure is
+ *     reported as SDQ_ERR_HIP; a fault inside a kernel surfaces at the
+ *     caller's next synchronization.
+ *   - Host entry points (pack, logical pack, unpack) take host pointers and
+ *     are deterministic: the output does not depend on the thread count.
+ */
+#ifndef SDQ_H_
+#define SDQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SDQ_OK = 0,
+  SDQ_ERR_NULL = -1,             /* a required pointer is NULL                 */
+  SDQ_ERR_SHAPE = -2,            /* M, N or K out of range / not divisible     */
+  SDQ_ERR_CONFIG = -3,           /* malformed sdq_config                       */
+  SDQ_ERR_BUFFER_TOO_SMALL = -4, /* output buffer smaller than required        */
+  SDQ_ERR_HIP = -5,              /* a HIP call or kernel launch failed         */
+  SDQ_ERR_UNSUPPORTED = -6,      /* well-formed but not implemented            */
+  SDQ_ERR_VALUE = -7             /* input value out of range (e.g. non-finite) */
+} sdq_status;
+
+/* Format families.
+ *  SDQ_FAMILY_INT: activations int8 per token (fp32 scale); outliers fp8-e4m3
+ *    or int8 with one fp32 scale per row of W; inliers int4 in [-7, 7] with one
+ *    fp16 scale per 16 consecutive K positions of a row.
+ *  SDQ_FAMILY_MX: activations fp8-e4m3 per token (fp32 scale); outliers
+ *    fp8-e4m3 and inliers fp4-e2m1, each branch with one e8m0 (power of two)
+ *    scale per 32 consecutive K positions of a row (OCP MX shared exponents).
+ */
+enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1 };
+enum { SDQ_FMT_INT8 = 1, SDQ_FMT_INT4 = 2, SDQ_FMT_E4M3 = 3, SDQ_FMT_E2M1 = 4 };
+enum { SDQ_METRIC_MAGNITUDE = 0, SDQ_METRIC_PRODUCT = 1 };
+enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
+/* sdq_gemm_ex kernel choice. */
+enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2 };
+
+/* One SDQ configuration (the paper's SDQ-k:m-n_o:m{fmt}-n_i:m{fmt} naming,
+ * Section 6 "Methodology", restricted to what the kernels implement):
+ *   family  SDQ_FAMILY_INT | SDQ_FAMILY_MX
+ *   n_o:m_o outlier sparsity, n_o in {0, 1}, m_o in {8, 16} (n_o = 0: none)
+ *   fmt_o   INT: SDQ_FMT_E4M3 | SDQ_FMT_INT8;  MX: SDQ_FMT_E4M3
+ *   n_i:m_i inlier sparsity, n_i in {1, 2, 3}, m_i = 8
+ *   fmt_i   INT: SDQ_FMT_INT4;  MX: SDQ_FMT_E2M1
+ *   fmt_a   INT: SDQ_FMT_INT8;  MX: SDQ_FMT_E4M3
+ *   metric  significance used to pick outliers and inliers (Section 5,
+ *           Stages 1-2): |W| (SDQ_METRIC_MAGNITUDE) or |W| * act_norm[k]
+ *           (SDQ_METRIC_PRODUCT, Wanda's weight-activation product). */
+typedef struct {
+  int32_t family;
+  int32_t n_o, m_o, fmt_o;
+  int32_t n_i, m_i, fmt_i;
+  int32_t fmt_a;
+  int32_t metric;
+} sdq_config;
+
+/* Static description of an error code (never NULL). */
+const char* sdq_status_string(sdq_status s);
+
+/* Validate a configuration for a W of shape [N, K].  K must be a positive
+ * multiple of 128 and N positive.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
+ * SDQ_ERR_UNSUPPORTED without touching anything else. */
+sdq_status sdq_check(const sdq_config* cfg, int64_t N, int64_t K);
+
+/* Size in bytes of the packed (physical) weight blob that sdq_pack writes. */
+sdq_status sdq_pack_size(const sdq_config* cfg, int64_t N, int64_t K, size_t* bytes);
+
+/* Algorithmic size in bytes of the decomposed layer in the paper's logical
+ * ELLPACK-like form (Section 3.3): per branch n values and n log2(m)-bit
+ * indices per m weights, plus the scales.  This is the byte count that
+ * throughput figures are quoted against; the physical blob may be larger. */
+sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t* bytes);
+
+/* Offline pack (Section 5, Stages 1-3), on the host.
+ *   W         host, [N, K] fp32 row-major, finite values
+ *   act_norm  host, [K] fp32 (per-input-channel activation norm), required
+ *             for SDQ_METRIC_PRODUCT and ignored otherwise (may be NULL)
+ *   packed    host, caller-owned, at least sdq_pack_size() bytes; copy it to
+ *             the device unchanged before calling sdq_gemm
+ *   n_threads host threads to use (<= 0: one per hardware thread)
+ * Selection: in every m_o-group the n_o most significant positions are the
+ * outliers; in every m_i-group the n_i most significant remaining positions
+ * are the inliers; the rest are pruned.  Ties go to the lower k.
+ * Quantization (IEEE fp32 arithmetic, round-to-nearest-even):
+ *   INT outliers: s_o[n] = amax_row / qmax (qmax 127 or 448), q = enc(W / s_o)
+ *   INT inliers:  s = fp16(amax_block16 / 7), q = clamp(rne(W / s), -7, 7)
+ *   MX:           E = floor(log2 amax_block32) - emax (8 for e4m3, 2 for
+ *                 e2m1), q = enc(W / 2^E) saturating
+ *   an all-zero block gets a zero scale (E = -127) and zero codes.
+ * Returns SDQ_ERR_VALUE if W holds a non-finite value or an inlier scale
+ * overflows fp16. */
+sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
+                    const float* act_norm, void* packed, size_t bytes, int n_threads);
+
+/* The same selection and quantization as sdq_pack, returned in the logical
+ * form instead of the kernel layout (host, caller-owned arrays):
+ *   pos_o, code_o  uint8 [N][K/m_o][n_o]  positions within the group
+ *                  (ascending) and codes (e4m3 bits or int8 bits)
+ *   scale_o        INT: float [N];  MX: uint8 e8m0 [N][K/32]
+ *   pos_i, code_i  uint8 [N][K/m_i][n_i]  (int4 codes as int8 bits, e2m1
+ *                  codes as the low nibble)
+ *   scale_i        INT: uint16 fp16 bits [N][K/16];  MX: uint8 e8m0 [N][K/32]
+ * Any pointer for a branch with n = 0 may be NULL. */
+sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
+                            const float* act_norm, uint8_t* pos_o, uint8_t* code_o,
+                            void* scale_o, uint8_t* pos_i, uint8_t* code_i, void* scale_i,
+                            int n_threads);
+
+/* Decode a packed blob (host copy) back to dense code arrays: code_o_dense
+ * and code_i_dense are uint8 [N][K] holding each stored code at its position
+ * and 0 elsewhere; scale_o / scale_i as in sdq_pack_logical.  Used to check
+ * that the kernel layout round-trips. */
+sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed, size_t bytes,
+                            int64_t N, int64_t K, uint8_t* code_o_dense,
+                            uint8_t* code_i_dense, void* scale_o, void* scale_i);
+
+/* Per-token activation quantization (Section 5, Stage 3; the activations
+ * are quantized to match the weights).  For each row m:
+ *   a = max_k |X[m,k]|;  s_a[m] = a / qmax;  inv = qmax / a  (fp32 divides)
+ *   Xq[m,k] = enc(X[m,k] * inv)  (one fp32 multiply, then round to nearest
+ *   even: int8 clamps to [-127, 127], e4m3 saturates to +-448)
+ * A row with a == 0 gets s_a = 0 and zero codes.
+ *   X      device, [M, K] row-major, x_dtype SDQ_DTYPE_F32 or SDQ_DTYPE_BF16
+ *   Xq     device, [M, K] row-major, 1 byte per element (int8 for the INT
+ *          family, e4m3 bits for the MX family)
+ *   s_a    device, [M] fp32
+ * M = 0 is a no-op.  K must be a positive multiple of 128. */
+sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int32_t x_dtype,
+                            int64_t M, int64_t K, void* Xq, float* s_a, void* stream);
+
+/* The decomposed GEMM (Section 5.1):
+ *   Y[m,n] = s_a[m] * ( sum over outlier slots of Xq[m,k] * deq W_o[n,k]
+ *                     + sum over inlier slots  of Xq[m,k] * deq W_i[n,k] )
+ * with both branches accumulated in one fp32 accumulator per output.
+ *   Xq, s_a  device, as written by sdq_quantize_act for the same cfg
+ *   packed   device, the blob written by sdq_pack for the same cfg, N, K
+ *   Y        device, [M, N] fp32 row-major (overwritten)
+ * M = 0 is a no-op.  The result is deterministic (no atomics). */
+sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                    const void* packed, int64_t N, int64_t K, float* Y, void* stream);
+
+/* sdq_gemm with an explicit kernel choice: SDQ_PATH_DECODE (weight-streaming
+ * vector kernel, INT family, any M up to 8), SDQ_PATH_MFMA (matrix-core
+ * kernels, any M) or SDQ_PATH_AUTO (what sdq_gemm does).  Returns
+ * SDQ_ERR_UNSUPPORTED for a path that does not serve the configuration. */
+sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                       const void* packed, int64_t N, int64_t K, float* Y, void* stream,
+                       int32_t path);
+
+/* Activation quantization and the decomposed GEMM in one call: the same
+ * results as sdq_quantize_act followed by sdq_gemm (Xq, s_a and Y are
+ * identical bit for bit).  Where sdq_gemm would take the decode path (INT
+ * family, small M) this is a single kernel in which every workgroup quantizes
+ * the activations into LDS itself; otherwise it enqueues the two kernels.
+ *   X       device, [M, K] fp32 or bf16 (x_dtype)
+ *   Xq, s_a device, outputs as in sdq_quantize_act (always written)
+ *   packed  device, as in sdq_gemm;  Y device, [M, N] fp32 (overwritten) */
+sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int64_t M,
+                      void* Xq, float* s_a, const void* packed, int64_t N, int64_t K, float* Y,
+                      void* stream);
+
+/* The path sdq_gemm takes for this configuration and M (SDQ_PATH_DECODE or
+ * SDQ_PATH_MFMA). */
+sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K, int32_t* path);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SDQ_H_ */

@@ -1,0 +1,213 @@
+"""SDQ (Sparse Decomposed Quantization) decomposed GEMM for MI355X (gfx950).
+
+Thin Python binding over ``libsdq.so`` (C ABI in ``include/sdq.h``): it only
+marshals arguments.  Every step of the hot path (activation quantization and
+the decomposed product) runs in the library's HIP kernels; PyTorch provides
+device memory and the current stream, nothing else.  There is no CPU
+fallback: if the library is missing every call raises.
+
+    cfg = Config.int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3)
+    blob = pack(W, cfg)                      # host numpy, offline (Section 5)
+    packed = torch.from_numpy(blob).cuda()
+    Xq, s_a = quantize_act(X_cuda, cfg)      # per-token activation quantization
+    Y = gemm(Xq, s_a, packed, N, K, cfg)     # Y = s_a * Xq (W_o + W_i)^T (Section 5.1)
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+from typing import Dict, Optional
+
+import numpy as np
+
+from . import _lib
+from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_INT, FAMILY_MX, FMT_E2M1, FMT_E4M3, FMT_INT4,
+                   FMT_INT8, METRIC_MAGNITUDE, METRIC_PRODUCT, PATH_AUTO, PATH_DECODE, PATH_MFMA,
+                   SDQError)
+
+__all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
+           "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
+           "PATH_MFMA", "check"]
+
+_FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    family: str = "int"      # "int" | "mx"
+    n_o: int = 1
+    m_o: int = 8
+    fmt_o: str = "e4m3"      # "e4m3" | "int8"
+    n_i: int = 3
+    m_i: int = 8
+    fmt_i: str = "int4"      # "int4" | "e2m1"
+    fmt_a: str = "int8"      # "int8" | "e4m3"
+    metric: str = "magnitude"  # "magnitude" | "product"
+
+    @staticmethod
+    def int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, metric="magnitude") -> "Config":
+        return Config("int", n_o, m_o, fmt_o, n_i, 8, "int4", "int8", metric)
+
+    @staticmethod
+    def mx_family(n_o=1, m_o=8, n_i=2, metric="magnitude") -> "Config":
+        return Config("mx", n_o, m_o, "e4m3", n_i, 8, "e2m1", "e4m3", metric)
+
+    @staticmethod
+    def of(fmt, metric: str = "magnitude") -> "Config":
+        """From any object with the same field names (e.g. a workload format)."""
+        return Config(fmt.family, fmt.n_o, fmt.m_o, fmt.fmt_o, fmt.n_i, fmt.m_i, fmt.fmt_i,
+                      fmt.fmt_a, metric)
+
+    @property
+    def mx(self) -> bool:
+        return self.family == "mx"
+
+    def c(self) -> _lib.sdq_config:
+        return _lib.sdq_config(FAMILY_MX if self.mx else FAMILY_INT, self.n_o, self.m_o,
+                               _FMT[self.fmt_o], self.n_i, self.m_i, _FMT[self.fmt_i],
+                               _FMT[self.fmt_a],
+                               METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE)
+
+
+def _p(a) -> C.c_void_p:
+    return C.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def check(cfg: Config, N: int, K: int) -> None:
+    _lib.check(_lib.lib().sdq_check(C.byref(cfg.c()), N, K), "sdq_check")
+
+
+def pack_size(cfg: Config, N: int, K: int) -> int:
+    n = C.c_size_t()
+    _lib.check(_lib.lib().sdq_pack_size(C.byref(cfg.c()), N, K, C.byref(n)), "sdq_pack_size")
+    return n.value
+
+
+def logical_bytes(cfg: Config, N: int, K: int) -> int:
+    n = C.c_size_t()
+    _lib.check(_lib.lib().sdq_logical_bytes(C.byref(cfg.c()), N, K, C.byref(n)),
+               "sdq_logical_bytes")
+    return n.value
+
+
+def pack(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = None,
+         n_threads: int = 0) -> np.ndarray:
+    """Offline decomposition + quantization into the kernel layout (host)."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    N, K = W.shape
+    an = None if act_norm is None else np.ascontiguousarray(act_norm, dtype=np.float32)
+    out = np.empty(pack_size(cfg, N, K), dtype=np.uint8)
+    _lib.check(_lib.lib().sdq_pack(C.byref(cfg.c()), _p(W), N, K, _p(an), _p(out), out.nbytes,
+                                   n_threads), "sdq_pack")
+    return out
+
+
+def pack_logical(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = None,
+                 n_threads: int = 0) -> Dict[str, np.ndarray]:
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    N, K = W.shape
+    an = None if act_norm is None else np.ascontiguousarray(act_norm, dtype=np.float32)
+    no = max(cfg.n_o, 0)
+    pos_o = np.zeros((N, K // cfg.m_o, no), np.uint8)
+    code_o = np.zeros((N, K // cfg.m_o, no), np.uint8)
+    pos_i = np.zeros((N, K // cfg.m_i, cfg.n_i), np.uint8)
+    code_i = np.zeros((N, K // cfg.m_i, cfg.n_i), np.uint8)
+    if cfg.mx:
+        scale_o = np.zeros((N, K // 32), np.uint8)
+        scale_i = np.zeros((N, K // 32), np.uint8)
+    else:
+        scale_o = np.zeros(N, np.float32)
+        scale_i = np.zeros((N, K // 16), np.uint16)
+    _lib.check(_lib.lib().sdq_pack_logical(
+        C.byref(cfg.c()), _p(W), N, K, _p(an), _p(pos_o), _p(code_o), _p(scale_o), _p(pos_i),
+        _p(code_i), _p(scale_i), n_threads), "sdq_pack_logical")
+    return dict(pos_o=pos_o, code_o=code_o, scale_o=scale_o, pos_i=pos_i, code_i=code_i,
+                scale_i=scale_i)
+
+
+def unpack_dense(blob: np.ndarray, cfg: Config, N: int, K: int) -> Dict[str, np.ndarray]:
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    co = np.zeros((N, K), np.uint8)
+    ci = np.zeros((N, K), np.uint8)
+    if cfg.mx:
+        so, si = np.zeros((N, K // 32), np.uint8), np.zeros((N, K // 32), np.uint8)
+    else:
+        so, si = np.zeros(N, np.float32), np.zeros((N, K // 16), np.uint16)
+    _lib.check(_lib.lib().sdq_unpack_dense(C.byref(cfg.c()), _p(blob), blob.nbytes, N, K, _p(co),
+                                           _p(ci), _p(so), _p(si)), "sdq_unpack_dense")
+    return dict(code_o_dense=co, code_i_dense=ci, scale_o=so, scale_i=si)
+
+
+# ----------------------------------------------------------------- device side
+def _stream(stream) -> C.c_void_p:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dev(t, what: str):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous CUDA (HIP) tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
+    """Per-token activation quantization on the GPU: returns (Xq uint8, s_a f32)."""
+    import torch
+    M, K = X.shape
+    if X.dtype == torch.float32:
+        dt = DTYPE_F32
+    elif X.dtype == torch.bfloat16:
+        dt = DTYPE_BF16
+    else:
+        raise ValueError("X must be float32 or bfloat16")
+    Xq = out if out is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
+    s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
+    _lib.check(_lib.lib().sdq_quantize_act(C.byref(cfg.c()), _dev(X, "X"), dt, M, K,
+                                           _dev(Xq, "Xq"), _dev(s_a, "s_a"), _stream(stream)),
+               "sdq_quantize_act")
+    return Xq, s_a
+
+
+def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PATH_AUTO,
+         stream=None):
+    """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 output)."""
+    import torch
+    M = Xq.shape[0]
+    if Xq.shape[1] != K:
+        raise ValueError("Xq has the wrong K")
+    if packed.numel() < pack_size(cfg, N, K):
+        raise ValueError("packed buffer too small")
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=Xq.device)
+    _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
+                                      _dev(packed, "packed"), N, K, _dev(Y, "Y"), _stream(stream),
+                                      path), "sdq_gemm")
+    return Y
+
+
+def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=None, stream=None):
+    """Quantize X per token and multiply: returns (Y, Xq, s_a).  One fused
+    kernel on the decode path; otherwise the two kernels back to back."""
+    import torch
+    M = X.shape[0]
+    if X.shape[1] != K:
+        raise ValueError("X has the wrong K")
+    if X.dtype == torch.float32:
+        dt = DTYPE_F32
+    elif X.dtype == torch.bfloat16:
+        dt = DTYPE_BF16
+    else:
+        raise ValueError("X must be float32 or bfloat16")
+    Xq = xq if xq is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
+    s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=X.device)
+    _lib.check(_lib.lib().sdq_linear(C.byref(cfg.c()), _dev(X, "X"), dt, M, _dev(Xq, "Xq"),
+                                     _dev(s_a, "s_a"), _dev(packed, "packed"), N, K, _dev(Y, "Y"),
+                                     _stream(stream)), "sdq_linear")
+    return Y, Xq, s_a
+
+
+def gemm_path(cfg: Config, M: int, N: int, K: int) -> int:
+    p = C.c_int32()
+    _lib.check(_lib.lib().sdq_gemm_path(C.byref(cfg.c()), M, N, K, C.byref(p)), "sdq_gemm_path")
+    return p.value

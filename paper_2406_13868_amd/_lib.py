@@ -1,0 +1,81 @@
+"""ctypes view of libsdq.so (declarations in include/sdq.h)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsdq.so")
+
+SDQ_OK = 0
+STATUS = {
+    0: "SDQ_OK", -1: "SDQ_ERR_NULL", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_CONFIG",
+    -4: "SDQ_ERR_BUFFER_TOO_SMALL", -5: "SDQ_ERR_HIP", -6: "SDQ_ERR_UNSUPPORTED",
+    -7: "SDQ_ERR_VALUE",
+}
+FAMILY_INT, FAMILY_MX = 0, 1
+FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
+METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
+DTYPE_F32, DTYPE_BF16 = 0, 1
+PATH_AUTO, PATH_DECODE, PATH_MFMA = 0, 1, 2
+
+# Every exported symbol, as declared in include/sdq.h.
+EXPORTS = (
+    "sdq_status_string", "sdq_check", "sdq_pack_size", "sdq_logical_bytes", "sdq_pack",
+    "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
+    "sdq_gemm_path", "sdq_linear",
+)
+
+
+class sdq_config(C.Structure):
+    _fields_ = [("family", C.c_int32), ("n_o", C.c_int32), ("m_o", C.c_int32),
+                ("fmt_o", C.c_int32), ("n_i", C.c_int32), ("m_i", C.c_int32),
+                ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32)]
+
+
+class SDQError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {STATUS.get(status, status)}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load libsdq.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2406_13868_amd.build` (no CPU fallback exists)")
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        cfgp = P(sdq_config)
+        i64, vp, f32p, u8p = C.c_int64, C.c_void_p, P(C.c_float), P(C.c_uint8)
+        sig = {
+            "sdq_status_string": (C.c_char_p, [C.c_int]),
+            "sdq_check": (C.c_int, [cfgp, i64, i64]),
+            "sdq_pack_size": (C.c_int, [cfgp, i64, i64, P(C.c_size_t)]),
+            "sdq_logical_bytes": (C.c_int, [cfgp, i64, i64, P(C.c_size_t)]),
+            "sdq_pack": (C.c_int, [cfgp, vp, i64, i64, vp, vp, C.c_size_t, C.c_int]),
+            "sdq_pack_logical": (C.c_int, [cfgp, vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, C.c_int]),
+            "sdq_unpack_dense": (C.c_int, [cfgp, vp, C.c_size_t, i64, i64, vp, vp, vp, vp]),
+            "sdq_quantize_act": (C.c_int, [cfgp, vp, C.c_int32, i64, i64, vp, vp, vp]),
+            "sdq_gemm": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp]),
+            "sdq_gemm_ex": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),
+            "sdq_gemm_path": (C.c_int, [cfgp, i64, i64, i64, P(C.c_int32)]),
+            "sdq_linear": (C.c_int, [cfgp, vp, C.c_int32, i64, vp, vp, vp, i64, i64, vp, vp]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        del u8p, f32p
+        _lib = L
+    return _lib
+
+
+def check(status: int, what: str) -> None:
+    if status != SDQ_OK:
+        raise SDQError(status, what)

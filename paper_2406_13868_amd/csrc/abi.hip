@@ -1,0 +1,137 @@
+// C ABI of libsdq: argument validation and kernel dispatch (see include/sdq.h).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+
+#include "kernels.h"
+
+using namespace sdq;
+
+namespace {
+
+bool log_enabled() {
+  static const bool on = [] {
+    const char* e = std::getenv("SDQ_LOG");
+    return e && e[0] == '1';
+  }();
+  return on;
+}
+
+int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
+  if (!c.mx && M <= 2 && decode_fits(M, K)) return SDQ_PATH_DECODE;
+  return SDQ_PATH_MFMA;
+}
+
+}  // namespace
+
+extern "C" const char* sdq_status_string(sdq_status s) {
+  switch (s) {
+    case SDQ_OK: return "SDQ_OK: success";
+    case SDQ_ERR_NULL: return "SDQ_ERR_NULL: a required pointer is NULL";
+    case SDQ_ERR_SHAPE: return "SDQ_ERR_SHAPE: M, N or K out of range or K not a multiple of 128";
+    case SDQ_ERR_CONFIG: return "SDQ_ERR_CONFIG: malformed configuration";
+    case SDQ_ERR_BUFFER_TOO_SMALL: return "SDQ_ERR_BUFFER_TOO_SMALL: output buffer too small";
+    case SDQ_ERR_HIP: return "SDQ_ERR_HIP: a HIP call or kernel launch failed";
+    case SDQ_ERR_UNSUPPORTED: return "SDQ_ERR_UNSUPPORTED: configuration or path not implemented";
+    case SDQ_ERR_VALUE: return "SDQ_ERR_VALUE: input value out of range";
+  }
+  return "unknown sdq_status";
+}
+
+extern "C" sdq_status sdq_check(const sdq_config* cfg, int64_t N, int64_t K) {
+  return check_config(cfg, N, K, nullptr);
+}
+
+extern "C" sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int32_t x_dtype,
+                                       int64_t M, int64_t K, void* Xq, float* s_a, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, 1, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31)) return SDQ_ERR_SHAPE;
+  if (x_dtype != SDQ_DTYPE_F32 && x_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
+  if (M == 0) return SDQ_OK;
+  if (!X || !Xq || !s_a) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq) % 16) return SDQ_ERR_SHAPE;
+  const hipError_t e = launch_act_quant(c, X, x_dtype, M, K, static_cast<uint8_t*>(Xq), s_a,
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
+                                    int32_t* path) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!path) return SDQ_ERR_NULL;
+  if (M < 0) return SDQ_ERR_SHAPE;
+  *path = auto_path(c, M, K);
+  return SDQ_OK;
+}
+
+extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a,
+                                  int64_t M, const void* packed, int64_t N, int64_t K, float* Y,
+                                  void* stream, int32_t path) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (path != SDQ_PATH_AUTO && path != SDQ_PATH_DECODE && path != SDQ_PATH_MFMA) return SDQ_ERR_CONFIG;
+  if (M == 0) return SDQ_OK;
+  if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16)
+    return SDQ_ERR_SHAPE;
+  if (path == SDQ_PATH_AUTO) path = auto_path(c, M, K);
+  if (path == SDQ_PATH_DECODE && (c.mx || !decode_fits(M, K))) return SDQ_ERR_UNSUPPORTED;
+  const auto* xq = static_cast<const uint8_t*>(Xq);
+  const auto* blob = static_cast<const uint8_t*>(packed);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  const char* name;
+  if (c.mx) {
+    e = launch_mx_mfma(c, xq, s_a, M, blob, N, K, Y, st);
+    name = "mx_mfma";
+  } else if (path == SDQ_PATH_DECODE) {
+    e = launch_int_decode(c, xq, s_a, M, blob, N, K, Y, st);
+    name = "int_decode";
+  } else {
+    e = launch_int_mfma(c, xq, s_a, M, blob, N, K, Y, st);
+    name = "int_mfma";
+  }
+  if (log_enabled())
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s\n", (long long)M, (long long)N,
+                 (long long)K, name);
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                               const void* packed, int64_t N, int64_t K, float* Y, void* stream) {
+  return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, SDQ_PATH_AUTO);
+}
+
+extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int64_t M,
+                                 void* Xq, float* s_a, const void* packed, int64_t N, int64_t K,
+                                 float* Y, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (x_dtype != SDQ_DTYPE_F32 && x_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
+  if (M == 0) return SDQ_OK;
+  if (!X || !Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq) % 16 ||
+      reinterpret_cast<uintptr_t>(packed) % 16)
+    return SDQ_ERR_SHAPE;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (auto_path(c, M, K) == SDQ_PATH_DECODE && decode_fused_fits(M, K)) {
+    const hipError_t e = launch_int_decode_fused(c, X, x_dtype, M, static_cast<uint8_t*>(Xq), s_a,
+                                                 static_cast<const uint8_t*>(packed), N, K, Y, st);
+    if (log_enabled())
+      std::fprintf(stderr, "[sdq] linear M=%lld N=%lld K=%lld -> int_decode (fused act quant)\n",
+                   (long long)M, (long long)N, (long long)K);
+    return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+  }
+  const sdq_status q = sdq_quantize_act(cfg, X, x_dtype, M, K, Xq, s_a, stream);
+  if (q != SDQ_OK) return q;
+  return sdq_gemm(cfg, Xq, s_a, M, packed, N, K, Y, stream);
+}

@@ -1,0 +1,219 @@
+// MX-family decomposed GEMM on the matrix cores (any M).  Section 5.1:
+// Y = SpMM(A, W_o) + SpMM(A, W_i), both branches accumulated by the matrix
+// core itself into one fp32 accumulator per output.
+//
+// gfx950's v_mfma_scale_f32_32x32x64_f8f6f4 multiplies fp8 activations by
+// fp8 or fp4 weights and applies an e8m0 scale to every 32 K of each weight
+// column inside the instruction, which is exactly the MX form of both
+// branches:
+//   acc += Xq(e4m3) * W_o(e4m3, 2^Eo per 32 K)      fp8 x fp8
+//   acc += Xq(e4m3) * W_i(e2m1, 2^Ei per 32 K)      fp8 x fp4
+//   Y = s_a * acc
+// The products are exact and accumulate in fp32.
+//
+// Operand layouts (32x32x64, lane l, lane half h = l/32, column/row l%32):
+//   fp8 operand: byte i of the 8 dwords holds K = 32*(i/16) + 16*h + i%16
+//   fp4 operand: nibble i of the first 4 dwords holds K = 32*h + i
+//   scale:       lane half h supplies the scale of K block [32h, 32h+32)
+// A lane reads the four group words of one 32-K block (the fp4 order); the
+// fp8 order needs two of them from the other lane half, exchanged with
+// v_permlane32_swap.
+//
+// Tiling: a workgroup of 4 waves owns 4 row tiles of W (128 outputs) and BM
+// = 32*MS tokens; fp8 activations are staged per 128-K chunk in LDS (double
+// buffered) and shared by the 4 waves; weights stream from HBM into
+// registers and are expanded there into dense fp8 / fp4 fragments.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace sdq {
+namespace {
+
+typedef int i8v __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kLdsRow = kChunkK + 16;  // bytes per LDS row (padding against bank conflicts)
+constexpr uint32_t kOutPosMagic = (1u << 21) | (1u << 14) | (1u << 7);
+
+struct MxArgs {
+  const uint8_t* Xq;
+  const float* s_a;
+  const uint8_t* blob;
+  float* Y;
+  int M, N, K, n_chunks, n_tiles;
+  int64_t scales_off;
+};
+
+// Dense e2m1 nibbles (position p at nibble p) of one group word.
+template <int NI>
+__device__ __forceinline__ uint32_t inlier_fp4(uint32_t w) {
+  uint32_t D = 0;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const uint32_t q = (w >> (8 * j + 4)) & 0xFu;
+    const uint32_t sh = ((w >> (8 * j)) & 7u) << 2;
+    D |= q << sh;
+  }
+  return D;
+}
+
+// Dense e4m3 bytes (position p at byte p of lo:hi) of one group word.
+__device__ __forceinline__ void outlier_fp8(uint32_t w, uint32_t& lo, uint32_t& hi) {
+  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
+  const uint32_t v = (w >> 24) << ((pos & 3u) << 3);
+  lo = pos < 4u ? v : 0u;
+  hi = pos < 4u ? 0u : v;
+}
+
+template <int MS, int NI, bool HAS_O>
+__global__ __launch_bounds__(kThreads) void mx_mfma_kernel(MxArgs a) {
+  constexpr int BM = 32 * MS;
+  __shared__ __align__(16) uint8_t xs[2][BM * kLdsRow];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, h = lane >> 5;
+  const int m0 = blockIdx.y * BM;
+  const int tile = blockIdx.x * kWaves + wave;
+  const bool tile_ok = tile < a.n_tiles;
+  const int KC = a.n_chunks;
+
+  constexpr int kPieces = BM * 8;  // 16-byte pieces per chunk of activations
+  constexpr int kPerThread = (kPieces + kThreads - 1) / kThreads;
+  uint4 xr[kPerThread];
+  auto load_x = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int pc = tid + i * kThreads;
+      const int rr = pc >> 3, cp = pc & 7;
+      xr[i] = make_uint4(0, 0, 0, 0);
+      if (pc < kPieces && m0 + rr < a.M)
+        xr[i] = *reinterpret_cast<const uint4*>(a.Xq + size_t(m0 + rr) * a.K + c * kChunkK + cp * 16);
+    }
+  };
+  auto store_x = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int pc = tid + i * kThreads;
+      if (pc >= kPieces) continue;
+      const int rr = pc >> 3, cp = pc & 7;
+      *reinterpret_cast<uint4*>(&xs[buf][rr * kLdsRow + cp * 16]) = xr[i];
+    }
+  };
+
+  const uint8_t* wbase = a.blob + size_t(tile_ok ? tile : 0) * KC * kWordBytesPerTC + size_t(lane) * 16;
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kMxScaleBytesPerTC + lane * 4;
+  uint4 wr0, wr1;
+  uint32_t sr;
+  auto load_w = [&](int c) {
+    if (tile_ok) {
+      wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
+      wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 1024);
+      sr = *reinterpret_cast<const uint32_t*>(sbase + size_t(c) * kMxScaleBytesPerTC);
+    } else {
+      wr0 = wr1 = make_uint4(0, 0, 0, 0);
+      sr = 0;
+    }
+  };
+
+  f16v acc[MS];
+#pragma unroll
+  for (int s = 0; s < MS; ++s)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
+
+  load_x(0);
+  load_w(0);
+  store_x(0);
+  __syncthreads();
+
+  for (int c = 0; c < KC; ++c) {
+    const int buf = c & 1;
+    const uint4 wq[2] = {wr0, wr1};
+    const uint32_t scl = sr;
+    if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {  // two 64-K steps per chunk
+      uint32_t w[4] = {wq[s].x, wq[s].y, wq[s].z, wq[s].w};
+      i8v bi, bo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bi[i] = int(inlier_fp4<NI>(w[i]));
+#pragma unroll
+      for (int i = 4; i < 8; ++i) bi[i] = 0;
+      if constexpr (HAS_O) {
+        // fp8 order: lane half 0 needs groups {0,1,4,5}, half 1 {2,3,6,7} of the step
+        auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+        auto s13 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+        const uint32_t u[4] = {s02[0], s13[0], s02[1], s13[1]};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint32_t lo, hi;
+          outlier_fp8(u[i], lo, hi);
+          bo[2 * i] = int(lo);
+          bo[2 * i + 1] = int(hi);
+        }
+      }
+      const int eo = int((scl >> (16 * s)) & 0xFFu);
+      const int ei = int((scl >> (16 * s + 8)) & 0xFFu);
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        const uint8_t* ap = &xs[buf][(ms * 32 + col) * kLdsRow + s * 64 + h * 16];
+        const uint4 a0 = *reinterpret_cast<const uint4*>(ap);
+        const uint4 a1 = *reinterpret_cast<const uint4*>(ap + 32);
+        const i8v av = {int(a0.x), int(a0.y), int(a0.z), int(a0.w),
+                        int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
+        if constexpr (HAS_O)
+          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bo, acc[ms], 0, 0, 0, 127, 0, eo);
+        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bi, acc[ms], 0, 4, 0, 127, 0, ei);
+      }
+    }
+    if (c + 1 < KC) {
+      store_x(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  if (!tile_ok) return;
+  const int n = tile * kTileN + col;
+  if (n >= a.N) return;
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + ms * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+      if (m < a.M) a.Y[size_t(m) * a.N + n] = a.s_a[m] * acc[ms][e];
+    }
+}
+
+template <int MS, int NI>
+hipError_t launch_ms_ni(const Cfg& c, const MxArgs& a, hipStream_t st) {
+  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
+  const dim3 block(kThreads);
+  if (c.n_o)
+    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, true>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, false>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+template <int MS>
+hipError_t launch_ms(const Cfg& c, const MxArgs& a, hipStream_t st) {
+  if (c.n_i == 1) return launch_ms_ni<MS, 1>(c, a, st);
+  if (c.n_i == 2) return launch_ms_ni<MS, 2>(c, a, st);
+  return launch_ms_ni<MS, 3>(c, a, st);
+}
+
+}  // namespace
+
+hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                          const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
+  const Layout L = make_layout(true, N, K);
+  MxArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles), L.scales_off};
+  if (M <= 32) return launch_ms<1>(c, a, st);
+  if (M <= 64) return launch_ms<2>(c, a, st);
+  return launch_ms<4>(c, a, st);
+}
+
+}  // namespace sdq

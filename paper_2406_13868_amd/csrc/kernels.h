@@ -1,0 +1,38 @@
+// Kernel launchers of libsdq (device side).  Shapes and configurations are
+// validated by the C ABI before any of these is called.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "layout.h"
+#include "sdq_internal.h"
+
+namespace sdq {
+
+hipError_t launch_act_quant(const Cfg& c, const void* X, int x_dtype, int64_t M, int64_t K,
+                            uint8_t* Xq, float* s_a, hipStream_t st);
+
+// INT family, weight-streaming vector kernel (small M).
+constexpr int kDecodeMaxM = 8;
+hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                             const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+// Same kernel with the per-token activation quantization fused in front: every
+// workgroup quantizes X into LDS; workgroup 0 also writes Xq and s_a.
+hipError_t launch_int_decode_fused(const Cfg& c, const void* X, int x_dtype, int64_t M,
+                                   uint8_t* Xq_out, float* s_a_out, const uint8_t* blob, int64_t N,
+                                   int64_t K, float* Y, hipStream_t st);
+// Whether the decode kernel takes M tokens of width K (it keeps them in LDS),
+// and whether its fused form does.
+bool decode_fits(int64_t M, int64_t K);
+bool decode_fused_fits(int64_t M, int64_t K);
+
+// INT family, matrix-core kernel (any M).
+hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                           const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+
+// MX family, scaled matrix-core kernel (any M).
+hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                          const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+
+}  // namespace sdq

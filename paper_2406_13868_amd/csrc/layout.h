@@ -1,0 +1,93 @@
+// Physical layout of a packed SDQ weight blob, shared by the host packer and
+// the GPU kernels of this library.
+//
+// The blob is organised in tiles of 32 rows of W by chunks of 128 K.  For
+// every (tile t, chunk c), in this order:
+//
+//   section A  group words     512 x 32-bit   [t][c] (2 KiB)
+//   section B  block scales    INT: 512 B, MX: 256 B   [t][c]
+//   section C  row scales      INT only: fp32 [t][32]
+//
+// One 32-bit *group word* describes one 8-wide group (m_i = 8) of one row:
+//
+//   byte j (j = 0,1,2)  bits 0-2  position (0..7) of inlier slot j
+//                       bit  3    bit j of the position of the outlier
+//                       bits 4-7  code of inlier slot j (int4 two's
+//                                 complement, or an e2m1 code)
+//   byte 3              code of the outlier (e4m3 or int8 bits)
+//
+// Inlier slots are in ascending position order; an unused slot (n_i < 3) has
+// position 0 and code 0.  With 1:16 outliers the outlier lives in the word
+// of the 8-group that holds it; the other word of its 16-group has outlier
+// code 0 and position 0.  A zero code contributes nothing, so the position
+// of an unused slot never matters.
+//
+// This layout lets a lane turn one word into a v_perm_b32 byte selector
+// (positions in bits 0-2 of bytes 0-2 and 3 bits for byte 3), and keep the
+// inlier codes at the top of each byte, where an int8 view of the byte is
+// 16x the int4 value.
+//
+// Word order inside a (tile, chunk), with r the row inside the tile:
+//   INT family (16-K scale blocks):   g = 8*j + 2*q + h,  kb = 4*j + q
+//       word = ((h*32 + r)*2 + j)*4 + q          j,h in {0,1}, q in 0..3
+//     so the 16 bytes at ((h*32 + r)*2 + j)*16 are the groups
+//     {2*kb + h : kb = 4j..4j+3} of row r, and the words of four consecutive
+//     rows (both j) for one h form one 128-byte run.
+//   MX family (32-K scale blocks):    g = 4*b + i,  b = 2*s + h
+//       word = ((s*2 + h)*32 + r)*4 + i          s,h in {0,1}, i in 0..3
+//     so lane l = h*32 + r reads the four groups of 32-K block 2s+h of row r.
+//
+// Block scales inside a (tile, chunk):
+//   INT: fp16 scale of row r, 16-K block kb (0..7) at byte (r*8 + kb)*2
+//   MX:  e8m0 of row r, 32-K block b = 2s+h at byte ((h*32 + r)*2 + s)*2 + br
+//        with br = 0 for the outlier branch and 1 for the inlier branch
+//
+// Rows beyond N in the last tile are all-zero (codes and scales).
+#pragma once
+#include <cstddef>
+#include <cstdint>
+
+namespace sdq {
+
+constexpr int kTileN = 32;
+constexpr int kChunkK = 128;
+constexpr int kGroup = 8;
+constexpr int kWordsPerTC = kTileN * kChunkK / kGroup;            // 512
+constexpr int kWordBytesPerTC = kWordsPerTC * 4;                  // 2048
+constexpr int kIntScaleBytesPerTC = kTileN * (kChunkK / 16) * 2;  // 512
+constexpr int kMxScaleBytesPerTC = kTileN * (kChunkK / 32) * 2;   // 256
+
+struct Layout {
+  int64_t n_tiles = 0, n_chunks = 0;
+  int64_t words_off = 0, scales_off = 0, rows_off = 0, total = 0;
+  int scale_bytes_per_tc = 0;
+};
+
+inline Layout make_layout(bool mx, int64_t N, int64_t K) {
+  Layout L;
+  L.n_tiles = (N + kTileN - 1) / kTileN;
+  L.n_chunks = K / kChunkK;
+  L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : kIntScaleBytesPerTC;
+  L.words_off = 0;
+  L.scales_off = L.n_tiles * L.n_chunks * kWordBytesPerTC;
+  L.rows_off = L.scales_off + L.n_tiles * L.n_chunks * L.scale_bytes_per_tc;
+  L.total = L.rows_off + (mx ? 0 : L.n_tiles * kTileN * 4);
+  return L;
+}
+
+// Word index of group g (0..15 within the chunk) of tile row r.
+inline int int_word_index(int g, int r) {
+  const int kb = g >> 1, h = g & 1, j = kb >> 2, q = kb & 3;
+  return ((h * 32 + r) * 2 + j) * 4 + q;
+}
+inline int mx_word_index(int g, int r) {
+  const int b = g >> 2, i = g & 3, s = b >> 1, h = b & 1;
+  return ((s * 2 + h) * 32 + r) * 4 + i;
+}
+inline int int_scale_byte(int kb, int r) { return (r * 8 + kb) * 2; }
+inline int mx_scale_byte(int b, int r, int branch) {
+  const int s = b >> 1, h = b & 1;
+  return ((h * 32 + r) * 2 + s) * 2 + branch;
+}
+
+}  // namespace sdq

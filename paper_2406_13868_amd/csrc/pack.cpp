@@ -1,0 +1,488 @@
+// Offline SDQ packer (host): Section 5, Stages 1-3 of the paper.
+//
+//   Stage 1+2  In every m_o-group of a row the n_o most significant positions
+//              become the outliers (local outlier extraction, Section 4); in
+//              every 8-group the n_i most significant remaining positions
+//              become the inliers; everything else is pruned.  Significance
+//              is |w| or |w| * act_norm[k] (Wanda's product metric); ties go
+//              to the lower k.
+//   Stage 3    Per-vector quantization of each branch (VS-Quant style), with
+//              the formats of the configuration's family.
+//
+// Arithmetic is IEEE fp32 with round-to-nearest-even, in the order stated in
+// sdq.h, so that the result is reproducible bit for bit.  The packer writes
+// either the logical form (positions, codes, scales) or the kernel layout
+// described in layout.h.  Rows are independent; worker threads take
+// contiguous row ranges, so the output does not depend on the thread count.
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+#include "layout.h"
+#include "sdq_internal.h"
+
+namespace sdq {
+namespace {
+
+// ---------------------------------------------------------------- encoders
+// fp32 -> IEEE binary16 bits, round to nearest even.
+uint16_t f32_to_f16_bits(float f) {
+  uint32_t x;
+  std::memcpy(&x, &f, 4);
+  const uint32_t sign = (x >> 16) & 0x8000u;
+  const uint32_t ax = x & 0x7FFFFFFFu;
+  if (ax >= 0x7F800000u) return uint16_t(sign | 0x7C00u | (ax > 0x7F800000u ? 0x200u : 0u));
+  const int e = int(ax >> 23) - 127;  // unbiased exponent of the fp32 value
+  if (e > 15) return uint16_t(sign | 0x7C00u);  // overflow to infinity
+  uint32_t mant = (ax & 0x7FFFFFu) | 0x800000u;  // 24-bit significand (normal input)
+  if (ax < 0x00800000u) return uint16_t(sign);     // fp32 subnormal: far below fp16 range
+  int shift;                                        // bits to drop from the 24-bit significand
+  uint32_t exp_field;
+  if (e >= -14) {                                   // fp16 normal
+    shift = 13;
+    exp_field = uint32_t(e + 15);
+  } else {                                          // fp16 subnormal (or underflow)
+    shift = 13 + (-14 - e);
+    exp_field = 0;
+    if (shift > 24) return uint16_t(sign);
+  }
+  uint32_t q = mant >> shift;
+  const uint32_t rem = mant & ((1u << shift) - 1u);
+  const uint32_t half = 1u << (shift - 1);
+  if (rem > half || (rem == half && (q & 1u))) ++q;
+  uint32_t bits;
+  if (exp_field) {
+    bits = (exp_field << 10) + (q - 0x400u);  // q in [0x400, 0x800]; carry bumps the exponent
+  } else {
+    bits = q;  // subnormal; q == 0x400 rounds up into the smallest normal
+  }
+  if (bits >= 0x7C00u) bits = 0x7C00u;
+  return uint16_t(sign | bits);
+}
+
+float f16_bits_to_f32(uint16_t h) {
+  const uint32_t sign = uint32_t(h & 0x8000u) << 16;
+  const uint32_t e = (h >> 10) & 0x1F, m = h & 0x3FF;
+  float v;
+  if (e == 0) v = std::ldexp(float(m), -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = std::ldexp(float(m | 0x400u), int(e) - 25);
+  uint32_t b;
+  std::memcpy(&b, &v, 4);
+  b |= sign;
+  std::memcpy(&v, &b, 4);
+  return v;
+}
+
+// Nearest-even OCP fp8 E4M3FN code of x, saturating at +-448; keeps the sign.
+uint8_t enc_e4m3(double x) {
+  const uint8_t s = std::signbit(x) ? 0x80 : 0x00;
+  double a = std::fabs(x);
+  if (a > 448.0) a = 448.0;
+  if (a < 0.015625) {  // below 2^-6: subnormal spacing 2^-9
+    const int q = int(std::nearbyint(a * 512.0));  // 8 becomes the first normal code
+    return uint8_t(s | q);
+  }
+  int e;
+  const double f = std::frexp(a, &e);  // a = f * 2^e, f in [0.5, 1)
+  int E = e - 1;
+  int mq = int(std::nearbyint((2.0 * f - 1.0) * 8.0));
+  if (mq == 8) { ++E; mq = 0; }
+  return uint8_t(s | ((E + 7) << 3) | mq);
+}
+
+// Nearest-even OCP fp4 E2M1 code (low nibble), saturating at +-6; keeps the sign.
+uint8_t enc_e2m1(double x) {
+  const uint8_t s = std::signbit(x) ? 0x8 : 0x0;
+  double a = std::fabs(x);
+  if (a > 6.0) a = 6.0;
+  if (a < 1.0) return uint8_t(s | int(std::nearbyint(a * 2.0)));  // 0, 0.5, (1.0)
+  int e;
+  const double f = std::frexp(a, &e);
+  int E = e - 1;
+  int mq = int(std::nearbyint((2.0 * f - 1.0) * 2.0));
+  if (mq == 2) { ++E; mq = 0; }
+  return uint8_t(s | ((E + 1) << 1) | mq);
+}
+
+int floor_log2f(float a) {
+  int e;
+  std::frexp(a, &e);
+  return e - 1;
+}
+
+int clamp_int(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// The first n allowed positions of a group by (-S, k); returns a position mask.
+uint32_t top_n(const float* S, uint32_t allowed, int m, int n) {
+  float bs[16];
+  int bk[16];
+  int cnt = 0;
+  for (int p = 0; p < m; ++p) {
+    if (!((allowed >> p) & 1u)) continue;
+    const float s = S[p];
+    int pos = cnt;
+    while (pos > 0 && bs[pos - 1] < s) --pos;  // equal keys keep the earlier k
+    if (pos >= n) continue;
+    const int last = cnt < n ? cnt : n - 1;
+    for (int q = last; q > pos; --q) { bs[q] = bs[q - 1]; bk[q] = bk[q - 1]; }
+    bs[pos] = s;
+    bk[pos] = p;
+    if (cnt < n) ++cnt;
+  }
+  uint32_t mask = 0;
+  for (int i = 0; i < cnt; ++i) mask |= 1u << bk[i];
+  return mask;
+}
+
+// ---------------------------------------------------------------- one row
+// Everything the packer decides for one row of W.
+struct RowSink {
+  // logical outputs (any may be null)
+  uint8_t* pos_o; uint8_t* code_o; void* scale_o;
+  uint8_t* pos_i; uint8_t* code_i; void* scale_i;
+  // kernel layout output (may be null)
+  uint8_t* blob;
+  const Layout* lay;
+};
+
+// Packs row n.  `S` is scratch of K floats.
+sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t K, int64_t n,
+                    float* S, const RowSink& out) {
+  for (int64_t k = 0; k < K; ++k) {
+    if (!std::isfinite(w[k])) return SDQ_ERR_VALUE;
+    S[k] = std::fabs(w[k]);
+    if (c.metric == SDQ_METRIC_PRODUCT) S[k] = S[k] * act_norm[k];
+  }
+  const int64_t G8 = K / 8, Go = K / c.m_o;
+  // Outlier masks per m_o-group and inlier masks per 8-group (bit p = position p).
+  // Stored per 8-group: omask8[g] holds the outlier bits that fall in 8-group g.
+  auto omask_of_group = [&](int64_t go) -> uint32_t {
+    return c.n_o ? top_n(S + go * c.m_o, (1u << c.m_o) - 1u, c.m_o, c.n_o) : 0u;
+  };
+
+  // ---- outlier row scale (INT family) needs the row amax over the outliers
+  float s_o = 0.f;
+  if (!c.mx && c.n_o) {
+    float a = 0.f;
+    for (int64_t go = 0; go < Go; ++go) {
+      const uint32_t mk = omask_of_group(go);
+      for (int p = 0; p < c.m_o; ++p)
+        if ((mk >> p) & 1u) a = std::fmax(a, std::fabs(w[go * c.m_o + p]));
+    }
+    s_o = a / (c.fmt_o == SDQ_FMT_INT8 ? 127.0f : 448.0f);
+    if (out.scale_o) static_cast<float*>(out.scale_o)[n] = s_o;
+  }
+
+  // ---- walk 32-K spans (one MX block, two INT blocks, four 8-groups)
+  const int64_t r = n % kTileN, t = n / kTileN;
+  for (int64_t k0 = 0; k0 < K; k0 += 32) {
+    uint32_t om[4], im[4];  // per 8-group position masks
+    for (int gg = 0; gg < 4; ++gg) om[gg] = 0;
+    if (c.n_o) {
+      if (c.m_o == 8) {
+        for (int gg = 0; gg < 4; ++gg) om[gg] = omask_of_group(k0 / 8 + gg);
+      } else {  // m_o == 16
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint32_t mk = omask_of_group(k0 / 16 + hh);
+          om[2 * hh] = mk & 0xFFu;
+          om[2 * hh + 1] = (mk >> 8) & 0xFFu;
+        }
+      }
+    }
+    for (int gg = 0; gg < 4; ++gg) {
+      im[gg] = top_n(S + k0 + 8 * gg, 0xFFu & ~om[gg], 8, c.n_i);
+      int cnt = 0;
+      for (int p = 0; p < 8; ++p) cnt += (im[gg] >> p) & 1;
+      if (cnt != c.n_i) return SDQ_ERR_CONFIG;  // fewer candidates than slots
+    }
+
+    // ---- scales and codes
+    uint8_t ocode[32] = {0}, icode[32] = {0};  // per position of the span
+    if (c.mx) {
+      float ao = 0.f, ai = 0.f;
+      for (int gg = 0; gg < 4; ++gg)
+        for (int p = 0; p < 8; ++p) {
+          const float v = std::fabs(w[k0 + 8 * gg + p]);
+          if ((om[gg] >> p) & 1u) ao = std::fmax(ao, v);
+          if ((im[gg] >> p) & 1u) ai = std::fmax(ai, v);
+        }
+      const int Eo = ao > 0.f ? clamp_int(floor_log2f(ao) - 8, -127, 127) : -127;
+      const int Ei = ai > 0.f ? clamp_int(floor_log2f(ai) - 2, -127, 127) : -127;
+      for (int gg = 0; gg < 4; ++gg)
+        for (int p = 0; p < 8; ++p) {
+          const int kk = 8 * gg + p;
+          const double v = double(w[k0 + kk]);
+          if (((om[gg] >> p) & 1u) && ao > 0.f) ocode[kk] = enc_e4m3(std::ldexp(v, -Eo));
+          if (((im[gg] >> p) & 1u) && ai > 0.f) icode[kk] = enc_e2m1(std::ldexp(v, -Ei));
+        }
+      const int64_t b = k0 / 32;
+      if (out.scale_o && c.n_o) static_cast<uint8_t*>(out.scale_o)[n * (K / 32) + b] = uint8_t(Eo + 127);
+      if (out.scale_i) static_cast<uint8_t*>(out.scale_i)[n * (K / 32) + b] = uint8_t(Ei + 127);
+      if (out.blob) {
+        const int64_t ch = k0 / kChunkK;
+        const int bb = int((k0 % kChunkK) / 32);
+        uint8_t* sc = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * kMxScaleBytesPerTC;
+        sc[mx_scale_byte(bb, int(r), 0)] = c.n_o ? uint8_t(Eo + 127) : 0;
+        sc[mx_scale_byte(bb, int(r), 1)] = uint8_t(Ei + 127);
+      }
+    } else {
+      for (int hb = 0; hb < 2; ++hb) {  // two 16-K blocks
+        float ai = 0.f;
+        for (int gg = 2 * hb; gg < 2 * hb + 2; ++gg)
+          for (int p = 0; p < 8; ++p)
+            if ((im[gg] >> p) & 1u) ai = std::fmax(ai, std::fabs(w[k0 + 8 * gg + p]));
+        const uint16_t h = f32_to_f16_bits(ai / 7.0f);
+        if ((h & 0x7C00u) == 0x7C00u) return SDQ_ERR_VALUE;  // scale overflows fp16
+        const float s = f16_bits_to_f32(h);
+        for (int gg = 2 * hb; gg < 2 * hb + 2; ++gg)
+          for (int p = 0; p < 8; ++p)
+            if (((im[gg] >> p) & 1u) && s != 0.f) {
+              const float v = w[k0 + 8 * gg + p] / s;
+              icode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(v)), -7, 7)));
+            }
+        const int64_t kb = k0 / 16 + hb;
+        if (out.scale_i) static_cast<uint16_t*>(out.scale_i)[n * (K / 16) + kb] = h;
+        if (out.blob) {
+          const int64_t ch = k0 / kChunkK;
+          const int kbl = int((k0 % kChunkK) / 16) + hb;
+          uint8_t* sc = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * kIntScaleBytesPerTC;
+          std::memcpy(sc + int_scale_byte(kbl, int(r)), &h, 2);
+        }
+      }
+      if (c.n_o && s_o != 0.f) {
+        for (int gg = 0; gg < 4; ++gg)
+          for (int p = 0; p < 8; ++p)
+            if ((om[gg] >> p) & 1u) {
+              const float v = w[k0 + 8 * gg + p] / s_o;
+              ocode[8 * gg + p] = c.fmt_o == SDQ_FMT_INT8
+                                      ? uint8_t(int8_t(clamp_int(int(std::nearbyint(v)), -127, 127)))
+                                      : enc_e4m3(double(v));
+            }
+      }
+    }
+
+    // ---- logical outputs
+    for (int gg = 0; gg < 4; ++gg) {
+      const int64_t g8 = k0 / 8 + gg;
+      int j = 0;
+      for (int p = 0; p < 8; ++p)
+        if ((im[gg] >> p) & 1u) {
+          if (out.pos_i) out.pos_i[(n * G8 + g8) * c.n_i + j] = uint8_t(p);
+          if (out.code_i) out.code_i[(n * G8 + g8) * c.n_i + j] = icode[8 * gg + p];
+          ++j;
+        }
+    }
+    if (c.n_o) {
+      const int per = 32 / c.m_o;  // outlier groups in this span
+      for (int go = 0; go < per; ++go) {
+        const int64_t gidx = k0 / c.m_o + go;
+        int j = 0;
+        for (int p = 0; p < c.m_o; ++p) {
+          const int kk = go * c.m_o + p;
+          if ((om[kk / 8] >> (kk % 8)) & 1u) {
+            if (out.pos_o) out.pos_o[(n * Go + gidx) * c.n_o + j] = uint8_t(p);
+            if (out.code_o) out.code_o[(n * Go + gidx) * c.n_o + j] = ocode[kk];
+            ++j;
+          }
+        }
+      }
+    }
+
+    // ---- kernel layout
+    if (out.blob) {
+      const int64_t ch = k0 / kChunkK;
+      uint32_t* words = reinterpret_cast<uint32_t*>(out.blob + out.lay->words_off) +
+                        (t * out.lay->n_chunks + ch) * kWordsPerTC;
+      for (int gg = 0; gg < 4; ++gg) {
+        uint32_t word = 0;
+        int j = 0;
+        for (int p = 0; p < 8; ++p)
+          if ((im[gg] >> p) & 1u) {
+            word |= uint32_t(p) << (8 * j);
+            word |= uint32_t(icode[8 * gg + p] & 0xF) << (8 * j + 4);
+            ++j;
+          }
+        for (int p = 0; p < 8; ++p)
+          if ((om[gg] >> p) & 1u) {
+            for (int bit = 0; bit < 3; ++bit) word |= uint32_t((p >> bit) & 1) << (8 * bit + 3);
+            word |= uint32_t(ocode[8 * gg + p]) << 24;
+          }
+        const int g = int((k0 % kChunkK) / 8) + gg;
+        words[c.mx ? mx_word_index(g, int(r)) : int_word_index(g, int(r))] = word;
+      }
+    }
+  }
+  if (out.blob && !c.mx) {
+    float* rows = reinterpret_cast<float*>(out.blob + out.lay->rows_off);
+    rows[n] = s_o;
+  }
+  return SDQ_OK;
+}
+
+int resolve_threads(int n_threads, int64_t N) {
+  int T = n_threads > 0 ? n_threads : int(std::thread::hardware_concurrency());
+  if (T < 1) T = 1;
+  if (T > 256) T = 256;
+  if (int64_t(T) > N) T = int(N);
+  return T;
+}
+
+sdq_status run_rows(const Cfg& c, const float* W, int64_t N, int64_t K, const float* act_norm,
+                    const RowSink& sink, int n_threads) {
+  const int T = resolve_threads(n_threads, N);
+  std::atomic<int> err{SDQ_OK};
+  auto work = [&](int64_t r0, int64_t r1) {
+    std::vector<float> S(static_cast<size_t>(K));
+    for (int64_t n = r0; n < r1 && err.load(std::memory_order_relaxed) == SDQ_OK; ++n) {
+      const sdq_status s = pack_row(c, W + n * K, act_norm, K, n, S.data(), sink);
+      if (s != SDQ_OK) {
+        int expect = SDQ_OK;
+        err.compare_exchange_strong(expect, s);
+      }
+    }
+  };
+  if (T == 1) {
+    work(0, N);
+  } else {
+    std::vector<std::thread> pool;
+    pool.reserve(size_t(T));
+    for (int i = 0; i < T; ++i) pool.emplace_back(work, N * i / T, N * (i + 1) / T);
+    for (auto& th : pool) th.join();
+  }
+  return sdq_status(err.load());
+}
+
+sdq_status check_act_norm(const Cfg& c, const float* act_norm, int64_t K) {
+  if (c.metric != SDQ_METRIC_PRODUCT) return SDQ_OK;
+  if (!act_norm) return SDQ_ERR_NULL;
+  for (int64_t k = 0; k < K; ++k)
+    if (!std::isfinite(act_norm[k]) || act_norm[k] < 0.f) return SDQ_ERR_VALUE;
+  return SDQ_OK;
+}
+
+}  // namespace
+}  // namespace sdq
+
+using namespace sdq;
+
+extern "C" sdq_status sdq_pack_size(const sdq_config* cfg, int64_t N, int64_t K, size_t* bytes) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!bytes) return SDQ_ERR_NULL;
+  *bytes = size_t(make_layout(c.mx, N, K).total);
+  return SDQ_OK;
+}
+
+extern "C" sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t* bytes) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!bytes) return SDQ_ERR_NULL;
+  auto lg2 = [](int m) { int b = 0; while ((1 << b) < m) ++b; return b; };
+  // bits per row
+  int64_t bits = 0;
+  if (c.n_o) bits += (K / c.m_o) * c.n_o * (8 + lg2(c.m_o));
+  bits += (K / c.m_i) * c.n_i * (4 + lg2(c.m_i));
+  if (c.mx) {
+    bits += (K / 32) * 8;               // inlier e8m0
+    if (c.n_o) bits += (K / 32) * 8;    // outlier e8m0
+  } else {
+    bits += (K / 16) * 16;              // inlier fp16
+    if (c.n_o) bits += 32;              // outlier fp32 per row
+  }
+  *bytes = size_t((bits * N + 7) / 8);
+  return SDQ_OK;
+}
+
+extern "C" sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
+                               const float* act_norm, void* packed, size_t bytes, int n_threads) {
+  Cfg c;
+  sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!W || !packed) return SDQ_ERR_NULL;
+  const Layout lay = make_layout(c.mx, N, K);
+  if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  if ((s = check_act_norm(c, act_norm, K)) != SDQ_OK) return s;
+  std::memset(packed, 0, size_t(lay.total));
+  RowSink sink{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+               static_cast<uint8_t*>(packed), &lay};
+  return run_rows(c, W, N, K, act_norm, sink, n_threads);
+}
+
+extern "C" sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
+                                       const float* act_norm, uint8_t* pos_o, uint8_t* code_o,
+                                       void* scale_o, uint8_t* pos_i, uint8_t* code_i,
+                                       void* scale_i, int n_threads) {
+  Cfg c;
+  sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!W || !pos_i || !code_i || !scale_i) return SDQ_ERR_NULL;
+  if (c.n_o && (!pos_o || !code_o || !scale_o)) return SDQ_ERR_NULL;
+  if ((s = check_act_norm(c, act_norm, K)) != SDQ_OK) return s;
+  if (!c.n_o && scale_o) {  // no outlier branch: report zero scales
+    if (c.mx) std::memset(scale_o, 0, size_t(N * (K / 32)));
+    else std::memset(scale_o, 0, size_t(N) * 4);
+  }
+  RowSink sink{pos_o, code_o, scale_o, pos_i, code_i, scale_i, nullptr, nullptr};
+  return run_rows(c, W, N, K, act_norm, sink, n_threads);
+}
+
+extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed, size_t bytes,
+                                       int64_t N, int64_t K, uint8_t* code_o_dense,
+                                       uint8_t* code_i_dense, void* scale_o, void* scale_i) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!packed || !code_o_dense || !code_i_dense || !scale_o || !scale_i) return SDQ_ERR_NULL;
+  const Layout lay = make_layout(c.mx, N, K);
+  if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  const uint8_t* blob = static_cast<const uint8_t*>(packed);
+  std::memset(code_o_dense, 0, size_t(N * K));
+  std::memset(code_i_dense, 0, size_t(N * K));
+  for (int64_t n = 0; n < N; ++n) {
+    const int64_t t = n / kTileN;
+    const int r = int(n % kTileN);
+    for (int64_t ch = 0; ch < lay.n_chunks; ++ch) {
+      const uint32_t* words = reinterpret_cast<const uint32_t*>(blob + lay.words_off) +
+                              (t * lay.n_chunks + ch) * kWordsPerTC;
+      const uint8_t* sc = blob + lay.scales_off + (t * lay.n_chunks + ch) * lay.scale_bytes_per_tc;
+      for (int g = 0; g < 16; ++g) {
+        const uint32_t word = words[c.mx ? mx_word_index(g, r) : int_word_index(g, r)];
+        const int64_t kbase = n * K + ch * kChunkK + g * 8;
+        for (int j = 0; j < 3; ++j) {
+          const int p = int((word >> (8 * j)) & 7u);
+          const uint8_t nib = uint8_t((word >> (8 * j + 4)) & 0xFu);
+          if (!nib) continue;
+          code_i_dense[kbase + p] = c.mx ? nib : uint8_t(int8_t(int8_t(nib << 4) >> 4));
+        }
+        const uint8_t oc = uint8_t(word >> 24);
+        if (oc) {
+          const int p = int(((word >> 3) & 1u) | ((word >> 10) & 2u) | ((word >> 17) & 4u));
+          code_o_dense[kbase + p] = oc;
+        }
+      }
+      if (c.mx) {
+        for (int b = 0; b < 4; ++b) {
+          const int64_t bi = n * (K / 32) + ch * 4 + b;
+          static_cast<uint8_t*>(scale_o)[bi] = sc[mx_scale_byte(b, r, 0)];
+          static_cast<uint8_t*>(scale_i)[bi] = sc[mx_scale_byte(b, r, 1)];
+        }
+      } else {
+        for (int kb = 0; kb < 8; ++kb) {
+          uint16_t h;
+          std::memcpy(&h, sc + int_scale_byte(kb, r), 2);
+          static_cast<uint16_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = h;
+        }
+      }
+    }
+    if (!c.mx) {
+      const float* rows = reinterpret_cast<const float*>(blob + lay.rows_off);
+      static_cast<float*>(scale_o)[n] = rows[n];
+    }
+  }
+  return SDQ_OK;
+}

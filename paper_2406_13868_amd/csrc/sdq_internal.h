@@ -1,0 +1,49 @@
+// Internal helpers shared by the host-side translation units of libsdq.
+#pragma once
+#include <cstdint>
+
+#include "../../include/sdq.h"
+
+namespace sdq {
+
+struct Cfg {
+  bool mx;
+  int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric;
+};
+
+// Validates a configuration and shape; fills `out` on success.
+inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* out) {
+  if (!c) return SDQ_ERR_NULL;
+  if (c->family != SDQ_FAMILY_INT && c->family != SDQ_FAMILY_MX) return SDQ_ERR_CONFIG;
+  const bool mx = c->family == SDQ_FAMILY_MX;
+  if (c->n_o < 0 || c->n_i < 0 || c->m_o <= 0 || c->m_i <= 0) return SDQ_ERR_CONFIG;
+  if (c->n_o > c->m_o || c->n_i > c->m_i || c->n_i == 0) return SDQ_ERR_CONFIG;
+  if (c->metric != SDQ_METRIC_MAGNITUDE && c->metric != SDQ_METRIC_PRODUCT) return SDQ_ERR_CONFIG;
+  if (mx) {
+    if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
+      return SDQ_ERR_CONFIG;
+  } else {
+    if ((c->fmt_o != SDQ_FMT_E4M3 && c->fmt_o != SDQ_FMT_INT8) || c->fmt_i != SDQ_FMT_INT4 ||
+        c->fmt_a != SDQ_FMT_INT8)
+      return SDQ_ERR_CONFIG;
+  }
+  // What the kernels implement.
+  if (c->m_i != 8 || c->n_i > 3) return SDQ_ERR_UNSUPPORTED;
+  if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
+  if (N <= 0 || K <= 0 || K % 128 != 0) return SDQ_ERR_SHAPE;
+  if (N > (int64_t(1) << 31) || K > (int64_t(1) << 24)) return SDQ_ERR_SHAPE;
+  if (out) {
+    out->mx = mx;
+    out->n_o = c->n_o;
+    out->m_o = c->n_o ? c->m_o : 8;
+    out->fmt_o = c->fmt_o;
+    out->n_i = c->n_i;
+    out->m_i = c->m_i;
+    out->fmt_i = c->fmt_i;
+    out->fmt_a = c->fmt_a;
+    out->metric = c->metric;
+  }
+  return SDQ_OK;
+}
+
+}  // namespace sdq

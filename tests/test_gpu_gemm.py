@@ -1,0 +1,247 @@
+"""GPU: the decomposed GEMM against the fp64 oracle.
+
+The whole path runs on the library: X -> sdq_quantize_act (GPU), W ->
+sdq_pack (host C++) -> sdq_gemm (GPU).  The expected values come from the
+oracle alone (``oracle.sdq.reference`` on the same X and W).  Integer-grid
+inputs, on which every scale is exactly 1, must come out exact.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import sdq as S
+from tests.gpu_util import assert_close, assert_close_terms, say, torch_cuda
+
+import paper_2406_13868_amd as sdq
+
+pytestmark = pytest.mark.gpu
+
+INT_CFGS = [("int", 1, 8, "e4m3", 3), ("int", 1, 8, "int8", 3), ("int", 1, 16, "e4m3", 3),
+            ("int", 1, 8, "e4m3", 2), ("int", 1, 16, "e4m3", 2), ("int", 0, 8, "e4m3", 3)]
+MX_CFGS = [("mx", 1, 8, "e4m3", 2), ("mx", 1, 8, "e4m3", 3), ("mx", 1, 16, "e4m3", 2),
+           ("mx", 1, 16, "e4m3", 3), ("mx", 0, 8, "e4m3", 2)]
+
+
+def _cfgs(fam, n_o, m_o, fmt_o, n_i):
+    if fam == "int":
+        return (sdq.Config("int", n_o, m_o, fmt_o, n_i, 8, "int4", "int8"),
+                S.Config("int", n_o, m_o, fmt_o, n_i, 8, "int4", "int8"))
+    return (sdq.Config("mx", n_o, m_o, "e4m3", n_i, 8, "e2m1", "e4m3"),
+            S.Config("mx", n_o, m_o, "e4m3", n_i, 8, "e2m1", "e4m3"))
+
+
+def _ids(c):
+    return f"{c[0]}-{c[1]}:{c[2]}{c[3]}+{c[4]}:8"
+
+
+def run_gpu(X, W, cfg, path=sdq.PATH_AUTO, x_bf16=False):
+    torch = torch_cuda()
+    N, K = W.shape
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    t = torch.from_numpy(np.ascontiguousarray(X))
+    Xd = (t.to(torch.bfloat16) if x_bf16 else t).cuda()
+    Xq, s_a = sdq.quantize_act(Xd, cfg)
+    Y = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy(), Xq, s_a, blob
+
+
+def abs_terms(X, W, cfg_o):
+    """sum_k |s_a x_k| |w_k| per output (the scale of a dot product's rounding)."""
+    Xq, s_a = S.quantize_act(X, cfg_o)
+    L = S.pack_logical(W, cfg_o)
+    A = np.abs(S.dequant_act(Xq, s_a, cfg_o))
+    return A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
+
+
+def check(Y, Yref, X, W, cfg_o, what=""):
+    if cfg_o.family == "mx":
+        return assert_close_terms(Y, Yref, abs_terms(X, W, cfg_o), what)
+    return assert_close(Y, Yref, what)
+
+
+def _paths(fam, M):
+    if fam == "int" and M <= 8:
+        return [sdq.PATH_DECODE, sdq.PATH_MFMA]
+    return [sdq.PATH_MFMA]
+
+
+@pytest.mark.parametrize("c", INT_CFGS + MX_CFGS, ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(1, 256, 256), (2, 96, 384), (3, 50, 256), (5, 256, 512),
+                                   (8, 64, 128), (16, 256, 256), (17, 100, 384), (33, 160, 256),
+                                   (64, 256, 512), (100, 70, 256), (130, 129, 384)])
+def test_gemm_matches_oracle(c, M, N, K):
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(1, M, K)
+    W = synth.make_w(1, 0, N, K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    for path in _paths(c[0], M):
+        say("gemm", _ids(c), M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} path={path}")
+
+
+def _int_grid(rng, M, N, K, outlier_fmt):
+    """Inputs on which every scale is exactly 1 (act, inlier and outlier)."""
+    X = rng.integers(-127, 128, (M, K)).astype(np.float32)
+    X[:, 0] = 127.0
+    W = rng.integers(-7, 8, (N, K)).astype(np.float32)
+    W[:, ::16] = 7.0                              # every 16-block: inlier amax 7
+    big = 127.0 if outlier_fmt == "int8" else 448.0
+    vals = rng.integers(8, 17, (N, K // 8)).astype(np.float32)  # exact in e4m3 and int8
+    vals *= rng.choice([-1, 1], (N, K // 8))
+    vals[:, 0] = big                              # row amax of the outliers
+    W[:, 3::8] = vals                             # the largest of each 8-group
+    W[:, 0] = 7.0
+    return X, W
+
+
+@pytest.mark.parametrize("fmt_o", ["int8", "e4m3"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 4096), (2, 32, 1024), (16, 96, 1024), (64, 64, 4096)])
+def test_integer_grid_is_exact(fmt_o, M, N, K):
+    cfg, cfg_o = _cfgs("int", 1, 8, fmt_o, 3)
+    rng = np.random.default_rng(M * 7 + N)
+    X, W = _int_grid(rng, M, N, K, fmt_o)
+    Yref, Xq_ref, s_ref, L = S.reference(X, W, cfg_o)
+    assert (s_ref == 1).all() and (L["scale_i"] == 1).all() and (L["scale_o"] == 1).all()
+    P_i, P_o = S.int_partials(Xq_ref, L)
+    if fmt_o == "int8":
+        exact = P_i.sum(-1) + P_o
+        assert np.array_equal(Yref, exact.astype(np.float64))
+    for path in _paths("int", M):
+        say("int grid", fmt_o, M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        assert np.array_equal(Y.astype(np.float64), Yref), f"path {path}: not exact"
+
+
+@pytest.mark.parametrize("M,N,K", [(32, 64, 1024), (100, 96, 512)])
+def test_mx_grid_is_exact(M, N, K):
+    cfg, cfg_o = _cfgs("mx", 1, 8, "e4m3", 2)
+    rng = np.random.default_rng(5)
+    X = rng.integers(-16, 17, (M, K)).astype(np.float32)
+    X[:, 0] = 448.0                                   # s_a = 1, inv = 1
+    W = rng.choice([-3.0, -2.0, -1.0, 1.0, 2.0, 3.0], (N, K)).astype(np.float32)
+    W[:, ::32] = 4.0                                  # inlier block amax in [4, 8): E = 0
+    W[:, 5::8] = (256 + 32 * rng.integers(0, 7, (N, K // 8))).astype(np.float32)  # e4m3-exact outliers, E = 0
+    Yref, _, s_ref, L = S.reference(X, W, cfg_o)
+    assert (s_ref == 1).all() and (L["scale_i"] == 127).all() and (L["scale_o"] == 127).all()
+    say("mx grid", M, N, K)
+    Y, _, _, _ = run_gpu(X, W, cfg)
+    assert np.array_equal(Y.astype(np.float64), Yref)
+
+
+@pytest.mark.parametrize("c", [INT_CFGS[0], MX_CFGS[0]], ids=_ids)
+def test_degenerate_inputs(c):
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(1, 20, 256)
+    X[3] = 0.0
+    W = synth.make_w(1, 0, 64, 256)
+    W[10] = 0.0
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    say("degenerate", _ids(c))
+    for path in _paths(c[0], 1):
+        Xs = X[:1] if path == sdq.PATH_DECODE else X
+        Y, _, _, _ = run_gpu(Xs, W, cfg, path)
+        check(Y, Yref[: len(Xs)], Xs, W, cfg_o)
+        assert (Y[:, 10] == 0).all()
+    Y, _, _, _ = run_gpu(X, W, cfg)
+    assert (Y[3] == 0).all()
+    # all-zero weights
+    Y, _, _, _ = run_gpu(X, np.zeros_like(W), cfg)
+    assert (Y == 0).all()
+    # M = 0
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    Xq = torch.zeros((0, 256), dtype=torch.uint8, device="cuda")
+    s_a = torch.zeros((0,), dtype=torch.float32, device="cuda")
+    Y = sdq.gemm(Xq, s_a, blob, 64, 256, cfg)
+    torch.cuda.synchronize()
+    assert Y.shape == (0, 64)
+
+
+@pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], MX_CFGS[0]], ids=_ids)
+def test_repeat_runs_are_bit_identical(c):
+    cfg, _ = _cfgs(*c)
+    X = synth.make_x(2, 64, 1024)
+    W = synth.make_w(2, 0, 512, 1024)
+    for path in _paths(c[0], 2):
+        say("determinism", _ids(c), path)
+        Xs = X[:2] if path == sdq.PATH_DECODE else X
+        Y0, _, _, _ = run_gpu(Xs, W, cfg, path)
+        for _ in range(3):
+            Y1, _, _, _ = run_gpu(Xs, W, cfg, path)
+            assert np.array_equal(Y0.view(np.uint32), Y1.view(np.uint32))
+
+
+def test_quantized_activations_feed_gemm_like_oracle():
+    """The oracle's own Xq/s_a fed to the GPU GEMM give the same Y as the GPU's."""
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(*INT_CFGS[0])
+    X = synth.make_x(1, 16, 256)
+    W = synth.make_w(1, 0, 256, 256)
+    Yref, Xq_ref, s_ref, _ = S.reference(X, W, cfg_o)
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    Y = sdq.gemm(torch.from_numpy(Xq_ref).cuda(), torch.from_numpy(s_ref).cuda(), blob, 256, 256, cfg)
+    torch.cuda.synchronize()
+    assert_close(Y.cpu().numpy(), Yref)
+    Y2, _, _, _ = run_gpu(X, W, cfg)
+    assert np.array_equal(Y.cpu().numpy(), Y2)
+
+
+@pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[4], MX_CFGS[0]], ids=_ids)
+@pytest.mark.parametrize("M,dt", [(1, "bf16"), (2, "f32"), (3, "bf16"), (16, "bf16")])
+def test_linear_equals_quantize_then_gemm(c, M, dt):
+    """sdq_linear (one fused kernel on the decode path) == the two-call path, bit for bit."""
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(*c)
+    N, K = 300, 1024
+    X = synth.bf16_round(synth.make_x(2, M, K))
+    W = synth.make_w(2, 0, N, K)
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    Xd = torch.from_numpy(X).cuda()
+    if dt == "bf16":
+        Xd = Xd.to(torch.bfloat16)
+    say("linear", _ids(c), M, dt)
+    Y1, Xq1, s1 = sdq.linear(Xd, blob, N, K, cfg)
+    Xq2, s2 = sdq.quantize_act(Xd, cfg)
+    Y2 = sdq.gemm(Xq2, s2, blob, N, K, cfg)
+    torch.cuda.synchronize()
+    assert torch.equal(Xq1, Xq2) and torch.equal(s1.view(torch.int32), s2.view(torch.int32))
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+    Yref, Xq_ref, _, _ = S.reference(X, W, cfg_o)
+    assert np.array_equal(Xq1.cpu().numpy(), Xq_ref)
+    check(Y1.cpu().numpy(), Yref, X, W, cfg_o)
+
+
+@pytest.mark.parametrize("c", [INT_CFGS[0], MX_CFGS[0]], ids=_ids)
+def test_hip_graph_replays_match_eager(c):
+    """The step captured in a HIP graph gives the eager result on every replay."""
+    torch = torch_cuda()
+    cfg, _ = _cfgs(*c)
+    N, K, M = 512, 1024, (1 if c[0] == "int" else 64)
+    X = torch.from_numpy(synth.make_x(2, M, K)).cuda().to(torch.bfloat16)
+    blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
+    Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    Xq = torch.empty((M, K), dtype=torch.uint8, device="cuda")
+    s_a = torch.empty((M,), dtype=torch.float32, device="cuda")
+    say("graph", _ids(c))
+    sdq.linear(X, blob, N, K, cfg, out=Y, xq=Xq, scales=s_a)
+    torch.cuda.synchronize()
+    ref = Y.clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        sdq.linear(X, blob, N, K, cfg, out=Y, xq=Xq, scales=s_a)
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        sdq.linear(X, blob, N, K, cfg, out=Y, xq=Xq, scales=s_a)
+    for rep in range(4):
+        Y.fill_(float("nan"))
+        Xq.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
+        # eager work in between
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y))
+        torch.cuda.synchronize()

@@ -1,0 +1,217 @@
+"""Host packer and C ABI (no GPU): bit-exact against the oracle.
+
+The packer (C++, in libsdq.so) and the oracle (numpy) are independent
+implementations of the same definitions; their logical outputs (positions,
+codes, scales) must agree exactly, and the kernel layout must decode back to
+the oracle's dense codes.
+"""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import accounting as A
+from oracle import sdq as S
+
+sdq = pytest.importorskip("paper_2406_13868_amd")
+from paper_2406_13868_amd import _lib  # noqa: E402
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+HEADER = os.path.join(os.path.dirname(HERE), "include", "sdq.h")
+
+CONFIGS = [
+    ("int", 1, 8, "e4m3", 3), ("int", 1, 8, "int8", 3), ("int", 1, 16, "e4m3", 3),
+    ("int", 1, 8, "e4m3", 2), ("int", 1, 16, "e4m3", 2), ("int", 0, 8, "e4m3", 3),
+    ("mx", 1, 8, "e4m3", 2), ("mx", 1, 8, "e4m3", 3), ("mx", 1, 16, "e4m3", 2),
+    ("mx", 1, 16, "e4m3", 3), ("mx", 0, 8, "e4m3", 2),
+]
+
+
+def _cfgs(fam, n_o, m_o, fmt_o, n_i, metric="magnitude"):
+    if fam == "int":
+        lib = sdq.Config("int", n_o, m_o, fmt_o, n_i, 8, "int4", "int8", metric)
+        ora = S.Config("int", n_o, m_o, fmt_o, n_i, 8, "int4", "int8", metric)
+    else:
+        lib = sdq.Config("mx", n_o, m_o, "e4m3", n_i, 8, "e2m1", "e4m3", metric)
+        ora = S.Config("mx", n_o, m_o, "e4m3", n_i, 8, "e2m1", "e4m3", metric)
+    return lib, ora
+
+
+def _ids(c):
+    return f"{c[0]}-{c[1]}:{c[2]}{c[3]}+{c[4]}:8"
+
+
+def _compare_logical(Lg, Lo, cfg_o):
+    if cfg_o.n_o:
+        assert np.array_equal(Lg["pos_o"], Lo["pos_o"].astype(np.uint8))
+        assert np.array_equal(Lg["code_o"], Lo["code_o"])
+    assert np.array_equal(Lg["pos_i"], Lo["pos_i"].astype(np.uint8))
+    if cfg_o.family == "int":
+        assert np.array_equal(Lg["code_i"].view(np.int8), Lo["code_i"].astype(np.int8))
+        assert np.array_equal(Lg["scale_i"], Lo["scale_i"].view(np.uint16))
+        if cfg_o.n_o:
+            assert np.array_equal(Lg["scale_o"].view(np.uint32), Lo["scale_o"].view(np.uint32))
+    else:
+        assert np.array_equal(Lg["code_i"], Lo["code_i"])
+        assert np.array_equal(Lg["scale_i"], Lo["scale_i"])
+        if cfg_o.n_o:
+            assert np.array_equal(Lg["scale_o"], Lo["scale_o"])
+
+
+@pytest.mark.parametrize("c", CONFIGS, ids=_ids)
+@pytest.mark.parametrize("shape", [(256, 256), (50, 384), (33, 128)])
+def test_logical_pack_matches_oracle(c, shape):
+    cfg, cfg_o = _cfgs(*c)
+    N, K = shape
+    W = synth.make_w(2, 0, N, K)
+    Lg = sdq.pack_logical(W, cfg)
+    Lo = S.pack_logical(W, cfg_o)
+    _compare_logical(Lg, Lo, cfg_o)
+
+
+@pytest.mark.parametrize("c", CONFIGS, ids=_ids)
+def test_kernel_layout_roundtrip(c):
+    cfg, cfg_o = _cfgs(*c)
+    N, K = 70, 512  # ragged last tile of 32 rows
+    W = synth.make_w(5, 0, N, K)
+    blob = sdq.pack(W, cfg)
+    U = sdq.unpack_dense(blob, cfg, N, K)
+    Lo = S.pack_logical(W, cfg_o)
+    if cfg_o.family == "int":
+        assert np.array_equal(U["code_i_dense"].view(np.int8), Lo["code_i_dense"].astype(np.int8))
+        assert np.array_equal(U["scale_i"], Lo["scale_i"].view(np.uint16))
+        if cfg_o.n_o:
+            assert np.array_equal(U["scale_o"].view(np.uint32), Lo["scale_o"].view(np.uint32))
+    else:
+        assert np.array_equal(U["code_i_dense"], Lo["code_i_dense"])
+        assert np.array_equal(U["scale_i"], Lo["scale_i"])
+        if cfg_o.n_o:
+            assert np.array_equal(U["scale_o"], Lo["scale_o"])
+    assert np.array_equal(U["code_o_dense"], Lo["code_o_dense"])
+
+
+def test_product_metric_matches_oracle():
+    cfg, cfg_o = _cfgs("int", 1, 8, "e4m3", 3, metric="product")
+    W = synth.make_w(1, 0, 64, 256)
+    X_cal = synth.make_x(1, 32, 256)
+    c = S.activation_norm(X_cal)
+    _compare_logical(sdq.pack_logical(W, cfg, act_norm=c), S.pack_logical(W, cfg_o, act_norm=c), cfg_o)
+    cfg, cfg_o = _cfgs("mx", 1, 8, "e4m3", 2, metric="product")
+    _compare_logical(sdq.pack_logical(W, cfg, act_norm=c), S.pack_logical(W, cfg_o, act_norm=c), cfg_o)
+
+
+@pytest.mark.parametrize("wid", [1, 2, 4])
+def test_workload_first_layer_matches_oracle(wid):
+    """A row slice of each workload's first layer at its real K."""
+    w = synth.WORKLOADS[wid]
+    L = w.layers[0]
+    W = synth.make_w(wid, 0, L.N, L.K)[:96]
+    cfg = sdq.Config.of(w.formats[0])
+    cfg_o = S.config_from(w.formats[0])
+    _compare_logical(sdq.pack_logical(W, cfg), S.pack_logical(W, cfg_o), cfg_o)
+
+
+def test_tied_and_degenerate_weights():
+    cfg, cfg_o = _cfgs("int", 1, 8, "e4m3", 3)
+    rng = np.random.default_rng(3)
+    W = (rng.integers(-2, 3, (40, 256)) * 0.125).astype(np.float32)  # many exact ties
+    W[5] = 0.0                                                        # an all-zero row
+    W[7, :16] = 0.0                                                   # an all-zero block
+    W[9] = -0.0
+    _compare_logical(sdq.pack_logical(W, cfg), S.pack_logical(W, cfg_o), cfg_o)
+    cfgm, cfgm_o = _cfgs("mx", 1, 8, "e4m3", 3)
+    _compare_logical(sdq.pack_logical(W, cfgm), S.pack_logical(W, cfgm_o), cfgm_o)
+
+
+def test_pack_is_thread_count_independent():
+    cfg, _ = _cfgs("int", 1, 8, "e4m3", 3)
+    W = synth.make_w(2, 0, 333, 1024)
+    a = sdq.pack(W, cfg, n_threads=1)
+    b = sdq.pack(W, cfg, n_threads=7)
+    c = sdq.pack(W, cfg, n_threads=0)
+    assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+@pytest.mark.parametrize("c", CONFIGS, ids=_ids)
+def test_logical_bytes_match_accounting(c):
+    cfg, cfg_o = _cfgs(*c)
+    N, K = 4096, 4096
+    if cfg_o.family == "int":
+        b = A.sdq_bits_per_weight(cfg.n_o, cfg.m_o, 8, cfg.n_i, 8, 4, 32, 0, 16, 16, K)
+    else:
+        b = A.sdq_bits_per_weight(cfg.n_o, cfg.m_o, 8, cfg.n_i, 8, 4, 8, 32, 8, 32, K)
+    want = int(np.ceil(float(b * N * K) / 8))
+    assert sdq.logical_bytes(cfg, N, K) == want
+
+
+def test_logical_bytes_llama_decode_layer():
+    # 4096x4096, 1:8 e4m3 + 3:8 int4 with fp16 scales per 16: 5.008 bits per weight
+    assert sdq.logical_bytes(sdq.Config.int_family(), 4096, 4096) == 10_502_144
+
+
+def _raw(name):
+    return getattr(_lib.lib(), name)
+
+
+def test_error_paths():
+    cfg = sdq.Config.int_family().c()
+    L = _lib.lib()
+    n = C.c_size_t()
+    assert L.sdq_pack_size(None, 32, 128, C.byref(n)) == -1
+    assert L.sdq_pack_size(C.byref(cfg), 32, 100, C.byref(n)) == -2       # K % 128
+    assert L.sdq_pack_size(C.byref(cfg), 0, 128, C.byref(n)) == -2
+    bad = sdq.Config("int", 1, 8, "e2m1", 3).c()
+    assert L.sdq_pack_size(C.byref(bad), 32, 128, C.byref(n)) == -3
+    unsup = sdq.Config("int", 2, 8, "e4m3", 3).c()
+    assert L.sdq_pack_size(C.byref(unsup), 32, 128, C.byref(n)) == -6
+    W = np.zeros((32, 128), np.float32)
+    buf = np.zeros(16, np.uint8)
+    assert L.sdq_pack(C.byref(cfg), C.c_void_p(W.ctypes.data), 32, 128, None,
+                      C.c_void_p(buf.ctypes.data), buf.nbytes, 1) == -4
+    W[3, 7] = np.nan
+    with pytest.raises(sdq.SDQError) as e:
+        sdq.pack(W, sdq.Config.int_family())
+    assert e.value.status == -7
+    # product metric needs act_norm
+    with pytest.raises(sdq.SDQError) as e:
+        sdq.pack(np.zeros((32, 128), np.float32), sdq.Config.int_family(metric="product"))
+    assert e.value.status == -1
+    # device entry points validate before touching the GPU
+    assert L.sdq_gemm(C.byref(cfg), None, None, 4, None, 32, 128, None, None) == -1
+    assert L.sdq_gemm(C.byref(cfg), None, None, 4, None, 32, 120, None, None) == -2
+    assert L.sdq_gemm(C.byref(cfg), None, None, 0, None, 32, 128, None, None) == 0  # M = 0
+    assert L.sdq_quantize_act(C.byref(cfg), None, 0, 4, 128, None, None, None) == -1
+    assert L.sdq_quantize_act(C.byref(cfg), None, 5, 4, 128, None, None, None) == -3
+    mxc = sdq.Config.mx_family().c()
+    assert L.sdq_gemm_ex(C.byref(mxc), C.c_void_p(16), C.c_void_p(16), 1, C.c_void_p(16),
+                         32, 128, C.c_void_p(16), None, 1) == -6   # no decode path for MX
+    for s in list(_lib.STATUS) + [123]:
+        assert L.sdq_status_string(s)
+
+
+def test_fp16_scale_overflow_is_an_error():
+    W = np.zeros((32, 128), np.float32)
+    W[0, 0] = 1e6  # inlier scale 1e6/7 > 65504 (it is an inlier: the outlier is the other 1e6)
+    W[0, 1] = 1e6
+    with pytest.raises(sdq.SDQError) as e:
+        sdq.pack(W, sdq.Config.int_family())
+    assert e.value.status == -7
+
+
+def test_library_exports_every_header_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:sdq_status|const char\*)\s+(sdq_\w+)\s*\(", text, re.M))
+    assert declared == set(_lib.EXPORTS)
+    L = _lib.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_gemm_path_choice():
+    cfg = sdq.Config.int_family()
+    assert sdq.gemm_path(cfg, 1, 4096, 4096) == sdq.PATH_DECODE
+    assert sdq.gemm_path(cfg, 2048, 4096, 4096) == sdq.PATH_MFMA
+    assert sdq.gemm_path(sdq.Config.mx_family(), 1, 4096, 4096) == sdq.PATH_MFMA
