@@ -172,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
     const uint32_t wv[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
     const uint32_t sv[4] = {sr.x, sr.y, sr.z, sr.w};
     if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
-#pragma unroll
+#pragma unroll 2
     for (int kb = 0; kb < 8; ++kb) {
       const h8 bi = inlier_f16<NI>(wv[kb]);
       const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
@@ -209,8 +209,139 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
     }
 }
 
+// Split-K form for few tokens (M <= 64): one 32-row tile of W per workgroup,
+// its NW waves take interleaved 128-K chunks and each lane reads its 8-byte
+// A-fragment pieces of Xq straight from L2 (no LDS staging), converting them
+// to fp16 in registers; the wave partials are summed through LDS with a
+// fixed-order tree at the end.  This keeps NT*NW waves in flight where the
+// tiled form above would run only NT/4 workgroups.
+template <int MS, int NI, bool OUT_INT8, int NW>
+__global__ __launch_bounds__(NW * 64) void int_mfma_splitk_kernel(MfmaArgs a) {
+  constexpr int BM = 32 * MS;
+  __shared__ float red[NW / 2][16][64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, h = lane >> 5;
+  const int m0 = blockIdx.y * BM;
+  const int tile = blockIdx.x;
+  const int KC = a.n_chunks;
+
+  const uint8_t* wbase = a.blob + size_t(tile) * KC * kWordBytesPerTC + size_t(lane) * 32;
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile) * KC * kIntScaleBytesPerTC + col * 16;
+
+  // lane (col, h) of sub-tile ms reads row m0 + 32*ms + col, K bytes 16*kb + 8*h .. +8
+  uint2 xr[MS][8];
+  auto load_x = [&](int c) {
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms) {
+      const int m = m0 + ms * 32 + col;
+      const uint8_t* xp = a.Xq + size_t(m < a.M ? m : 0) * a.K + c * kChunkK + h * 8;
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb)
+        xr[ms][kb] = m < a.M ? *reinterpret_cast<const uint2*>(xp + kb * 16) : make_uint2(0, 0);
+    }
+  };
+  uint4 wr0, wr1, sr;
+  auto load_w = [&](int c) {
+    wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
+    wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 16);
+    sr = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kIntScaleBytesPerTC);
+  };
+
+  f16v acc[MS], acco[MS];
+#pragma unroll
+  for (int s = 0; s < MS; ++s)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) { acc[s][e] = 0.f; acco[s][e] = 0.f; }
+
+  int c = wave;
+  if (c < KC) { load_x(c); load_w(c); }
+  for (; c < KC; c += NW) {
+    uint2 xc[MS][8];
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) xc[ms][kb] = xr[ms][kb];
+    const uint32_t wv[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
+    const uint32_t sv[4] = {sr.x, sr.y, sr.z, sr.w};
+    if (c + NW < KC) { load_x(c + NW); load_w(c + NW); }
+#pragma unroll 2
+    for (int kb = 0; kb < 8; ++kb) {
+      const h8 bi = inlier_f16<NI>(wv[kb]);
+      const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
+      const uint32_t sw = sv[kb >> 1];
+      const float s = (float)__builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        uint32_t a0, a1, a2, a3;
+        i8x4_to_f16x4(xc[ms][kb].x, a0, a1);
+        i8x4_to_f16x4(xc[ms][kb].y, a2, a3);
+        const u4v av4 = {a0, a1, a2, a3};
+        const h8 av = __builtin_bit_cast(h8, av4);
+        f16v zero;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zero[e] = 0.f;
+        const f16v P = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bi, zero, 0, 0, 0);
+        acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bo, acco[ms], 0, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[ms][e] = fmaf(P[e], s, acc[ms][e]);
+      }
+    }
+  }
+
+  // ---- tree over the waves: in round r, wave w + 2^r hands its partial to w
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms) {
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+      f16v& v = which ? acco[ms] : acc[ms];
+#pragma unroll
+      for (int stride = NW / 2; stride >= 1; stride >>= 1) {
+        const bool sender = wave >= stride && wave < 2 * stride;
+        if (sender) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) red[wave - stride][e][lane] = v[e];
+        }
+        __syncthreads();
+        if (wave < stride) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) v[e] += red[wave][e][lane];
+        }
+        __syncthreads();
+      }
+    }
+  }
+  if (wave > 0) return;
+  const int n = tile * kTileN + col;
+  if (n >= a.N) return;
+  const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + ms * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+      if (m < a.M) a.Y[size_t(m) * a.N + n] = a.s_a[m] * fmaf(so, acco[ms][e], acc[ms][e]);
+    }
+}
+
+template <int MS, int NI, int NW>
+hipError_t launch_splitk(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
+  const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
+  const dim3 block(NW * 64);
+  if (c.fmt_o == SDQ_FMT_INT8)
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, true, NW>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, false, NW>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
 template <int MS, int NI>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
+  if constexpr (MS <= 2) {
+    // few tokens: split K inside the workgroup so that about 2048+ waves run
+    if (int64_t(a.n_tiles) * 4 >= 2048 || a.n_chunks < 8) return launch_splitk<MS, NI, 4>(c, a, st);
+    return launch_splitk<MS, NI, 8>(c, a, st);
+  }
   const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
   const dim3 block(kThreads);
   if (c.fmt_o == SDQ_FMT_INT8)
