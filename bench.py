@@ -57,6 +57,13 @@ def parse():
     p.add_argument("--rotate-mb", type=float, default=512.0)
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--context", action="store_true",
+                   help="also time cache-resident and eager GEMM launches (context figures)")
+    p.add_argument("--counters", type=int, default=0, metavar="L",
+                   help="counter-collection mode: L eager GEMM launches over the rotated "
+                        "weight copies, no graphs, no JSON line")
+    p.add_argument("--copy-calibration", type=float, default=0.0, metavar="MB",
+                   help="counter calibration: five plain device copies of MB megabytes")
     return p.parse_args()
 
 
@@ -94,6 +101,19 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     sdq._lib.lib()
+
+    if a.copy_calibration > 0:
+        # a plain copy kernel of known size: FETCH_SIZE and WRITE_SIZE of one
+        # dispatch should each read this many bytes
+        n = int(a.copy_calibration * 1e6) // 16 * 16
+        src = torch.randint(0, 255, (n,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
+        return
 
     if a.workload == "sweep":
         wid = 5
@@ -135,6 +155,10 @@ def main():
     sa = [[torch.empty((M,), dtype=torch.float32, device=dev) for _ in Ls] for _ in range(R)]
     Y = [[torch.empty((M, L.N), dtype=torch.float32, device=dev) for L in Ls] for _ in range(R)]
     stream = torch.cuda.current_stream()
+    for r in range(R):  # every rotated copy's Xq/s_a holds real codes before any GEMM-only launch
+        for j in range(len(Ls)):
+            sdq.quantize_act(Xd[r][j], cfg, out=Xq[r][j], scales=sa[r][j])
+    torch.cuda.synchronize()
 
     def step(i):
         r = i % R
@@ -174,6 +198,16 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n  # ms per call
 
+    if a.counters > 0:
+        # hardware-counter runs: eager launches of the GEMM kernel only, each on
+        # a different weight copy, so that every dispatch streams from HBM
+        for i in range(a.counters):
+            gemms(i)
+        torch.cuda.synchronize()
+        print(json.dumps({"counter_launches": a.counters * len(Ls), "rotated_copies": R,
+                          "kernel_source_hash": kernel_source_hash()}))
+        return
+
     # ---------------------------------------------------------------- timed steps
     for i in range(a.warmup):
         step(i)
@@ -187,18 +221,21 @@ def main():
     g_gemm = capture(gemms, n_g, 0)
     timed(g_gemm, n_g)
     gemm_us = timed(g_gemm, n_g) * 1e3
-    g_hot = capture(gemms_hot, n_g, 0)
-    timed(g_hot, n_g)
-    gemm_hot_us = timed(g_hot, n_g) * 1e3
-    # eager launches (host launch rate included): context only
-    torch.cuda.synchronize()
-    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    b0.record(stream)
-    for i in range(n_g):
-        gemms(i)
-    b1.record(stream)
-    torch.cuda.synchronize()
-    gemm_b2b_us = b0.elapsed_time(b1) * 1e3 / n_g
+    gemm_hot_us = gemm_b2b_us = None
+    if a.context:
+        g_hot = capture(gemms_hot, n_g, 0)
+        timed(g_hot, n_g)
+        gemm_hot_us = timed(g_hot, n_g) * 1e3
+        # eager launches (host launch rate included)
+        torch.cuda.synchronize()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record(stream)
+        for i in range(n_g):
+            gemms(i)
+        b1.record(stream)
+        torch.cuda.synchronize()
+        gemm_b2b_us = round(b0.elapsed_time(b1) * 1e3 / n_g, 3)
+        gemm_hot_us = round(gemm_hot_us, 3)
 
     flops = sum(2.0 * M * L.N * L.K for L in Ls)
     alg_bytes = logical + sum(M * L.K + 4 * M + 4 * M * L.N for L in Ls)
@@ -242,8 +279,8 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "gemm_us_graph": round(gemm_us, 3),
-        "gemm_us_eager": round(gemm_b2b_us, 3),
-        "gemm_us_cache_resident": round(gemm_hot_us, 3),
+        "gemm_us_eager": gemm_b2b_us,
+        "gemm_us_cache_resident": gemm_hot_us,
         "gemm_dense_equiv_tflops": round(flops / (gemm_us * 1e-6) / 1e12, 3),
         "logical_bytes": int(logical),
         "physical_bytes": int(phys),

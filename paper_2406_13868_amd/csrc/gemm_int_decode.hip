@@ -3,22 +3,24 @@
 // with both branches read from one stream of 32-bit group words.
 //
 // At M <= 8 the product is bound by the HBM stream of packed weights (about
-// 5 bits per weight).  The kernel is shaped so that every wave owns complete
-// outputs and can leave as soon as its own stream is consumed:
+// 5 bits per weight) and by the fixed cost of a launch, so the kernel keeps
+// every wave's dependency chain short:
 //
-//   * one wave per 4-row slice of a 32-row tile, over the whole of K (a
-//     4096-row layer runs 1024 waves, one per SIMD); four slices per
-//     workgroup, which share nothing but the per-token activation scales;
+//   * four waves per 4-row slice of a 32-row tile split K into parts; each
+//     owns S consecutive "steps" of eight 128-K chunks (S = ceil(K / 4096)
+//     for K <= 32768); two slices (eight waves) per workgroup, and the
+//     workgroups of one XCD take a contiguous range of slices, so the
+//     128-byte lines of block scales that two slices share are fetched once;
 //   * lane l works on row (l & 3) of the slice, on half j = (l>>2)&1 of the
-//     16-K scale blocks of a chunk, and on chunk cc = l>>3 of an 8-chunk
-//     step; one load instruction reads eight 128-byte runs of group words;
-//   * the weight stream of the first four steps is requested before
-//     anything else and every step requests the one four ahead;
-//   * the activations of all tokens are requested before the weight stream
-//     (the load counter is in order, so waiting for them never waits for the
-//     weights) and stored in LDS behind the one barrier of the kernel, copied
-//     from Xq or, in the fused form, quantized there with the arithmetic of
-//     the stand-alone activation kernel after a workgroup-wide amax;
+//     16-K scale blocks of a chunk, and on chunk cc = l>>3 of a step; one
+//     load instruction reads eight 128-byte runs of group words;
+//   * a wave requests its activations first and then all of its weight
+//     stream (S steps, three loads each), so the load counter lets it compute
+//     each step as soon as that step has landed;
+//   * each wave keeps the int8 activations of its own part of K in a private
+//     LDS region (chunk stride 144 bytes, plus one zero chunk that stands in
+//     for the chunks past K); only the fused form, which first needs the amax
+//     of the whole token, synchronises the workgroup before the products;
 //   * each group word becomes a v_perm_b32 selector that gathers the four
 //     activations its slots need (three inliers, one outlier); v_dot4_i32_i8
 //     multiplies them with the inlier codes (kept at the top nibble of each
@@ -26,8 +28,9 @@
 //     block, scaled by the block's fp16 scale into the fp32 accumulator; the
 //     outlier products are summed in fp32 (e4m3) or exactly in int32 (int8)
 //     and added with the row's outlier scale at the end;
-//   * the 16 lanes of a row are summed with a fixed butterfly: the result
-//     does not depend on timing.
+//   * the 16 lanes of a row are summed with DPP rotations and permlane swaps
+//     and the parts of K in a fixed order through LDS: the result does not
+//     depend on timing.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -35,17 +38,19 @@
 namespace sdq {
 namespace {
 
-constexpr int kSlices = 4;                     // waves (4-row slices) per workgroup
-constexpr int kThreads = kSlices * 64;
+constexpr int kKSplit = 4;                     // waves per 4-row slice (each owns a part of K)
 constexpr int kSliceRows = 4;
+constexpr int kWavesPerWG = 8;                 // slices x K parts per workgroup (LDS permitting)
+constexpr int kMaxLdsBytes = 64 * 1024;
 constexpr int kStepChunks = 8;                 // 128-K chunks per wave step
-constexpr int kDepth = 4;                      // steps in flight per wave
-// The activations of all M tokens sit in LDS, read in 16-element pieces:
-// at most kMaxPieces pieces per thread, i.e. M*K <= 16*kThreads*kMaxPieces.
-constexpr int kMaxPieces = 8;
+constexpr int kMaxSteps = 8;                   // steps per wave: K <= 4 * 8 * 8 * 128
+constexpr int kXStride = 144;                  // LDS bytes per 128-K chunk of one token
 constexpr int kFusedMaxM = 2;  // the fused form serves the decode sizes sdq_linear sends here
-// v_mul_u32_u24 magic that moves bits 3, 11, 19 of a group word to 24, 25, 26.
+// v_mul_u32_u24 magic that moves bits 3, 11, 19 of a group word to 24, 25, 26
+// (it also leaves copies at bits 10, 17, 18, inside the inlier position mask,
+// which the bitfield insert replaces).
 constexpr uint32_t kOutPosMagic = (1u << 21) | (1u << 14) | (1u << 7);
+constexpr uint32_t kInPosMask = 0x00070707u;
 
 struct DecodeArgs {
   const uint8_t* Xq;   // [M][K] int8 (unfused form)
@@ -59,34 +64,52 @@ struct DecodeArgs {
   int64_t scales_off, rows_off;
 };
 
-__device__ __forceinline__ float f16lo(uint32_t v) {
-  return (float)__builtin_bit_cast(_Float16, (unsigned short)(v & 0xFFFFu));
-}
-__device__ __forceinline__ float f16hi(uint32_t v) {
-  return (float)__builtin_bit_cast(_Float16, (unsigned short)(v >> 16));
+// LDS bytes of one wave's activation region: MT tokens x (8S chunks + the zero chunk).
+__host__ __device__ constexpr int wave_lds_bytes(int MT, int S) {
+  return MT * (S * kStepChunks + 1) * kXStride;
 }
 
-// Eight consecutive activations widened to fp32.
-template <bool BF16>
-__device__ __forceinline__ void load_x8(const void* X, size_t idx, float (&v)[8]) {
-  if constexpr (BF16) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(X) + idx);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = __uint_as_float(w[i] << 16);
-      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-    }
-  } else {
-    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(X) + idx);
-    const float4 b = *reinterpret_cast<const float4*>(static_cast<const float*>(X) + idx + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-  }
+// Perm selector of a group word: positions of the three inlier slots in
+// bytes 0-2, the outlier position (bits 3, 11, 19 gathered by one 24-bit
+// multiply) in byte 3.  The bitfield insert is spelled out because the
+// compiler otherwise splits it into two ops.
+__device__ __forceinline__ uint32_t perm_selector(uint32_t w) {
+  const uint32_t u = __umul24(w & 0x00080808u, kOutPosMagic);
+  uint32_t sel;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(sel) : "s"(kInPosMask), "v"(w), "v"(u));
+  return sel;
+}
+
+// Sum over the 16 lanes l' of the wave with l' = l (mod 4): two DPP row
+// rotations inside each row of 16 lanes, then the rows are exchanged with
+// the permlane swaps.  Every lane ends with the sum of its residue class,
+// in an order that does not depend on timing.
+__device__ __forceinline__ float sum_lanes_mod4(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false));  // row_ror:4
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));  // row_ror:8
+  const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(p16[0]) + __uint_as_float(p16[1]);
+  const auto p32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
+}
+
+// Workgroup b runs on XCD b % 8; give every XCD a contiguous range of the G
+// workgroups' work, so that neighbouring slices (which share the 128-byte
+// lines of a tile's block scales) meet in one L2.
+__device__ __forceinline__ int xcd_contiguous(int b, int G) {
+  const int x = b & 7, i = b >> 3, q = G >> 3, rem = G & 7;
+  return x * q + min(x, rem) + i;
+}
+
+__device__ __forceinline__ _Float16 f16lo(uint32_t v) {
+  return __builtin_bit_cast(_Float16, (unsigned short)(v & 0xFFFFu));
+}
+__device__ __forceinline__ _Float16 f16hi(uint32_t v) {
+  return __builtin_bit_cast(_Float16, (unsigned short)(v >> 16));
 }
 
 // int8 codes of eight activations: clamp(rne(x * inv), +-127), one fp32 multiply each.
-__device__ __forceinline__ uint2 quant8(const float (&v)[8], float inv) {
+__device__ __forceinline__ uint2 quant8(const float* v, float inv) {
   uint32_t lo = 0, hi = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -104,38 +127,38 @@ struct StepBuf {
 };
 
 // FUSE: 0 = activations from Xq/s_a, 1 = quantize fp32 X, 2 = quantize bf16 X.
-template <int MT, bool OUT_INT8, int FUSE, int PPT, int KSPLIT>
-__global__ __launch_bounds__(kThreads) void int_decode_kernel(DecodeArgs a) {
-  extern __shared__ __align__(16) uint8_t xs[];  // [MT][K] int8 activations
-  __shared__ float red[kSlices][kDecodeMaxM];
+template <int MT, bool OUT_INT8, int FUSE, int S, int KS, int SPW>
+__global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a) {
+  constexpr int kWG = SPW * KS;                  // waves per workgroup
+  extern __shared__ __align__(16) uint8_t xs[];  // [wave][MT][8S + 1][kXStride]
+  __shared__ float red[kWG][kDecodeMaxM];
   __shared__ float s_scale[kDecodeMaxM];
-  __shared__ float part[kSlices][kDecodeMaxM][kSliceRows];  // second K half of a slice
+  __shared__ float part[SPW][KS][kDecodeMaxM][kSliceRows];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int K = a.K, M = a.M;
+  const int ws = wave / KS, kq = wave % KS;  // slice in the workgroup, part of K
+  const int K = a.K, M = a.M, KC = a.n_chunks;
   const int r = lane & 3, j = (lane >> 2) & 1, cc = lane >> 3;
-  // KSPLIT = 2: two waves per slice, each over half of the steps
-  const int slices_per_wg = kSlices / KSPLIT;
-  const int wslice = wave % slices_per_wg, khalf = wave / slices_per_wg;
-  const int slice = blockIdx.x * slices_per_wg + wslice;  // 4-row slice of the layer
-  const int t = slice >> 3;                                // 32-row tile
-  const int row = ((slice & 7) << 2) + r;                  // row inside the tile
-  const int KC = a.n_chunks;
-  const int all_steps = (KC + kStepChunks - 1) / kStepChunks;
-  const int s_begin = KSPLIT == 1 ? 0 : (khalf == 0 ? 0 : (all_steps + 1) / 2);
-  const int s_end = KSPLIT == 1 ? all_steps : (khalf == 0 ? (all_steps + 1) / 2 : all_steps);
+  const int slice = xcd_contiguous(blockIdx.x, gridDim.x) * SPW + ws;  // 4-row slice of the layer
+  const int t = slice >> 3;                 // 32-row tile
+  const int row = ((slice & 7) << 2) + r;   // row inside the tile
+  const int chunk0 = kq * S * kStepChunks;  // first chunk of this wave's part of K
+  constexpr int kTokBytes = (S * kStepChunks + 1) * kXStride;
+  uint8_t* xw = xs + wave * wave_lds_bytes(MT, S);
 
-  // ---- 1. the activations first: their wait must not drain the weight loads
-  //         (the load counter is in order), so they are requested before them.
-  //         16 bytes of Xq, or 16 elements of X, per thread and piece.
-  const int pieces = (MT * K) >> 4;
-  uint4 xr[PPT][FUSE == 1 ? 4 : FUSE == 2 ? 2 : 1];
+  // ---- 1. this part's activations, requested first (the load counter is
+  //         in order: waiting for them never waits for the weight stream).
+  //         Piece i of a lane covers 16 bytes (or elements) of token i / S.
+  constexpr int kPieces = MT * S;
+  constexpr int kU = FUSE == 1 ? 4 : FUSE == 2 ? 2 : 1;
+  uint4 xr[kPieces][kU];
 #pragma unroll
-  for (int i = 0; i < PPT; ++i) {
-    const int pc = tid + i * kThreads;
-    const int m = (pc << 4) / K;
-    if (pc < pieces && m < M) {
-      const size_t e = size_t(pc) << 4;  // element index in [M][K]
+  for (int i = 0; i < kPieces; ++i) {
+    const int m = i / S;
+    const int off = ((i % S) * 64 + lane) * 16;  // byte (element) offset in the part
+    const int k = chunk0 * kChunkK + off;
+    if (m < M && k < K) {
+      const size_t e = size_t(m) * K + k;
       if constexpr (FUSE == 0) {
         xr[i][0] = *reinterpret_cast<const uint4*>(a.Xq + e);
       } else if constexpr (FUSE == 1) {
@@ -147,45 +170,54 @@ __global__ __launch_bounds__(kThreads) void int_decode_kernel(DecodeArgs a) {
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < (FUSE == 1 ? 4 : FUSE == 2 ? 2 : 1); ++u) xr[i][u] = make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kU; ++u) xr[i][u] = make_uint4(0, 0, 0, 0);
     }
   }
 
-  // ---- 2. the weight stream: the first kDepth steps of this wave.  Loads
-  //         are unconditional (addresses clamped into the tile), so the
-  //         prefetch ring needs no copies; the ragged last step is masked.
+  // ---- 2. the whole weight stream of the wave.  Chunks past K re-read the
+  //         last chunk of the tile (in bounds) and meet the zero chunk.
   const uint8_t* tbase = a.blob + size_t(t) * KC * kWordBytesPerTC;
   const uint8_t* sbase = a.blob + a.scales_off + size_t(t) * KC * kIntScaleBytesPerTC;
   const uint32_t woff = uint32_t(row * 2 + j) * 16, soff = uint32_t(row * 16 + j * 8);
-  auto load_step = [&](int s, StepBuf& b) {
-    // past the wave's own steps: re-read its last one (a cache hit), never
-    // the other K half's
-    const int c = min(min(s, s_end - 1) * kStepChunks + cc, KC - 1);
-    const uint8_t* wp = tbase + (uint32_t(c) * kWordBytesPerTC + woff);
-    b.w0 = *reinterpret_cast<const uint4*>(wp);
-    b.w1 = *reinterpret_cast<const uint4*>(wp + 1024);  // h = 1: 32 rows x 32 bytes further
-    b.sc = *reinterpret_cast<const uint2*>(sbase + (uint32_t(c) * kIntScaleBytesPerTC + soff));
-  };
-  StepBuf buf[kDepth];
+  StepBuf buf[S];
 #pragma unroll
-  for (int d = 0; d < kDepth; ++d) load_step(s_begin + d, buf[d]);
+  for (int d = 0; d < S; ++d) {
+    const int c = min(chunk0 + d * kStepChunks + cc, KC - 1);
+    const uint8_t* wp = tbase + (uint32_t(c) * kWordBytesPerTC + woff);
+    buf[d].w0 = *reinterpret_cast<const uint4*>(wp);
+    buf[d].w1 = *reinterpret_cast<const uint4*>(wp + 1024);  // h = 1: 32 rows x 32 bytes further
+    buf[d].sc = *reinterpret_cast<const uint2*>(sbase + (uint32_t(c) * kIntScaleBytesPerTC + soff));
+  }
   // 16 * s_o: the inlier dot products carry a factor 16, folded out at the end.
   const float so16 = 16.f * reinterpret_cast<const float*>(a.blob + a.rows_off)[t * kTileN + row];
 
-  // ---- 3. activations into LDS
+  // LDS address of piece i of this lane inside the wave's region
+  auto lds_piece = [&](int i) -> uint8_t* {
+    const int m = i / S;
+    const int off = ((i % S) * 64 + lane) * 16;
+    return xw + m * kTokBytes + (off >> 7) * kXStride + (off & 127);
+  };
+  // the zero chunk of every token (9 pieces of 16 bytes, stride padding included)
+  for (int z = lane; z < MT * 9; z += 64) {
+    const int m = z / 9, u = z % 9;
+    *reinterpret_cast<uint4*>(xw + m * kTokBytes + S * kStepChunks * kXStride + u * 16) = make_uint4(0, 0, 0, 0);
+  }
+
+  // ---- 3. activations into the wave's LDS region
   if constexpr (FUSE == 0) {
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int pc = tid + i * kThreads;
-      if (pc < pieces) *reinterpret_cast<uint4*>(xs + (size_t(pc) << 4)) = xr[i][0];
-    }
+    for (int i = 0; i < kPieces; ++i) *reinterpret_cast<uint4*>(lds_piece(i)) = xr[i][0];
     if (tid < kDecodeMaxM) s_scale[tid] = tid < M ? a.s_a[tid] : 0.f;
+    // the products below read only this wave's region (plus s_scale at the end)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   } else {
     // per-token quantization with the arithmetic of the activation kernel:
     // a = max|x|, s_a = a/127, inv = 127/a, q = clamp(rne(x*inv), +-127)
-    float v[PPT][16];
+    float v[kPieces][16];
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
+    for (int i = 0; i < kPieces; ++i) {
       if constexpr (FUSE == 1) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -204,20 +236,15 @@ __global__ __launch_bounds__(kThreads) void int_decode_kernel(DecodeArgs a) {
         }
       }
     }
-    // a piece never straddles two tokens (K is a multiple of 16)
     float amax[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) amax[m] = 0.f;
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int pc = tid + i * kThreads;
-      const int m = (pc << 4) / K;
+    for (int i = 0; i < kPieces; ++i) {
       float pm = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) pm = fmaxf(pm, fabsf(v[i][e]));
-#pragma unroll
-      for (int mm = 0; mm < MT; ++mm)
-        if (mm == m) amax[mm] = fmaxf(amax[mm], pm);
+      amax[i / S] = fmaxf(amax[i / S], pm);
     }
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
@@ -231,7 +258,7 @@ __global__ __launch_bounds__(kThreads) void int_decode_kernel(DecodeArgs a) {
     for (int m = 0; m < MT; ++m) {
       float am = red[0][m];
 #pragma unroll
-      for (int w = 1; w < kSlices; ++w) am = fmaxf(am, red[w][m]);
+      for (int w = 1; w < kWG; ++w) am = fmaxf(am, red[w][m]);  // each slice covers all of K
       inv[m] = am > 0.f ? 127.f / am : 0.f;
       if (tid == 0) {
         const float sc = am / 127.f;
@@ -240,142 +267,150 @@ __global__ __launch_bounds__(kThreads) void int_decode_kernel(DecodeArgs a) {
       }
     }
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int pc = tid + i * kThreads;
-      if (pc >= pieces) continue;
-      const int m = (pc << 4) / K;
-      float iv = 0.f;
-#pragma unroll
-      for (int mm = 0; mm < MT; ++mm)
-        if (mm == m) iv = inv[mm];
-      float lo8[8], hi8[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) { lo8[e] = v[i][e]; hi8[e] = v[i][8 + e]; }
-      const uint2 q0 = quant8(lo8, iv), q1 = quant8(hi8, iv);
+    for (int i = 0; i < kPieces; ++i) {
+      const uint2 q0 = quant8(&v[i][0], inv[i / S]), q1 = quant8(&v[i][8], inv[i / S]);
       const uint4 q = make_uint4(q0.x, q0.y, q1.x, q1.y);
-      *reinterpret_cast<uint4*>(xs + (size_t(pc) << 4)) = q;
-      if (blockIdx.x == 0 && m < M) *reinterpret_cast<uint4*>(a.Xq_out + (size_t(pc) << 4)) = q;
+      *reinterpret_cast<uint4*>(lds_piece(i)) = q;
+      const int m = i / S;
+      const int k = chunk0 * kChunkK + ((i % S) * 64 + lane) * 16;
+      if (blockIdx.x == 0 && m < M && k < K)
+        *reinterpret_cast<uint4*>(a.Xq_out + size_t(m) * K + k) = q;
     }
+    __syncthreads();
   }
-  __syncthreads();
 
-  // ---- 4. the steps
+  // ---- 4. the products, one step at a time as the stream lands
   float acc[MT], acco[MT];
   int po[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) { acc[m] = 0.f; acco[m] = 0.f; po[m] = 0; }
 
-  for (int s0 = s_begin; s0 < s_end; s0 += kDepth) {
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-      const int s = s0 + d;
-      if (s >= s_end) break;  // wave-uniform
-      const StepBuf cur = buf[d];
-      load_step(s + kDepth, buf[d]);
-      const int c = s * kStepChunks + cc;
-      const bool valid = c < KC;
-      const uint32_t wa[4] = {valid ? cur.w0.x : 0u, valid ? cur.w0.y : 0u, valid ? cur.w0.z : 0u, valid ? cur.w0.w : 0u};
-      const uint32_t wb[4] = {valid ? cur.w1.x : 0u, valid ? cur.w1.y : 0u, valid ? cur.w1.z : 0u, valid ? cur.w1.w : 0u};
-      const float scl[4] = {f16lo(cur.sc.x), f16hi(cur.sc.x), f16lo(cur.sc.y), f16hi(cur.sc.y)};
-      const uint8_t* xbase = xs + uint32_t(min(c, KC - 1)) * kChunkK;
+  for (int d = 0; d < S; ++d) {
+    if (chunk0 + d * kStepChunks >= KC) break;  // wave-uniform: the part starts past K
+    const int c = chunk0 + d * kStepChunks + cc;
+    const int lc = c < KC ? d * kStepChunks + cc : S * kStepChunks;  // past K: the zero chunk
+    const uint8_t* xbase = xw + lc * kXStride;
+    const StepBuf& cur = buf[d];
+    const uint32_t wa[4] = {cur.w0.x, cur.w0.y, cur.w0.z, cur.w0.w};
+    const uint32_t wb[4] = {cur.w1.x, cur.w1.y, cur.w1.z, cur.w1.w};
+    const _Float16 scl[4] = {f16lo(cur.sc.x), f16hi(cur.sc.x), f16lo(cur.sc.y), f16hi(cur.sc.y)};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int kb = 4 * j + q;  // 16-K block inside the chunk
-        uint32_t sel[2], wi[2], wo_i8[2];
-        float wo_f[2];
+    for (int q = 0; q < 4; ++q) {
+      const int kb = 4 * j + q;  // 16-K block inside the chunk
+      uint32_t sel[2], wi[2], wo_i8[2];
+      float wo_f[2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const uint32_t w = h ? wb[q] : wa[q];
-          const uint32_t u = __umul24(w & 0x00080808u, kOutPosMagic);
-          sel[h] = (u & 0x07000000u) | (w & 0x00070707u);
-          wi[h] = w & 0x00F0F0F0u;
-          if constexpr (OUT_INT8) wo_i8[h] = w & 0xFF000000u;
-          else wo_f[h] = __builtin_amdgcn_cvt_f32_fp8(int(w), 3);
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t w = h ? wb[q] : wa[q];
+        sel[h] = perm_selector(w);
+        wi[h] = w & 0x00F0F0F0u;
+        if constexpr (OUT_INT8) wo_i8[h] = w & 0xFF000000u;
+        else wo_f[h] = __builtin_amdgcn_cvt_f32_fp8(int(w), 3);
+      }
+      const uint8_t* xk = xbase + kb * 16;
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const uint4 xv = *reinterpret_cast<const uint4*>(xk + m * kTokBytes);
+        const uint32_t g0 = __builtin_amdgcn_perm(xv.y, xv.x, sel[0]);
+        const uint32_t g1 = __builtin_amdgcn_perm(xv.w, xv.z, sel[1]);
+        int P = __builtin_amdgcn_sdot4(int(g0), int(wi[0]), 0, false);
+        P = __builtin_amdgcn_sdot4(int(g1), int(wi[1]), P, false);
+        if constexpr (OUT_INT8) {
+          po[m] = __builtin_amdgcn_sdot4(int(g0), int(wo_i8[0]), po[m], false);
+          po[m] = __builtin_amdgcn_sdot4(int(g1), int(wo_i8[1]), po[m], false);
+        } else {
+          acco[m] = fmaf((float)(int(g0) >> 24), wo_f[0], acco[m]);
+          acco[m] = fmaf((float)(int(g1) >> 24), wo_f[1], acco[m]);
         }
-        const uint8_t* xk = xbase + kb * 16;
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const uint4 xv = *reinterpret_cast<const uint4*>(xk + uint32_t(m) * K);
-          const uint32_t g0 = __builtin_amdgcn_perm(xv.y, xv.x, sel[0]);
-          const uint32_t g1 = __builtin_amdgcn_perm(xv.w, xv.z, sel[1]);
-          int P = __builtin_amdgcn_sdot4(int(g0), int(wi[0]), 0, false);
-          P = __builtin_amdgcn_sdot4(int(g1), int(wi[1]), P, false);
-          if constexpr (OUT_INT8) {
-            po[m] = __builtin_amdgcn_sdot4(int(g0), int(wo_i8[0]), po[m], false);
-            po[m] = __builtin_amdgcn_sdot4(int(g1), int(wo_i8[1]), po[m], false);
-          } else {
-            acco[m] = fmaf((float)(int(g0) >> 24), wo_f[0], acco[m]);
-            acco[m] = fmaf((float)(int(g1) >> 24), wo_f[1], acco[m]);
-          }
-          acc[m] = fmaf((float)P, scl[q], acc[m]);
-        }
+        acc[m] = fmaf((float)P, (float)scl[q], acc[m]);
       }
     }
   }
 
-  // ---- 5. sum the 16 lanes of a row (j, cc) and fold in the outlier branch
+  // ---- 5. sum the 16 lanes of a row (j, cc), fold in the outlier branch,
+  //         then the parts of K in order
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     if constexpr (OUT_INT8) acco[m] = (float)po[m];
-    float v = fmaf(acco[m], so16, acc[m]);
-    v += __shfl_xor(v, 4, 64);
-    v += __shfl_xor(v, 8, 64);
-    v += __shfl_xor(v, 16, 64);
-    v += __shfl_xor(v, 32, 64);
-    acc[m] = v;
+    const float v = sum_lanes_mod4(fmaf(acco[m], so16, acc[m]));
+    if (lane < kSliceRows) part[ws][kq][m][lane] = v;
   }
+  __syncthreads();
   const int n = t * kTileN + row;
-  if constexpr (KSPLIT == 2) {
-    // the second half hands its sums to the first through LDS (fixed order)
-    if (khalf == 1 && lane < kSliceRows) {
+  if (kq == 0 && lane < kSliceRows && n < a.N) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m) part[wslice][m][lane] = acc[m];
+    for (int m = 0; m < MT; ++m) {
+      float v = part[ws][0][m][r];
+#pragma unroll
+      for (int p = 1; p < KS; ++p) v += part[ws][p][m][r];
+      if (m < M) a.Y[size_t(m) * a.N + n] = s_scale[m] * (v * 0.0625f);
     }
-    __syncthreads();
-    if (khalf == 1) return;
-#pragma unroll
-    for (int m = 0; m < MT; ++m) acc[m] += part[wslice][m][r];
-  }
-  if (lane < kSliceRows && n < a.N) {
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-      if (m < M) a.Y[size_t(m) * a.N + n] = s_scale[m] * (acc[m] * 0.0625f);
   }
 }
 
-template <int MT, int FUSE, int PPT>
-hipError_t launch_ppt(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
+// steps per wave for K (K is a multiple of 128) when KS waves share a slice
+int steps_for(int64_t K, int KS) {
+  const int64_t all_steps = (K / kChunkK + kStepChunks - 1) / kStepChunks;
+  return int((all_steps + KS - 1) / KS);
+}
+
+// K split of a slice: kKSplit waves, more (up to 4) where one wave's steps
+// would not fit MT * S <= kMaxSteps (activation registers and LDS)
+int ks_for(int64_t MT, int64_t K) {
+  for (int ks = kKSplit; ks < 4; ks *= 2)
+    if (MT * steps_for(K, ks) <= kMaxSteps) return ks;
+  return 4;
+}
+
+// slices per workgroup: kWavesPerWG / KS, fewer where the activation regions
+// would not fit the workgroup's LDS; it divides the 8 slices of a tile
+constexpr int spw_for(int MT, int S, int KS) {
+  int spw = kWavesPerWG / KS;
+  while (spw > 1 && spw * KS * wave_lds_bytes(MT, S) > kMaxLdsBytes) spw /= 2;
+  return spw;
+}
+
+template <int MT, int FUSE, int S, int KS>
+hipError_t launch_s(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
+  constexpr int SPW = spw_for(MT, S, KS);
+  static_assert((kTileN / kSliceRows) % SPW == 0, "slices per workgroup must divide a tile");
   const Layout L = make_layout(false, a.N, a.K);
-  // slices of 4 rows (the last tile may be padded); a workgroup of 4 waves
-  // takes 4 slices, or 2 slices with two waves each when there are too few
-  // slices to give every SIMD two waves
-  const int64_t slices = L.n_tiles * (kTileN / kSliceRows);
-  const size_t lds = size_t(MT) * a.K;
-  const bool split = slices < 2048 && (a.K / kChunkK) >= 2 * kStepChunks;
-  const dim3 block(kThreads);
-  if (split) {
-    const dim3 grid(unsigned(slices / (kSlices / 2)));
-    if (c.fmt_o == SDQ_FMT_INT8)
-      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, PPT, 2>), grid, block, lds, st, a);
-    else
-      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, PPT, 2>), grid, block, lds, st, a);
-  } else {
-    const dim3 grid(unsigned(slices / kSlices));
-    if (c.fmt_o == SDQ_FMT_INT8)
-      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, PPT, 1>), grid, block, lds, st, a);
-    else
-      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, PPT, 1>), grid, block, lds, st, a);
-  }
+  const dim3 grid(unsigned(L.n_tiles * (kTileN / kSliceRows) / SPW));
+  const dim3 block(SPW * KS * 64);
+  const size_t lds = size_t(SPW) * KS * wave_lds_bytes(MT, S);
+  if (c.fmt_o == SDQ_FMT_INT8)
+    hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW>), grid, block, lds, st, a);
+  else
+    hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW>), grid, block, lds, st, a);
   return hipGetLastError();
+}
+
+// MT * S <= 8 keeps the activation registers and LDS bounded (decode_fits).
+template <int MT, int FUSE, int KS>
+hipError_t launch_ks(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
+  switch (steps_for(a.K, KS)) {
+    case 1: return launch_s<MT, FUSE, 1, KS>(c, a, st);
+    case 2: if constexpr (MT <= 4) return launch_s<MT, FUSE, 2, KS>(c, a, st); break;
+    case 3: if constexpr (MT <= 2) return launch_s<MT, FUSE, 3, KS>(c, a, st); break;
+    case 4: if constexpr (MT <= 2) return launch_s<MT, FUSE, 4, KS>(c, a, st); break;
+    case 5: if constexpr (MT <= 1) return launch_s<MT, FUSE, 5, KS>(c, a, st); break;
+    case 6: if constexpr (MT <= 1) return launch_s<MT, FUSE, 6, KS>(c, a, st); break;
+    case 7: if constexpr (MT <= 1) return launch_s<MT, FUSE, 7, KS>(c, a, st); break;
+    case 8: if constexpr (MT <= 1) return launch_s<MT, FUSE, 8, KS>(c, a, st); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;  // excluded by decode_fits
 }
 
 template <int MT, int FUSE>
 hipError_t launch_mt(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
-  const int64_t per_thread = (int64_t(MT) * a.K / 16 + kThreads - 1) / kThreads;
-  if (per_thread <= 1) return launch_ppt<MT, FUSE, 1>(c, a, st);
-  if (per_thread <= 2) return launch_ppt<MT, FUSE, 2>(c, a, st);
-  if (per_thread <= 4) return launch_ppt<MT, FUSE, 4>(c, a, st);
-  return launch_ppt<MT, FUSE, 8>(c, a, st);
+  const int ks = ks_for(MT, a.K);
+  if constexpr (kKSplit <= 1)
+    if (ks == 1) return launch_ks<MT, FUSE, 1>(c, a, st);
+  if constexpr (kKSplit <= 2)
+    if (ks == 2) return launch_ks<MT, FUSE, 2>(c, a, st);
+  return launch_ks<MT, FUSE, 4>(c, a, st);
 }
 
 template <int FUSE>
@@ -394,8 +429,9 @@ hipError_t launch_fuse(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
 bool decode_fused_fits(int64_t M, int64_t K) { return M <= kFusedMaxM && decode_fits(M, K); }
 
 bool decode_fits(int64_t M, int64_t K) {
+  if (M < 1 || M > kDecodeMaxM || K < kChunkK) return false;
   const int64_t mt = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8;
-  return M <= kDecodeMaxM && mt * K <= int64_t(16) * kThreads * kMaxPieces;
+  return mt * steps_for(K, 4) <= kMaxSteps;
 }
 
 hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
