@@ -81,6 +81,18 @@ __device__ __forceinline__ h8 inlier_f16(uint32_t w) {
   return __builtin_bit_cast(h8, out);
 }
 
+// Exact split of the scaled inlier fragment q * s (q an int4 code, s the
+// block's fp16 scale) into two fp16 fragments: hi = f16(q*s) and the residual
+// lo = q*s - hi, which one fused multiply-add produces exactly (q*s has at
+// most 14 significant bits and is a multiple of the lowest bit of s, so the
+// residual is an fp16 number).  Two MFMAs on hi and lo then add q*s*a
+// exactly into the fp32 accumulator, with no per-block scaling of partials.
+__device__ __forceinline__ void scaled_hi_lo(h8 q, _Float16 s, h8& hi, h8& lo) {
+  const h8 sv = {s, s, s, s, s, s, s, s};
+  hi = q * sv;
+  lo = __builtin_elementwise_fma(q, sv, -hi);
+}
+
 // Dense fp16 outlier fragment of one group word (one non-zero at most).
 template <bool OUT_INT8>
 __device__ __forceinline__ h8 outlier_f16(uint32_t w) {
@@ -174,21 +186,21 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
     if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
 #pragma unroll 2
     for (int kb = 0; kb < 8; ++kb) {
-      const h8 bi = inlier_f16<NI>(wv[kb]);
-      const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
       const uint32_t sw = sv[kb >> 1];
-      const float s = (float)__builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      h8 bh, bl;
+      scaled_hi_lo(inlier_f16<NI>(wv[kb]), s, bh, bl);
+      const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
+      h8 av[MS];
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) {
-        const h8 av = *reinterpret_cast<const h8*>(&xs[buf][(ms * 32 + col) * kLdsRow + kb * 16 + h * 8]);
-        f16v zero;
+      for (int ms = 0; ms < MS; ++ms)
+        av[ms] = *reinterpret_cast<const h8*>(&xs[buf][(ms * 32 + col) * kLdsRow + kb * 16 + h * 8]);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) zero[e] = 0.f;
-        const f16v P = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bi, zero, 0, 0, 0);
-        acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bo, acco[ms], 0, 0, 0);
+      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bh, acc[ms], 0, 0, 0);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[ms][e] = fmaf(P[e], s, acc[ms][e]);
-      }
+      for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
     }
     if (c + 1 < KC) {
       store_x(buf ^ 1);
@@ -210,13 +222,19 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
 }
 
 // Split-K form for few tokens (M <= 64): one 32-row tile of W per workgroup,
-// its NW waves take interleaved 128-K chunks and each lane reads its 8-byte
-// A-fragment pieces of Xq straight from L2 (no LDS staging), converting them
-// to fp16 in registers; the wave partials are summed through LDS with a
-// fixed-order tree at the end.  This keeps NT*NW waves in flight where the
-// tiled form above would run only NT/4 workgroups.
+// its NW waves take interleaved 128-K chunks (two chunks in flight per wave)
+// and read their activations straight from L2 into registers; the wave
+// partials are summed through LDS with a fixed-order tree at the end.  This
+// keeps NT*NW waves in flight where the tiled form above would run only NT/4
+// workgroups.
+//
+// Because the inlier scales travel inside the hi/lo fragments, the K order of
+// an MFMA need not follow the 16-K scale blocks: MFMA i (0..7) of a chunk
+// takes group i on lane half 0 and group 8 + i on lane half 1, so that each
+// lane's activations for a chunk are 64 contiguous bytes (four 16-byte loads
+// per 32-token sub-tile) and its group words two 16-byte runs.
 template <int MS, int NI, bool OUT_INT8, int NW>
-__global__ __launch_bounds__(NW * 64) void int_mfma_splitk_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a) {
   constexpr int BM = 32 * MS;
   __shared__ float red[NW / 2][16][64];
 
@@ -226,26 +244,33 @@ __global__ __launch_bounds__(NW * 64) void int_mfma_splitk_kernel(MfmaArgs a) {
   const int tile = blockIdx.x;
   const int KC = a.n_chunks;
 
-  const uint8_t* wbase = a.blob + size_t(tile) * KC * kWordBytesPerTC + size_t(lane) * 32;
+  // groups 8h + i of row col: word ((h'*32 + col)*2 + h)*4 + q with i = 2q + h'
+  const uint8_t* wbase = a.blob + size_t(tile) * KC * kWordBytesPerTC + size_t(col * 2 + h) * 16;
   const uint8_t* sbase = a.blob + a.scales_off + size_t(tile) * KC * kIntScaleBytesPerTC + col * 16;
+  const uint8_t* xrow[MS];
+  bool mok[MS];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms) {
+    const int m = m0 + ms * 32 + col;
+    mok[ms] = m < a.M;
+    xrow[ms] = a.Xq + size_t(mok[ms] ? m : 0) * a.K + h * 64;
+  }
 
-  // lane (col, h) of sub-tile ms reads row m0 + 32*ms + col, K bytes 16*kb + 8*h .. +8
-  uint2 xr[MS][8];
-  auto load_x = [&](int c) {
-#pragma unroll
-    for (int ms = 0; ms < MS; ++ms) {
-      const int m = m0 + ms * 32 + col;
-      const uint8_t* xp = a.Xq + size_t(m < a.M ? m : 0) * a.K + c * kChunkK + h * 8;
-#pragma unroll
-      for (int kb = 0; kb < 8; ++kb)
-        xr[ms][kb] = m < a.M ? *reinterpret_cast<const uint2*>(xp + kb * 16) : make_uint2(0, 0);
-    }
+  struct Stage {
+    uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's eight fp16 block scales
+    uint4 x[MS][4];     // 64 activation bytes per sub-tile
   };
-  uint4 wr0, wr1, sr;
-  auto load_w = [&](int c) {
-    wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
-    wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 16);
-    sr = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kIntScaleBytesPerTC);
+  auto load = [&](int c, Stage& st) {
+    const uint8_t* wp = wbase + size_t(c) * kWordBytesPerTC;
+    st.w0 = *reinterpret_cast<const uint4*>(wp);
+    st.w1 = *reinterpret_cast<const uint4*>(wp + 1024);
+    st.sc = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kIntScaleBytesPerTC);
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        st.x[ms][u] = mok[ms] ? *reinterpret_cast<const uint4*>(xrow[ms] + size_t(c) * kChunkK + u * 16)
+                              : make_uint4(0, 0, 0, 0);
   };
 
   f16v acc[MS], acco[MS];
@@ -254,39 +279,57 @@ __global__ __launch_bounds__(NW * 64) void int_mfma_splitk_kernel(MfmaArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { acc[s][e] = 0.f; acco[s][e] = 0.f; }
 
-  int c = wave;
-  if (c < KC) { load_x(c); load_w(c); }
-  for (; c < KC; c += NW) {
-    uint2 xc[MS][8];
+  auto compute = [&](const Stage& st) {
+    const uint32_t wv[2][4] = {{st.w0.x, st.w0.y, st.w0.z, st.w0.w}, {st.w1.x, st.w1.y, st.w1.z, st.w1.w}};
+    const uint32_t sv[4] = {st.sc.x, st.sc.y, st.sc.z, st.sc.w};
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-      for (int kb = 0; kb < 8; ++kb) xc[ms][kb] = xr[ms][kb];
-    const uint32_t wv[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
-    const uint32_t sv[4] = {sr.x, sr.y, sr.z, sr.w};
-    if (c + NW < KC) { load_x(c + NW); load_w(c + NW); }
-#pragma unroll 2
-    for (int kb = 0; kb < 8; ++kb) {
-      const h8 bi = inlier_f16<NI>(wv[kb]);
-      const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
-      const uint32_t sw = sv[kb >> 1];
-      const float s = (float)__builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t w = wv[i & 1][i >> 1];
+      const int kb = 4 * h + (i >> 1);  // 16-K scale block of group 8h + i
+      // the scale of block kb: half (kb & 1) of word kb >> 1, with kb >> 1 = 2h + (i >> 2)
+      const uint32_t sw = h ? sv[2 + (i >> 2)] : sv[i >> 2];
+      const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      h8 bh, bl;
+      scaled_hi_lo(inlier_f16<NI>(w), s, bh, bl);
+      const h8 bo = outlier_f16<OUT_INT8>(w);
+      h8 av[MS];
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
+        const uint4 xv = st.x[ms][i >> 1];
         uint32_t a0, a1, a2, a3;
-        i8x4_to_f16x4(xc[ms][kb].x, a0, a1);
-        i8x4_to_f16x4(xc[ms][kb].y, a2, a3);
+        i8x4_to_f16x4((i & 1) ? xv.z : xv.x, a0, a1);
+        i8x4_to_f16x4((i & 1) ? xv.w : xv.y, a2, a3);
         const u4v av4 = {a0, a1, a2, a3};
-        const h8 av = __builtin_bit_cast(h8, av4);
-        f16v zero;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) zero[e] = 0.f;
-        const f16v P = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bi, zero, 0, 0, 0);
-        acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bo, acco[ms], 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[ms][e] = fmaf(P[e], s, acc[ms][e]);
+        av[ms] = __builtin_bit_cast(h8, av4);
       }
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bh, acc[ms], 0, 0, 0);
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
     }
+  };
+
+  // two stages in flight: chunk c is computed while c + NW and c + 2*NW land
+  Stage s0, s1;
+  int c = wave;
+  if (c < KC) load(c, s0);
+  if (c + NW < KC) load(c + NW, s1);
+  while (c < KC) {
+    {
+      const Stage cur = s0;
+      if (c + 2 * NW < KC) load(c + 2 * NW, s0);
+      compute(cur);
+    }
+    c += NW;
+    if (c >= KC) break;
+    {
+      const Stage cur = s1;
+      if (c + 2 * NW < KC) load(c + 2 * NW, s1);
+      compute(cur);
+    }
+    c += NW;
   }
 
   // ---- tree over the waves: in round r, wave w + 2^r hands its partial to w
@@ -339,7 +382,8 @@ template <int MS, int NI>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   if constexpr (MS <= 2) {
     // few tokens: split K inside the workgroup so that about 2048+ waves run
-    if (int64_t(a.n_tiles) * 4 >= 2048 || a.n_chunks < 8) return launch_splitk<MS, NI, 4>(c, a, st);
+    const int64_t waves4 = int64_t(a.n_tiles) * 4 * ((a.M + 32 * MS - 1) / (32 * MS));
+    if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4>(c, a, st);
     return launch_splitk<MS, NI, 8>(c, a, st);
   }
   const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
