@@ -93,14 +93,6 @@ __device__ __forceinline__ float sum_lanes_mod4(float v) {
   return __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
 }
 
-// Workgroup b runs on XCD b % 8; give every XCD a contiguous range of the G
-// workgroups' work, so that neighbouring slices (which share the 128-byte
-// lines of a tile's block scales) meet in one L2.
-__device__ __forceinline__ int xcd_contiguous(int b, int G) {
-  const int x = b & 7, i = b >> 3, q = G >> 3, rem = G & 7;
-  return x * q + min(x, rem) + i;
-}
-
 __device__ __forceinline__ _Float16 f16lo(uint32_t v) {
   return __builtin_bit_cast(_Float16, (unsigned short)(v & 0xFFFFu));
 }

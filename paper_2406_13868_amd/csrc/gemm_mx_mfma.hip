@@ -21,8 +21,9 @@
 //
 // Tiling: a workgroup of 4 waves owns 4 row tiles of W (128 outputs) and BM
 // = 32*MS tokens; fp8 activations are staged per 128-K chunk in LDS (double
-// buffered) and shared by the 4 waves; weights stream from HBM into
-// registers and are expanded there into dense fp8 / fp4 fragments.
+// buffered, XOR-swizzled) and shared by the 4 waves; weights stream from HBM
+// into registers and are expanded there into dense fp8 / fp4 fragments.
+// Weights and activations are requested two chunks before they are used.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -35,7 +36,6 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-constexpr int kLdsRow = kChunkK + 16;  // bytes per LDS row (padding against bank conflicts)
 constexpr uint32_t kOutPosMagic = (1u << 21) | (1u << 14) | (1u << 7);
 
 struct MxArgs {
@@ -45,6 +45,7 @@ struct MxArgs {
   float* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
+  int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
 };
 
 // Dense e2m1 nibbles (position p at nibble p) of one group word.
@@ -69,53 +70,68 @@ __device__ __forceinline__ void outlier_fp8(uint32_t w, uint32_t& lo, uint32_t& 
 }
 
 template <int MS, int NI, bool HAS_O>
-__global__ __launch_bounds__(kThreads) void mx_mfma_kernel(MxArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
   constexpr int BM = 32 * MS;
-  __shared__ __align__(16) uint8_t xs[2][BM * kLdsRow];
+  // fp8 activations of one 128-K chunk, BM rows of 128 bytes; 16-byte piece p
+  // of row r sits at piece p ^ (r & 7), so that the A-fragment reads of eight
+  // consecutive rows fall on distinct banks
+  __shared__ __align__(16) uint8_t xs[2][BM * kChunkK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, h = lane >> 5;
-  const int m0 = blockIdx.y * BM;
-  const int tile = blockIdx.x * kWaves + wave;
-  const bool tile_ok = tile < a.n_tiles;
+  // every XCD takes a contiguous range of tile groups and all their M blocks,
+  // so a tile's weights are reused from that XCD's L2
+  const int work = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int group = work / a.m_blocks;
+  const int m0 = (work - group * a.m_blocks) * BM;
+  const int tile = min(group * kWaves + wave, a.n_tiles - 1);  // spare waves recompute the last tile
+  const bool tile_ok = group * kWaves + wave < a.n_tiles;
   const int KC = a.n_chunks;
 
-  constexpr int kPieces = BM * 8;  // 16-byte pieces per chunk of activations
-  constexpr int kPerThread = (kPieces + kThreads - 1) / kThreads;
-  uint4 xr[kPerThread];
-  auto load_x = [&](int c) {
+  // ---- activation staging: every thread moves kPerThread 16-byte pieces
+  constexpr int kPerThread = BM * 8 / kThreads;
+  static_assert(kPerThread * kThreads == BM * 8, "whole pieces per thread");
+  const uint8_t* xsrc[kPerThread];
+  uint32_t xdst[kPerThread];
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i) {
-      const int pc = tid + i * kThreads;
-      const int rr = pc >> 3, cp = pc & 7;
-      xr[i] = make_uint4(0, 0, 0, 0);
-      if (pc < kPieces && m0 + rr < a.M)
-        xr[i] = *reinterpret_cast<const uint4*>(a.Xq + size_t(m0 + rr) * a.K + c * kChunkK + cp * 16);
-    }
-  };
-  auto store_x = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < kPerThread; ++i) {
-      const int pc = tid + i * kThreads;
-      if (pc >= kPieces) continue;
-      const int rr = pc >> 3, cp = pc & 7;
-      *reinterpret_cast<uint4*>(&xs[buf][rr * kLdsRow + cp * 16]) = xr[i];
-    }
-  };
+  for (int i = 0; i < kPerThread; ++i) {
+    const int pc = tid + i * kThreads, rr = pc >> 3, p = pc & 7;
+    // rows past M re-read row M-1 (their outputs are never stored)
+    xsrc[i] = a.Xq + size_t(min(m0 + rr, a.M - 1)) * a.K + p * 16;
+    xdst[i] = uint32_t(rr * kChunkK + ((p ^ (rr & 7)) << 4));
+  }
+  // activations of one chunk on their way to LDS, as named registers (the
+  // compiler keeps a local array of them in scratch across the products)
+  static_assert(kPerThread == 1 || kPerThread == 2 || kPerThread == 4, "1, 2 or 4 pieces per thread");
+  uint4 xr0, xr1, xr2, xr3;
+#define SDQ_XLD(i, c) *reinterpret_cast<const uint4*>(xsrc[i] + size_t(c) * kChunkK)
+#define SDQ_LOAD_X(c)                                        \
+  {                                                          \
+    xr0 = SDQ_XLD(0, c);                                     \
+    if constexpr (kPerThread > 1) xr1 = SDQ_XLD(1, c);       \
+    if constexpr (kPerThread > 2) {                          \
+      xr2 = SDQ_XLD(2, c);                                   \
+      xr3 = SDQ_XLD(3, c);                                   \
+    }                                                        \
+  }
+#define SDQ_STORE_X(buf)                                                            \
+  {                                                                                 \
+    *reinterpret_cast<uint4*>(&xs[buf][xdst[0]]) = xr0;                             \
+    if constexpr (kPerThread > 1) *reinterpret_cast<uint4*>(&xs[buf][xdst[1]]) = xr1; \
+    if constexpr (kPerThread > 2) {                                                 \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[2]]) = xr2;                           \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[3]]) = xr3;                           \
+    }                                                                               \
+  }
 
-  const uint8_t* wbase = a.blob + size_t(tile_ok ? tile : 0) * KC * kWordBytesPerTC + size_t(lane) * 16;
-  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kMxScaleBytesPerTC + lane * 4;
-  uint4 wr0, wr1;
-  uint32_t sr;
-  auto load_w = [&](int c) {
-    if (tile_ok) {
-      wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
-      wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 1024);
-      sr = *reinterpret_cast<const uint32_t*>(sbase + size_t(c) * kMxScaleBytesPerTC);
-    } else {
-      wr0 = wr1 = make_uint4(0, 0, 0, 0);
-      sr = 0;
-    }
+  // ---- weight stream of this wave's tile
+  const uint8_t* wbase = a.blob + size_t(tile) * KC * kWordBytesPerTC + size_t(lane) * 16;
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile) * KC * kMxScaleBytesPerTC + lane * 4;
+  struct WRegs { uint4 w0, w1; uint32_t sc; };
+  auto load_w = [&](int c, WRegs& r) __attribute__((always_inline)) {
+    r.w0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
+    r.w1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 1024);
+    r.sc = *reinterpret_cast<const uint32_t*>(sbase + size_t(c) * kMxScaleBytesPerTC);
   };
 
   f16v acc[MS];
@@ -124,16 +140,20 @@ __global__ __launch_bounds__(kThreads) void mx_mfma_kernel(MxArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
 
-  load_x(0);
-  load_w(0);
-  store_x(0);
-  __syncthreads();
+  // A-fragment byte offsets of this lane in a chunk buffer: row ms*32 + col,
+  // logical pieces 4s + h and 4s + h + 2 for step s
+  uint32_t aoff[MS][2][2];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms) {
+    const int row = ms * 32 + col;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) aoff[ms][s][u] = uint32_t(row * kChunkK + (((4 * s + h + 2 * u) ^ (row & 7)) << 4));
+  }
 
-  for (int c = 0; c < KC; ++c) {
-    const int buf = c & 1;
-    const uint4 wq[2] = {wr0, wr1};
-    const uint32_t scl = sr;
-    if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
+  auto compute = [&](int buf, const WRegs& wr) __attribute__((always_inline)) {
+    const uint4 wq[2] = {wr.w0, wr.w1};
 #pragma unroll
     for (int s = 0; s < 2; ++s) {  // two 64-K steps per chunk
       uint32_t w[4] = {wq[s].x, wq[s].y, wq[s].z, wq[s].w};
@@ -155,26 +175,59 @@ __global__ __launch_bounds__(kThreads) void mx_mfma_kernel(MxArgs a) {
           bo[2 * i + 1] = int(hi);
         }
       }
-      const int eo = int((scl >> (16 * s)) & 0xFFu);
-      const int ei = int((scl >> (16 * s + 8)) & 0xFFu);
+      const int eo = int((wr.sc >> (16 * s)) & 0xFFu);
+      const int ei = int((wr.sc >> (16 * s + 8)) & 0xFFu);
+      i8v av[MS];
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
-        const uint8_t* ap = &xs[buf][(ms * 32 + col) * kLdsRow + s * 64 + h * 16];
-        const uint4 a0 = *reinterpret_cast<const uint4*>(ap);
-        const uint4 a1 = *reinterpret_cast<const uint4*>(ap + 32);
-        const i8v av = {int(a0.x), int(a0.y), int(a0.z), int(a0.w),
-                        int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
-        if constexpr (HAS_O)
-          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bo, acc[ms], 0, 0, 0, 127, 0, eo);
-        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bi, acc[ms], 0, 4, 0, 127, 0, ei);
+        const uint4 a0 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][0]]);
+        const uint4 a1 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][1]]);
+        av[ms] = i8v{int(a0.x), int(a0.y), int(a0.z), int(a0.w), int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
       }
+      if constexpr (HAS_O) {
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms)
+          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bo, acc[ms], 0, 0, 0, 127, 0, eo);
+      }
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms)
+        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bi, acc[ms], 0, 4, 0, 127, 0, ei);
     }
-    if (c + 1 < KC) {
-      store_x(buf ^ 1);
-      __syncthreads();
-    }
+  };
+
+  // ---- pipeline: weights and activations are requested two chunks ahead;
+  //      iteration c computes chunk c from LDS, stores the registers of
+  //      chunk c+1 into the other LDS buffer and requests chunk c+3's.
+  // Loads past the last chunk re-read it (in bounds, never used), so that
+  // no load is conditional.  Each register set is refilled right after its
+  // products (never copied: a copy would wait for the load), so the weights
+  // of chunk c+2 fly during the products of chunk c+1, and the activations
+  // of chunk c+1 go from registers to LDS after the products of chunk c.
+  const int last = KC - 1;
+  WRegs wA, wB;     // weights of the even / odd chunks
+  SDQ_LOAD_X(0)
+  load_w(0, wA);
+  load_w(min(1, last), wB);
+  SDQ_STORE_X(0)
+  SDQ_LOAD_X(min(1, last))
+  __syncthreads();
+  for (int c = 0; c < KC; c += 2) {
+    compute(0, wA);
+    load_w(min(c + 2, last), wA);
+    SDQ_STORE_X(1)
+    SDQ_LOAD_X(min(c + 2, last))
+    __syncthreads();
+    if (c + 1 >= KC) break;
+    compute(1, wB);
+    load_w(min(c + 3, last), wB);
+    SDQ_STORE_X(0)
+    SDQ_LOAD_X(min(c + 3, last))
+    __syncthreads();
   }
 
+#undef SDQ_XLD
+#undef SDQ_LOAD_X
+#undef SDQ_STORE_X
   if (!tile_ok) return;
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
@@ -189,12 +242,14 @@ __global__ __launch_bounds__(kThreads) void mx_mfma_kernel(MxArgs a) {
 
 template <int MS, int NI>
 hipError_t launch_ms_ni(const Cfg& c, const MxArgs& a, hipStream_t st) {
-  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
+  MxArgs b = a;
+  b.m_blocks = int((a.M + 32 * MS - 1) / (32 * MS));
+  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves * b.m_blocks));
   const dim3 block(kThreads);
   if (c.n_o)
-    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, true>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, true>), grid, block, 0, st, b);
   else
-    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, false>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, false>), grid, block, 0, st, b);
   return hipGetLastError();
 }
 

@@ -10,6 +10,15 @@
 
 namespace sdq {
 
+// Workgroups are dispatched round robin over the 8 XCDs (workgroup b runs on
+// XCD b % 8, each with its own L2).  This maps b to a work index so that every
+// XCD takes a contiguous range of the G indices: neighbouring work items,
+// which share cache lines, meet in one L2.  It is a bijection on [0, G).
+__device__ __forceinline__ int xcd_contiguous(int b, int G) {
+  const int x = b & 7, i = b >> 3, q = G >> 3, rem = G & 7;
+  return x * q + min(x, rem) + i;
+}
+
 hipError_t launch_act_quant(const Cfg& c, const void* X, int x_dtype, int64_t M, int64_t K,
                             uint8_t* Xq, float* s_a, hipStream_t st);
 

@@ -2,7 +2,7 @@
 #pragma once
 #include <cstdint>
 
-#include "../../include/sdq.h"
+#include "sdq.h"
 
 namespace sdq {
 
