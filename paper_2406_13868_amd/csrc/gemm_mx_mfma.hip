@@ -48,6 +48,14 @@ struct MxArgs {
   int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
 };
 
+// Physical 16-byte piece offset of row r of an LDS tile with 128-byte rows.
+// A-fragment reads take one logical piece of consecutive rows; with this XOR
+// the rows of any aligned group of 8 fall on 8 distinct pieces, and those of
+// any aligned group of 16 on 16 distinct (row parity, piece) pairs, so that
+// the reads are free of bank conflicts whether the LDS serves 8 or 16 lanes
+// of a 16-byte read per cycle (32 or 64 banks of 4 bytes).
+__device__ __forceinline__ int lds_swizzle(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
 // Dense e2m1 nibbles (position p at nibble p) of one group word.
 template <int NI>
 __device__ __forceinline__ uint32_t inlier_fp4(uint32_t w) {
@@ -69,12 +77,54 @@ __device__ __forceinline__ void outlier_fp8(uint32_t w, uint32_t& lo, uint32_t& 
   hi = pos < 4u ? 0u : v;
 }
 
+// ---- merged branches -------------------------------------------------------
+// Within one 32-K block an inlier e2m1 value times 2^Ei equals an e4m3 value
+// times 2^Eo when d = Ei - Eo lies in [-5, 6]: e2m1 magnitudes are 2^e or
+// 1.5 * 2^e with e in [-1, 2], and shifting them by d keeps the e4m3 exponent
+// field in [1, 15] without reaching the NaN code.  Then the outlier and the
+// inlier branch of the block form one dense e4m3 fragment under the outlier's
+// scale and take a single fp8 x fp8 matrix instruction.  Blocks with d
+// outside that range keep their inliers out of the merged fragment and add
+// them with the fp8 x fp4 instruction as before (a rare, wave-uniform path).
+
+// e4m3 codes of the e2m1 magnitudes 0..7 shifted by d, as a v_perm table
+// (bytes 0-3 in lo, 4-7 in hi); zero tables when the block cannot merge.
+struct ShiftTable { uint32_t lo, hi, sign; };
+__device__ __forceinline__ ShiftTable shift_table(int d, bool ok) {
+  const int t = d * 8;                              // d in the exponent field
+  const int x8 = __mul24(t, 0x010101) << 8;         // t in bytes 1..3
+  ShiftTable T;
+  T.lo = ok ? uint32_t(0x3C383000 + x8) : 0u;       // 0, 0.5, 1, 1.5
+  T.hi = ok ? uint32_t(0x4C484440 + x8 + t) : 0u;   // 2, 3, 4, 6
+  T.sign = ok ? 0x00808080u : 0u;
+  return T;
+}
+
+// Dense e4m3 fragment (positions 0-3 in lo, 4-7 in hi) of one group word:
+// the NI inliers converted with T and the outlier code, scattered by v_perm.
+// A nibble map holds, per position, the v_perm selector of its byte: 4 + j
+// for inlier slot j (bytes of the converted inliers), 3 for the outlier
+// (byte 3 of the outlier-only word), 0 for an empty position (a zero byte).
+template <int NI>
+__device__ __forceinline__ void merged_e4m3(uint32_t w, const ShiftTable& T, uint32_t& lo, uint32_t& hi) {
+  const uint32_t conv = __builtin_amdgcn_perm(T.hi, T.lo, (w >> 4) & 0x00070707u) | (w & T.sign);
+  const uint32_t ob = w & 0xFF000000u;
+  uint32_t N = 4u << (w << 2);  // slot 0 at 4 * p0 (bits 2-4 of w << 2; its low bits are 0)
+  if constexpr (NI > 1) N |= 5u << ((w >> 6) & 0x1Cu);
+  if constexpr (NI > 2) N |= 6u << ((w >> 14) & 0x1Cu);
+  N |= 3u << (__umul24(w & 0x00080808u, kOutPosMagic) >> 22);  // 4 * outlier position
+  const uint32_t Nh = N >> 4;
+  const uint32_t e_lo = __builtin_amdgcn_perm(Nh, N, 0x05010400u) & 0x0F0F0F0Fu;
+  const uint32_t e_hi = __builtin_amdgcn_perm(Nh, N, 0x07030602u) & 0x0F0F0F0Fu;
+  lo = __builtin_amdgcn_perm(conv, ob, e_lo);
+  hi = __builtin_amdgcn_perm(conv, ob, e_hi);
+}
+
 template <int MS, int NI, bool HAS_O>
-__global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
+__global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxArgs a) {
   constexpr int BM = 32 * MS;
-  // fp8 activations of one 128-K chunk, BM rows of 128 bytes; 16-byte piece p
-  // of row r sits at piece p ^ (r & 7), so that the A-fragment reads of eight
-  // consecutive rows fall on distinct banks
+  // fp8 activations of one 128-K chunk, BM rows of 128 bytes, each 16-byte
+  // piece p of row r at piece p ^ lds_swizzle(r)
   __shared__ __align__(16) uint8_t xs[2][BM * kChunkK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -98,12 +148,13 @@ __global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
     const int pc = tid + i * kThreads, rr = pc >> 3, p = pc & 7;
     // rows past M re-read row M-1 (their outputs are never stored)
     xsrc[i] = a.Xq + size_t(min(m0 + rr, a.M - 1)) * a.K + p * 16;
-    xdst[i] = uint32_t(rr * kChunkK + ((p ^ (rr & 7)) << 4));
+    xdst[i] = uint32_t(rr * kChunkK + ((p ^ lds_swizzle(rr)) << 4));
   }
   // activations of one chunk on their way to LDS, as named registers (the
   // compiler keeps a local array of them in scratch across the products)
-  static_assert(kPerThread == 1 || kPerThread == 2 || kPerThread == 4, "1, 2 or 4 pieces per thread");
-  uint4 xr0, xr1, xr2, xr3;
+  static_assert(kPerThread == 1 || kPerThread == 2 || kPerThread == 4 || kPerThread == 8,
+                "1, 2, 4 or 8 pieces per thread");
+  uint4 xr0, xr1, xr2, xr3, xr4, xr5, xr6, xr7;
 #define SDQ_XLD(i, c) *reinterpret_cast<const uint4*>(xsrc[i] + size_t(c) * kChunkK)
 #define SDQ_LOAD_X(c)                                        \
   {                                                          \
@@ -113,6 +164,12 @@ __global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
       xr2 = SDQ_XLD(2, c);                                   \
       xr3 = SDQ_XLD(3, c);                                   \
     }                                                        \
+    if constexpr (kPerThread > 4) {                          \
+      xr4 = SDQ_XLD(4, c);                                   \
+      xr5 = SDQ_XLD(5, c);                                   \
+      xr6 = SDQ_XLD(6, c);                                   \
+      xr7 = SDQ_XLD(7, c);                                   \
+    }                                                        \
   }
 #define SDQ_STORE_X(buf)                                                            \
   {                                                                                 \
@@ -121,6 +178,12 @@ __global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
     if constexpr (kPerThread > 2) {                                                 \
       *reinterpret_cast<uint4*>(&xs[buf][xdst[2]]) = xr2;                           \
       *reinterpret_cast<uint4*>(&xs[buf][xdst[3]]) = xr3;                           \
+    }                                                                               \
+    if constexpr (kPerThread > 4) {                                                 \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[4]]) = xr4;                           \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[5]]) = xr5;                           \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[6]]) = xr6;                           \
+      *reinterpret_cast<uint4*>(&xs[buf][xdst[7]]) = xr7;                           \
     }                                                                               \
   }
 
@@ -149,60 +212,104 @@ __global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) aoff[ms][s][u] = uint32_t(row * kChunkK + (((4 * s + h + 2 * u) ^ (row & 7)) << 4));
+      for (int u = 0; u < 2; ++u) aoff[ms][s][u] = uint32_t(row * kChunkK + (((4 * s + h + 2 * u) ^ lds_swizzle(row)) << 4));
   }
 
-  auto compute = [&](int buf, const WRegs& wr) __attribute__((always_inline)) {
-    const uint4 wq[2] = {wr.w0, wr.w1};
+  // B fragments of one 64-K step.  With outliers: the merged e4m3 fragment
+  // (lane half h holds groups {2h, 2h+1, 4+2h, 5+2h} of the step, the fp8
+  // operand order) under the scale of block h, plus the flags of blocks that
+  // cannot merge.  Without outliers: the fp4 inlier fragment (groups 4h..4h+3).
+  struct BFrag { i8v b; int e; bool split; };
+  auto expand = [&](const WRegs& wr, int s) __attribute__((always_inline)) {
+    BFrag f;
+    const uint4 wq = s ? wr.w1 : wr.w0;
+    const uint32_t w[4] = {wq.x, wq.y, wq.z, wq.w};
+    if constexpr (HAS_O) {
+      auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+      auto s13 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+      const uint32_t u[4] = {s02[0], s13[0], s02[1], s13[1]};
+      // scale bytes of block 2s + b of this row, b = 0, 1 (lane halves 0, 1)
+      auto ss = __builtin_amdgcn_permlane32_swap(wr.sc, wr.sc, false, false);
+      ShiftTable T[2];
+      bool ok[2];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {  // two 64-K steps per chunk
-      uint32_t w[4] = {wq[s].x, wq[s].y, wq[s].z, wq[s].w};
-      i8v bi, bo;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) bi[i] = int(inlier_fp4<NI>(w[i]));
-#pragma unroll
-      for (int i = 4; i < 8; ++i) bi[i] = 0;
-      if constexpr (HAS_O) {
-        // fp8 order: lane half 0 needs groups {0,1,4,5}, half 1 {2,3,6,7} of the step
-        auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
-        auto s13 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
-        const uint32_t u[4] = {s02[0], s13[0], s02[1], s13[1]};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          uint32_t lo, hi;
-          outlier_fp8(u[i], lo, hi);
-          bo[2 * i] = int(lo);
-          bo[2 * i + 1] = int(hi);
-        }
+      for (int b = 0; b < 2; ++b) {
+        const uint32_t sb = ss[b] >> (16 * s);
+        const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
+        ok[b] = d >= -5 && d <= 6;
+        T[b] = shift_table(d, ok[b]);
       }
-      const int eo = int((wr.sc >> (16 * s)) & 0xFFu);
-      const int ei = int((wr.sc >> (16 * s + 8)) & 0xFFu);
-      i8v av[MS];
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) {
-        const uint4 a0 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][0]]);
-        const uint4 a1 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][1]]);
-        av[ms] = i8v{int(a0.x), int(a0.y), int(a0.z), int(a0.w), int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
+      for (int i = 0; i < 4; ++i) {
+        uint32_t lo, hi;
+        merged_e4m3<NI>(u[i], T[i >> 1], lo, hi);
+        f.b[2 * i] = int(lo);
+        f.b[2 * i + 1] = int(hi);
       }
-      if constexpr (HAS_O) {
+      f.e = int((wr.sc >> (16 * s)) & 0xFFu);  // Eo of block 2s + h
+      f.split = !(ok[0] && ok[1]);
+    } else {
 #pragma unroll
-        for (int ms = 0; ms < MS; ++ms)
-          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bo, acc[ms], 0, 0, 0, 127, 0, eo);
-      }
+      for (int i = 0; i < 4; ++i) f.b[i] = int(inlier_fp4<NI>(w[i]));
+#pragma unroll
+      for (int i = 4; i < 8; ++i) f.b[i] = 0;
+      f.e = int((wr.sc >> (16 * s + 8)) & 0xFFu);  // Ei of block 2s + h
+      f.split = false;
+    }
+    return f;
+  };
+  // the inliers of blocks that did not merge (fp4 order: block 2s + h of
+  // this lane), for the fp8 x fp4 instruction; chunk c's words are read again
+  // (an L2 hit) so that the common path keeps no copy of them
+  auto split_inliers = [&](int c, int s, i8v& bi, int& ei) __attribute__((always_inline)) {
+    WRegs wr;
+    load_w(c, wr);
+    const uint4 wq = s ? wr.w1 : wr.w0;
+    const uint32_t w[4] = {wq.x, wq.y, wq.z, wq.w};
+    const uint32_t sb = wr.sc >> (16 * s);
+    const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
+    const bool ok = d >= -5 && d <= 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bi[i] = ok ? 0 : int(inlier_fp4<NI>(w[i]));
+#pragma unroll
+    for (int i = 4; i < 8; ++i) bi[i] = 0;
+    ei = int((sb >> 8) & 0xFFu);
+  };
+  auto mfmas = [&](int buf, int c, int s, const BFrag& f) __attribute__((always_inline)) {
+    i8v av[MS];
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms) {
+      const uint4 a0 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][0]]);
+      const uint4 a1 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][1]]);
+      av[ms] = i8v{int(a0.x), int(a0.y), int(a0.z), int(a0.w), int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
+    }
+    if constexpr (HAS_O) {
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms)
-        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bi, acc[ms], 0, 4, 0, 127, 0, ei);
+        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], f.b, acc[ms], 0, 0, 0, 127, 0, f.e);
+      if (__any(f.split)) {  // wave-uniform
+        i8v bi;
+        int ei;
+        split_inliers(c, s, bi, ei);
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms)
+          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bi, acc[ms], 0, 4, 0, 127, 0, ei);
+      }
+    } else {
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms)
+        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], f.b, acc[ms], 0, 4, 0, 127, 0, f.e);
     }
   };
 
-  // ---- pipeline: weights and activations are requested two chunks ahead;
-  //      iteration c computes chunk c from LDS, stores the registers of
-  //      chunk c+1 into the other LDS buffer and requests chunk c+3's.
-  // Loads past the last chunk re-read it (in bounds, never used), so that
-  // no load is conditional.  Each register set is refilled right after its
-  // products (never copied: a copy would wait for the load), so the weights
-  // of chunk c+2 fly during the products of chunk c+1, and the activations
-  // of chunk c+1 go from registers to LDS after the products of chunk c.
+  // ---- pipeline.  Weights are requested two chunks ahead and expanded one
+  //      step ahead of their products (the next chunk's first step while
+  //      this chunk's second step runs), so that the expansion of one step
+  //      overlaps the matrix instructions of the other; activations of chunk
+  //      c+1 go from registers to LDS after the products of chunk c.  Loads
+  //      past the last chunk re-read it (in bounds, never used), so that no
+  //      load is conditional.  A register set is refilled right after its
+  //      last expansion, never copied (a copy would wait for the load).
   const int last = KC - 1;
   WRegs wA, wB;     // weights of the even / odd chunks
   SDQ_LOAD_X(0)
@@ -210,19 +317,30 @@ __global__ __launch_bounds__(kThreads, 2) void mx_mfma_kernel(MxArgs a) {
   load_w(min(1, last), wB);
   SDQ_STORE_X(0)
   SDQ_LOAD_X(min(1, last))
+  BFrag fE = expand(wA, 0), fO;  // first step of the next even / odd chunk
   __syncthreads();
   for (int c = 0; c < KC; c += 2) {
-    compute(0, wA);
-    load_w(min(c + 2, last), wA);
-    SDQ_STORE_X(1)
-    SDQ_LOAD_X(min(c + 2, last))
-    __syncthreads();
+    {
+      const BFrag f1 = expand(wA, 1);
+      load_w(min(c + 2, last), wA);
+      mfmas(0, c, 0, fE);
+      fO = expand(wB, 0);
+      mfmas(0, c, 1, f1);
+      SDQ_STORE_X(1)
+      SDQ_LOAD_X(min(c + 2, last))
+      __syncthreads();
+    }
     if (c + 1 >= KC) break;
-    compute(1, wB);
-    load_w(min(c + 3, last), wB);
-    SDQ_STORE_X(0)
-    SDQ_LOAD_X(min(c + 3, last))
-    __syncthreads();
+    {
+      const BFrag f1 = expand(wB, 1);
+      load_w(min(c + 3, last), wB);
+      mfmas(1, c + 1, 0, fO);
+      fE = expand(wA, 0);
+      mfmas(1, c + 1, 1, f1);
+      SDQ_STORE_X(0)
+      SDQ_LOAD_X(min(c + 3, last))
+      __syncthreads();
+    }
   }
 
 #undef SDQ_XLD

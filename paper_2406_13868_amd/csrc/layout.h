@@ -18,9 +18,11 @@
 //
 // Inlier slots are in ascending position order; an unused slot (n_i < 3) has
 // position 0 and code 0.  With 1:16 outliers the outlier lives in the word
-// of the 8-group that holds it; the other word of its 16-group has outlier
-// code 0 and position 0.  A zero code contributes nothing, so the position
-// of an unused slot never matters.
+// of the 8-group that holds it; the other word of its 16-group (and every
+// word when there is no outlier branch) has outlier code 0 at the lowest
+// position that holds no inlier.  A zero code contributes nothing; keeping
+// the outlier position off the inlier positions lets a kernel scatter all
+// four slots of a word into one dense fragment without collisions.
 //
 // This layout lets a lane turn one word into a v_perm_b32 byte selector
 // (positions in bits 0-2 of bytes 0-2 and 3 bits for byte 3), and keep the

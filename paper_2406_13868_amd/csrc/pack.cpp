@@ -305,11 +305,18 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
             word |= uint32_t(icode[8 * gg + p] & 0xF) << (8 * j + 4);
             ++j;
           }
+        // the outlier of the group, or (1:16 word without one, or no outlier
+        // branch) code 0 at the lowest position no inlier occupies
+        int po = 0;
+        while ((im[gg] >> po) & 1u) ++po;
+        uint32_t oc = 0;
         for (int p = 0; p < 8; ++p)
           if ((om[gg] >> p) & 1u) {
-            for (int bit = 0; bit < 3; ++bit) word |= uint32_t((p >> bit) & 1) << (8 * bit + 3);
-            word |= uint32_t(ocode[8 * gg + p]) << 24;
+            po = p;
+            oc = ocode[8 * gg + p];
           }
+        for (int bit = 0; bit < 3; ++bit) word |= uint32_t((po >> bit) & 1) << (8 * bit + 3);
+        word |= oc << 24;
         const int g = int((k0 % kChunkK) / 8) + gg;
         words[c.mx ? mx_word_index(g, int(r)) : int_word_index(g, int(r))] = word;
       }

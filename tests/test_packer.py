@@ -215,3 +215,20 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(cfg, 1, 4096, 4096) == sdq.PATH_DECODE
     assert sdq.gemm_path(cfg, 2048, 4096, 4096) == sdq.PATH_MFMA
     assert sdq.gemm_path(sdq.Config.mx_family(), 1, 4096, 4096) == sdq.PATH_MFMA
+
+
+@pytest.mark.parametrize("c", [c for c in CONFIGS if c[1] == 0 or c[2] == 16], ids=_ids)
+def test_absent_outlier_position_is_free(c):
+    """A group word without an outlier (1:16 words, or no outlier branch) keeps
+    its outlier position off every inlier position (kernels scatter all four
+    slots of a word into one dense fragment)."""
+    cfg, cfg_o = _cfgs(*c)
+    N, K = 64, 512
+    blob = sdq.pack(synth.make_w(5, 0, N, K), cfg)
+    n_words = ((N + 31) // 32) * (K // 128) * 512
+    w = np.frombuffer(blob[: n_words * 4].tobytes(), dtype=np.uint32).astype(np.int64)
+    po = ((w >> 3) & 1) | ((w >> 10) & 2) | ((w >> 17) & 4)
+    absent = (w >> 24) == 0
+    for j in range(cfg_o.n_i):
+        pj = (w >> (8 * j)) & 7
+        assert not np.any(absent & (po == pj)), f"slot {j}"
