@@ -141,14 +141,16 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   // ---- activation staging: every thread moves kPerThread 16-byte pieces
   constexpr int kPerThread = BM * 8 / kThreads;
   static_assert(kPerThread * kThreads == BM * 8, "whole pieces per thread");
+  // thread tid moves pieces p = tid & 7 of rows (tid >> 3) + 32 i; the
+  // swizzle of those rows does not depend on i, so their LDS offsets are one
+  // register plus i * 32 rows
   const uint8_t* xsrc[kPerThread];
-  uint32_t xdst[kPerThread];
+  const uint32_t xdst0 = uint32_t((tid >> 3) * kChunkK + (((tid & 7) ^ lds_swizzle(tid >> 3)) << 4));
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int pc = tid + i * kThreads, rr = pc >> 3, p = pc & 7;
+    const int rr = (tid >> 3) + i * 32;
     // rows past M re-read row M-1 (their outputs are never stored)
-    xsrc[i] = a.Xq + size_t(min(m0 + rr, a.M - 1)) * a.K + p * 16;
-    xdst[i] = uint32_t(rr * kChunkK + ((p ^ lds_swizzle(rr)) << 4));
+    xsrc[i] = a.Xq + size_t(min(m0 + rr, a.M - 1)) * a.K + (tid & 7) * 16;
   }
   // activations of one chunk on their way to LDS, as named registers (the
   // compiler keeps a local array of them in scratch across the products)
@@ -171,19 +173,20 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
       xr7 = SDQ_XLD(7, c);                                   \
     }                                                        \
   }
+#define SDQ_XST(b, i) *reinterpret_cast<uint4*>(&xs[b][xdst0 + (i) * 32 * kChunkK])
 #define SDQ_STORE_X(buf)                                                            \
   {                                                                                 \
-    *reinterpret_cast<uint4*>(&xs[buf][xdst[0]]) = xr0;                             \
-    if constexpr (kPerThread > 1) *reinterpret_cast<uint4*>(&xs[buf][xdst[1]]) = xr1; \
+    SDQ_XST(buf, 0) = xr0;                                                               \
+    if constexpr (kPerThread > 1) SDQ_XST(buf, 1) = xr1;                                 \
     if constexpr (kPerThread > 2) {                                                 \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[2]]) = xr2;                           \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[3]]) = xr3;                           \
+      SDQ_XST(buf, 2) = xr2;                                                           \
+      SDQ_XST(buf, 3) = xr3;                                                           \
     }                                                                               \
     if constexpr (kPerThread > 4) {                                                 \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[4]]) = xr4;                           \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[5]]) = xr5;                           \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[6]]) = xr6;                           \
-      *reinterpret_cast<uint4*>(&xs[buf][xdst[7]]) = xr7;                           \
+      SDQ_XST(buf, 4) = xr4;                                                           \
+      SDQ_XST(buf, 5) = xr5;                                                           \
+      SDQ_XST(buf, 6) = xr6;                                                           \
+      SDQ_XST(buf, 7) = xr7;                                                           \
     }                                                                               \
   }
 
@@ -204,16 +207,13 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
     for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
 
   // A-fragment byte offsets of this lane in a chunk buffer: row ms*32 + col,
-  // logical pieces 4s + h and 4s + h + 2 for step s
-  uint32_t aoff[MS][2][2];
+  // logical pieces 4s + h and 4s + h + 2 for step s; the swizzle of row
+  // ms*32 + col is that of col, so sub-tile ms adds ms * 32 rows
+  uint32_t aoff[2][2];
 #pragma unroll
-  for (int ms = 0; ms < MS; ++ms) {
-    const int row = ms * 32 + col;
+  for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) aoff[ms][s][u] = uint32_t(row * kChunkK + (((4 * s + h + 2 * u) ^ lds_swizzle(row)) << 4));
-  }
+    for (int u = 0; u < 2; ++u) aoff[s][u] = uint32_t(col * kChunkK + (((4 * s + h + 2 * u) ^ lds_swizzle(col)) << 4));
 
   // B fragments of one 64-K step.  With outliers: the merged e4m3 fragment
   // (lane half h holds groups {2h, 2h+1, 4+2h, 5+2h} of the step, the fp8
@@ -279,8 +279,8 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
     i8v av[MS];
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms) {
-      const uint4 a0 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][0]]);
-      const uint4 a1 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[ms][s][1]]);
+      const uint4 a0 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[s][0] + ms * 32 * kChunkK]);
+      const uint4 a1 = *reinterpret_cast<const uint4*>(&xs[buf][aoff[s][1] + ms * 32 * kChunkK]);
       av[ms] = i8v{int(a0.x), int(a0.y), int(a0.z), int(a0.w), int(a1.x), int(a1.y), int(a1.z), int(a1.w)};
     }
     if constexpr (HAS_O) {
@@ -344,6 +344,7 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   }
 
 #undef SDQ_XLD
+#undef SDQ_XST
 #undef SDQ_LOAD_X
 #undef SDQ_STORE_X
   if (!tile_ok) return;
