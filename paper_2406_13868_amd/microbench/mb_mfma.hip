@@ -1,0 +1,62 @@
+// Microbenchmark: issue rate of the matrix instructions used by libsdq (no memory traffic in the loop).
+#include <hip/hip_runtime.h>
+#include <cstdio>
+#include <cstdlib>
+#define CK(x) do { hipError_t e = (x); if (e != hipSuccess) { printf("HIP error %s at %d\n", hipGetErrorString(e), __LINE__); exit(1);} } while (0)
+typedef int i8v __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+template <int FA, int FB, int NACC>
+__global__ __launch_bounds__(256) void k_scale(float* out, int iters, int seed) {
+  i8v a, b;
+  for (int i = 0; i < 8; ++i) { a[i] = seed * (threadIdx.x + i); b[i] = seed ^ (threadIdx.x * 7 + i); }
+  f16v acc[NACC];
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < NACC; ++j)
+      acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc[j], FA, FB, 0, 127, 0, 127);
+  }
+  float s = 0.f;
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) s += acc[j][e];
+  if (s == 1234.5f) out[threadIdx.x] = s;
+}
+template <int NACC>
+__global__ __launch_bounds__(256) void k_f16(float* out, int iters, int seed) {
+  h8 a, b;
+  for (int i = 0; i < 8; ++i) { a[i] = (_Float16)(seed * (threadIdx.x + i) & 7); b[i] = (_Float16)((seed ^ i) & 7); }
+  f16v acc[NACC];
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[j], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) s += acc[j][e];
+  if (s == 1234.5f) out[threadIdx.x] = s;
+}
+int main() {
+  float* out; CK(hipMalloc(&out, 1024 * 4));
+  hipEvent_t e0, e1; CK(hipEventCreate(&e0)); CK(hipEventCreate(&e1));
+  const int iters = 2000;
+  auto run = [&](const char* nm, auto kern, int blocks, int nacc) {
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, 0, out, 10, 3);
+    CK(hipDeviceSynchronize());
+    CK(hipEventRecord(e0)); hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, 0, out, iters, 3); CK(hipEventRecord(e1));
+    CK(hipEventSynchronize(e1)); float ms; CK(hipEventElapsedTime(&ms, e0, e1));
+    const double mfmas_per_simd = double(blocks) * 4 / 1024.0 * iters * nacc;  // 4 waves per block, 1024 SIMDs
+    printf("%-34s blocks %5d  %8.3f ms  %6.1f cycles/MFMA/SIMD @2.4GHz\n", nm, blocks, ms, ms * 1e-3 * 2.4e9 / mfmas_per_simd);
+    fflush(stdout);
+  };
+  for (int blocks : {256, 512}) {
+    run("scale fp8 x fp8, 4 acc", k_scale<0, 0, 4>, blocks, 4);
+    run("scale fp8 x fp4, 4 acc", k_scale<0, 4, 4>, blocks, 4);
+    run("scale fp4 x fp4, 4 acc", k_scale<4, 4, 4>, blocks, 4);
+    run("scale fp8 x fp8, 8 acc", k_scale<0, 0, 8>, blocks, 8);
+    run("f16 32x32x16, 4 acc", k_f16<4>, blocks, 4);
+    run("f16 32x32x16, 8 acc", k_f16<8>, blocks, 8);
+  }
+  printf("mb done\n");
+  return 0;
+}
