@@ -245,3 +245,50 @@ def test_hip_graph_replays_match_eager(c):
         # eager work in between
         sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y))
         torch.cuda.synchronize()
+
+
+def _split_case(kind, N, K, rng):
+    """MX weights whose blocks cannot merge the inliers into the outliers' e4m3
+    fragment (inlier/outlier exponent difference outside [-5, 6])."""
+    W = synth.make_w(1, 0, N, K).copy()
+    an = None
+    if kind == "product":          # inliers may exceed the outliers
+        an = np.abs(rng.standard_normal(K)).astype(np.float32) * 10.0
+    elif kind == "zero_inliers":   # blocks holding only their outliers
+        blk = rng.random((N, K // 32)) < 0.3
+        keep = np.zeros((N, K), bool)
+        for n, b in zip(*np.nonzero(blk)):
+            seg = W[n, 32 * b:32 * b + 32]
+            top = np.argsort(-np.abs(seg.reshape(4, 8)), axis=1, kind="stable")[:, 0] + np.arange(4) * 8
+            mask = np.zeros(32, bool)
+            mask[top] = True
+            W[n, 32 * b:32 * b + 32] = np.where(mask, seg, 0.0)
+    elif kind == "huge_outliers":  # outliers 2^13 times the block's inliers
+        W[:, 5::8] = np.sign(W[:, 5::8] + 1e-9) * 8192.0 * np.abs(W).max()
+    return W, an
+
+
+@pytest.mark.parametrize("kind", ["product", "zero_inliers", "huge_outliers"])
+@pytest.mark.parametrize("n_i", [2, 3])
+@pytest.mark.parametrize("M,N,K", [(64, 96, 512), (256, 64, 1024)])
+def test_mx_unmergeable_blocks(kind, n_i, M, N, K):
+    """The matrix kernel's correction path for blocks that stay split."""
+    rng = np.random.default_rng(7)
+    metric = "product" if kind == "product" else "magnitude"
+    cfg = sdq.Config("mx", 1, 8, "e4m3", n_i, 8, "e2m1", "e4m3", metric)
+    cfg_o = S.Config("mx", 1, 8, "e4m3", n_i, 8, "e2m1", "e4m3", metric)
+    W, an = _split_case(kind, N, K, rng)
+    X = synth.make_x(1, M, K)
+    # the case must contain unmergeable blocks, or it tests nothing
+    L = S.pack_logical(W, cfg_o, an)
+    d = L["scale_i"].astype(int) - L["scale_o"].astype(int)
+    assert np.any((d < -5) | (d > 6)), "no unmergeable block in the case"
+    say("mx split", kind, n_i, M, N, K)
+    torch = torch_cuda()
+    blob = torch.from_numpy(sdq.pack(W, cfg, act_norm=an)).cuda()
+    Xq, s_a = sdq.quantize_act(torch.from_numpy(X).cuda(), cfg)
+    Y = sdq.gemm(Xq, s_a, blob, N, K, cfg).cpu().numpy()
+    Yref, _, _, _ = S.reference(X, W, cfg_o, an)
+    A = np.abs(S.dequant_act(*S.quantize_act(X, cfg_o), cfg_o))
+    T = A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
+    assert_close_terms(Y, Yref, T, f"{kind} n_i={n_i} M={M}")
