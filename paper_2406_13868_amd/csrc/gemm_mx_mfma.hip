@@ -120,6 +120,57 @@ __device__ __forceinline__ void merged_e4m3(uint32_t w, const ShiftTable& T, uin
   hi = __builtin_amdgcn_perm(conv, ob, e_hi);
 }
 
+// Merged e4m3 fragment of one 64-K step for the fp8 operand order (lane half
+// h holds groups {2h, 2h+1, 4+2h, 5+2h}) from the step's four fp4-order
+// words of this lane (groups 4h..4h+3) and the lane's scale word (Eo, Ei of
+// blocks 2s+h for s = 0, 1).  e: the outlier scale of block 2s+h (the MFMA
+// scale this lane supplies); split: some block of this lane's groups did not
+// merge its inliers.
+struct MergedFrag { i8v b; int e; bool split; };
+template <int NI>
+__device__ __forceinline__ MergedFrag expand_merged(uint4 wq, uint32_t sc, int s) {
+  MergedFrag f;
+  auto s02 = __builtin_amdgcn_permlane32_swap(wq.x, wq.z, false, false);
+  auto s13 = __builtin_amdgcn_permlane32_swap(wq.y, wq.w, false, false);
+  const uint32_t u[4] = {s02[0], s13[0], s02[1], s13[1]};
+  // scale bytes of block 2s + b of this row, b = 0, 1 (lane halves 0, 1)
+  auto ss = __builtin_amdgcn_permlane32_swap(sc, sc, false, false);
+  ShiftTable T[2];
+  bool ok[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const uint32_t sb = ss[b] >> (16 * s);
+    const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
+    ok[b] = d >= -5 && d <= 6;
+    T[b] = shift_table(d, ok[b]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t lo, hi;
+    merged_e4m3<NI>(u[i], T[i >> 1], lo, hi);
+    f.b[2 * i] = int(lo);
+    f.b[2 * i + 1] = int(hi);
+  }
+  f.e = int((sc >> (16 * s)) & 0xFFu);  // Eo of block 2s + h
+  f.split = !(ok[0] && ok[1]);
+  return f;
+}
+
+// The inliers of this lane's block (fp4 order: block 2s + h) when that block
+// did not merge, else zeros, with their scale Ei.
+template <int NI>
+__device__ __forceinline__ void split_inliers_fp4(uint4 wq, uint32_t sc, int s, i8v& bi, int& ei) {
+  const uint32_t w[4] = {wq.x, wq.y, wq.z, wq.w};
+  const uint32_t sb = sc >> (16 * s);
+  const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
+  const bool ok = d >= -5 && d <= 6;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) bi[i] = ok ? 0 : int(inlier_fp4<NI>(w[i]));
+#pragma unroll
+  for (int i = 4; i < 8; ++i) bi[i] = 0;
+  ei = int((sb >> 8) & 0xFFu);
+}
+
 template <int MS, int NI, bool HAS_O>
 __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxArgs a) {
   constexpr int BM = 32 * MS;
@@ -219,35 +270,20 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   // (lane half h holds groups {2h, 2h+1, 4+2h, 5+2h} of the step, the fp8
   // operand order) under the scale of block h, plus the flags of blocks that
   // cannot merge.  Without outliers: the fp4 inlier fragment (groups 4h..4h+3).
-  struct BFrag { i8v b; int e; bool split; };
+  // When any block of the wave's step did not merge (wave-uniform flag), the
+  // expansion also builds the fp4 inlier fragment of those blocks (bi, ei), so
+  // that the product loop issues no memory access of its own.
+  struct BFrag { i8v b; int e; bool split; i8v bi; int ei; };
   auto expand = [&](const WRegs& wr, int s) __attribute__((always_inline)) {
     BFrag f;
     const uint4 wq = s ? wr.w1 : wr.w0;
     const uint32_t w[4] = {wq.x, wq.y, wq.z, wq.w};
     if constexpr (HAS_O) {
-      auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
-      auto s13 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
-      const uint32_t u[4] = {s02[0], s13[0], s02[1], s13[1]};
-      // scale bytes of block 2s + b of this row, b = 0, 1 (lane halves 0, 1)
-      auto ss = __builtin_amdgcn_permlane32_swap(wr.sc, wr.sc, false, false);
-      ShiftTable T[2];
-      bool ok[2];
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const uint32_t sb = ss[b] >> (16 * s);
-        const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
-        ok[b] = d >= -5 && d <= 6;
-        T[b] = shift_table(d, ok[b]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint32_t lo, hi;
-        merged_e4m3<NI>(u[i], T[i >> 1], lo, hi);
-        f.b[2 * i] = int(lo);
-        f.b[2 * i + 1] = int(hi);
-      }
-      f.e = int((wr.sc >> (16 * s)) & 0xFFu);  // Eo of block 2s + h
-      f.split = !(ok[0] && ok[1]);
+      const MergedFrag m = expand_merged<NI>(wq, wr.sc, s);
+      f.b = m.b;
+      f.e = m.e;
+      f.split = __any(m.split);
+      if (f.split) split_inliers_fp4<NI>(wq, wr.sc, s, f.bi, f.ei);
     } else {
 #pragma unroll
       for (int i = 0; i < 4; ++i) f.b[i] = int(inlier_fp4<NI>(w[i]));
@@ -258,24 +294,7 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
     }
     return f;
   };
-  // the inliers of blocks that did not merge (fp4 order: block 2s + h of
-  // this lane), for the fp8 x fp4 instruction; chunk c's words are read again
-  // (an L2 hit) so that the common path keeps no copy of them
-  auto split_inliers = [&](int c, int s, i8v& bi, int& ei) __attribute__((always_inline)) {
-    WRegs wr;
-    load_w(c, wr);
-    const uint4 wq = s ? wr.w1 : wr.w0;
-    const uint32_t w[4] = {wq.x, wq.y, wq.z, wq.w};
-    const uint32_t sb = wr.sc >> (16 * s);
-    const int d = int((sb >> 8) & 0xFFu) - int(sb & 0xFFu);
-    const bool ok = d >= -5 && d <= 6;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) bi[i] = ok ? 0 : int(inlier_fp4<NI>(w[i]));
-#pragma unroll
-    for (int i = 4; i < 8; ++i) bi[i] = 0;
-    ei = int((sb >> 8) & 0xFFu);
-  };
-  auto mfmas = [&](int buf, int c, int s, const BFrag& f) __attribute__((always_inline)) {
+  auto mfmas = [&](int buf, int s, const BFrag& f) __attribute__((always_inline)) {
     i8v av[MS];
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms) {
@@ -287,13 +306,10 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms)
         acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], f.b, acc[ms], 0, 0, 0, 127, 0, f.e);
-      if (__any(f.split)) {  // wave-uniform
-        i8v bi;
-        int ei;
-        split_inliers(c, s, bi, ei);
+      if (f.split) {  // wave-uniform, rare: the inliers of blocks that did not merge
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms)
-          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], bi, acc[ms], 0, 4, 0, 127, 0, ei);
+          acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[ms], f.bi, acc[ms], 0, 4, 0, 127, 0, f.ei);
       }
     } else {
 #pragma unroll
@@ -323,9 +339,9 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
     {
       const BFrag f1 = expand(wA, 1);
       load_w(min(c + 2, last), wA);
-      mfmas(0, c, 0, fE);
+      mfmas(0, 0, fE);
       fO = expand(wB, 0);
-      mfmas(0, c, 1, f1);
+      mfmas(0, 1, f1);
       SDQ_STORE_X(1)
       SDQ_LOAD_X(min(c + 2, last))
       __syncthreads();
@@ -334,9 +350,9 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
     {
       const BFrag f1 = expand(wB, 1);
       load_w(min(c + 3, last), wB);
-      mfmas(1, c + 1, 0, fO);
+      mfmas(1, 0, fO);
       fE = expand(wA, 0);
-      mfmas(1, c + 1, 1, f1);
+      mfmas(1, 1, f1);
       SDQ_STORE_X(0)
       SDQ_LOAD_X(min(c + 3, last))
       __syncthreads();

@@ -81,6 +81,22 @@ def test_gemm_matches_oracle(c, M, N, K):
         check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} path={path}")
 
 
+@pytest.mark.parametrize("c", [MX_CFGS[0], MX_CFGS[1], MX_CFGS[3]], ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(512, 256, 256), (600, 100, 384), (777, 544, 128),
+                                   (1030, 288, 640)])
+def test_mx_many_rows(c, M, N, K):
+    """Row counts of large prefill batches: several 256-row blocks, a ragged last
+    block, column groups of eight 32-wide tiles with a ragged last group, and odd
+    and single chunk counts along K."""
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(3, M, K)
+    W = synth.make_w(3, 1, N, K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    say("mx rows", _ids(c), M, N, K)
+    Y, _, _, _ = run_gpu(X, W, cfg)
+    check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K}")
+
+
 def _int_grid(rng, M, N, K, outlier_fmt):
     """Inputs on which every scale is exactly 1 (act, inlier and outlier)."""
     X = rng.integers(-127, 128, (M, K)).astype(np.float32)
@@ -270,7 +286,7 @@ def _split_case(kind, N, K, rng):
 
 @pytest.mark.parametrize("kind", ["product", "zero_inliers", "huge_outliers"])
 @pytest.mark.parametrize("n_i", [2, 3])
-@pytest.mark.parametrize("M,N,K", [(64, 96, 512), (256, 64, 1024)])
+@pytest.mark.parametrize("M,N,K", [(64, 96, 512), (256, 64, 1024), (520, 96, 384)])
 def test_mx_unmergeable_blocks(kind, n_i, M, N, K):
     """The matrix kernel's correction path for blocks that stay split."""
     rng = np.random.default_rng(7)
