@@ -154,6 +154,10 @@ def main():
     Xq = [[torch.empty((M, L.K), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)]
     sa = [[torch.empty((M,), dtype=torch.float32, device=dev) for _ in Ls] for _ in range(R)]
     Y = [[torch.empty((M, L.N), dtype=torch.float32, device=dev) for L in Ls] for _ in range(R)]
+    # GEMM workspace (the two-pass path for many MX tokens), one for all layers:
+    # the calls are ordered on one stream
+    ws_bytes = max(sdq.gemm_workspace_size(cfg, M, L.N, L.K) for L in Ls)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
     stream = torch.cuda.current_stream()
     for r in range(R):  # every rotated copy's Xq/s_a holds real codes before any GEMM-only launch
         for j in range(len(Ls)):
@@ -164,16 +168,16 @@ def main():
         r = i % R
         for j, L in enumerate(Ls):
             sdq.linear(Xd[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], xq=Xq[r][j],
-                       scales=sa[r][j])
+                       scales=sa[r][j], workspace=ws)
 
     def gemms(i):
         r = i % R
         for j, L in enumerate(Ls):
-            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j])
+            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], workspace=ws)
 
     def gemms_hot(i):
         for j, L in enumerate(Ls):
-            sdq.gemm(Xq[0][j], sa[0][j], blobs[0][j], L.N, L.K, cfg, out=Y[0][j])
+            sdq.gemm(Xq[0][j], sa[0][j], blobs[0][j], L.N, L.K, cfg, out=Y[0][j], workspace=ws)
 
     def capture(fn, n, start):
         """HIP graph of n calls of fn (launch-bound loops replay without host gaps)."""
@@ -239,7 +243,7 @@ def main():
 
     flops = sum(2.0 * M * L.N * L.K for L in Ls)
     alg_bytes = logical + sum(M * L.K + 4 * M + 4 * M * L.N for L in Ls)
-    paths = sorted({sdq.gemm_path(cfg, M, L.N, L.K) for L in Ls})
+    paths = sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
     hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family == "mx" and M < 256)
     if hbm_bound:
         achieved = alg_bytes / (gemm_us * 1e-6) / 1e9
@@ -253,6 +257,8 @@ def main():
     tkey = a.workload if a.workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
     roof["traffic"] = measured_traffic(tkey)
     roof["kernel_us"] = round(gemm_us / len(Ls), 3)
+    # kernels per GEMM call: the two-pass path's time is both passes together
+    roof["kernels_per_call"] = 2 if sdq.PATH_DENSE in paths else 1
 
     # ---------------------------------------------------------------- CPU oracle
     cpu = None
@@ -274,7 +280,7 @@ def main():
         "dtype": "int8" if cfg.family == "int" else "fp8",
         "data": "synthetic (seeded generators shaped like the named layers; no weights or datasets)",
         "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
-                   "formats": fmt.label, "gemm_path": ["decode", "mfma"][paths[-1] - 1] if paths else None,
+                   "formats": fmt.label, "gemm_path": ["decode", "mfma", "dense (two passes)"][paths[-1] - 1] if paths else None,
                    "parallelism": "none (one GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,

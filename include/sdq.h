@@ -65,8 +65,8 @@ enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1 };
 enum { SDQ_FMT_INT8 = 1, SDQ_FMT_INT4 = 2, SDQ_FMT_E4M3 = 3, SDQ_FMT_E2M1 = 4 };
 enum { SDQ_METRIC_MAGNITUDE = 0, SDQ_METRIC_PRODUCT = 1 };
 enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
-/* sdq_gemm_ex kernel choice. */
-enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2 };
+/* sdq_gemm_ex / sdq_gemm_ws kernel choice. */
+enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3 };
 
 /* One SDQ configuration (the paper's SDQ-k:m-n_o:m{fmt}-n_i:m{fmt} naming,
  * Section 6 "Methodology", restricted to what the kernels implement):
@@ -91,7 +91,7 @@ typedef struct {
 const char* sdq_status_string(sdq_status s);
 
 /* Validate a configuration for a W of shape [N, K].  K must be a positive
- * multiple of 128 and N positive.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
+ * multiple of 128 up to 2^22 and N positive up to 2^21.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
  * SDQ_ERR_UNSUPPORTED without touching anything else. */
 sdq_status sdq_check(const sdq_config* cfg, int64_t N, int64_t K);
 
@@ -175,7 +175,8 @@ sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int
 /* sdq_gemm with an explicit kernel choice: SDQ_PATH_DECODE (weight-streaming
  * vector kernel, INT family, any M up to 8), SDQ_PATH_MFMA (matrix-core
  * kernels, any M) or SDQ_PATH_AUTO (what sdq_gemm does).  Returns
- * SDQ_ERR_UNSUPPORTED for a path that does not serve the configuration. */
+ * SDQ_ERR_UNSUPPORTED for a path that does not serve the configuration and
+ * for SDQ_PATH_DENSE, which takes a workspace (sdq_gemm_ws). */
 sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, float* Y, void* stream,
                        int32_t path);
@@ -195,6 +196,37 @@ sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int
 /* The path sdq_gemm takes for this configuration and M (SDQ_PATH_DECODE or
  * SDQ_PATH_MFMA). */
 sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K, int32_t* path);
+
+/* Device workspace that sdq_gemm_ws needs (the product is sdq_gemm's,
+ * Section 5.1).  SDQ_PATH_DENSE, the two-pass matrix-core path of the MX
+ * family with outliers, first expands every packed weight once into the dense
+ * fp8 B operand of the matrix instruction (both branches of a 32-K block
+ * merged into one e4m3 value per position under the outlier's e8m0 scale,
+ * wherever the inliers fit it) and then multiplies those operands, so that
+ * the expansion runs once per weight instead of once per weight and block of
+ * 128 tokens.
+ *   path   SDQ_PATH_AUTO (what sdq_gemm_ws takes: SDQ_PATH_DENSE for the MX
+ *          family with outliers when M >= 256, else what sdq_gemm takes), or
+ *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE
+ *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE, 0 for the other paths
+ * Returns SDQ_ERR_UNSUPPORTED for SDQ_PATH_DENSE outside the MX family with
+ * outliers. */
+sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
+                                   int32_t path, size_t* bytes);
+
+/* sdq_gemm_ex with a caller-owned device workspace of ws_bytes bytes (at least
+ * sdq_gemm_workspace_size for the same arguments, else
+ * SDQ_ERR_BUFFER_TOO_SMALL; 16-byte aligned; NULL with ws_bytes = 0 when the
+ * path needs none).  The workspace is scratch: its contents on entry are
+ * ignored and on return unspecified, and calls that share one must be ordered
+ * on one stream.  SDQ_PATH_DENSE gives the results of SDQ_PATH_MFMA bit for
+ * bit when every block merged its inliers (each accumulator takes the same
+ * matrix instructions in the same order); the inliers of blocks that did not
+ * merge are added after the last chunk instead of within their chunk, a
+ * different fp32 rounding order. */
+sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                       const void* packed, int64_t N, int64_t K, float* Y, void* workspace,
+                       size_t ws_bytes, void* stream, int32_t path);
 
 #ifdef __cplusplus
 }

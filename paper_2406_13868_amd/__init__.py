@@ -23,11 +23,12 @@ import numpy as np
 from . import _lib
 from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_INT, FAMILY_MX, FMT_E2M1, FMT_E4M3, FMT_INT4,
                    FMT_INT8, METRIC_MAGNITUDE, METRIC_PRODUCT, PATH_AUTO, PATH_DECODE, PATH_MFMA,
+                   PATH_DENSE,
                    SDQError)
 
 __all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
            "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
-           "PATH_MFMA", "check"]
+           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check"]
 
 _FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
 
@@ -169,9 +170,21 @@ def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
     return Xq, s_a
 
 
+def gemm_workspace_size(cfg: Config, M: int, N: int, K: int, path: int = PATH_AUTO) -> int:
+    """Device workspace bytes the GEMM takes for this shape and path (0: none)."""
+    b = C.c_size_t()
+    _lib.check(_lib.lib().sdq_gemm_workspace_size(C.byref(cfg.c()), M, N, K, path, C.byref(b)),
+               "sdq_gemm_workspace_size")
+    return b.value
+
+
 def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PATH_AUTO,
-         stream=None):
-    """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 output)."""
+         stream=None, workspace=None):
+    """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 output).
+
+    Paths that take a workspace (the two-pass MX path for many tokens) use
+    `workspace` (a uint8 CUDA tensor of at least gemm_workspace_size bytes)
+    or a fresh one."""
     import torch
     M = Xq.shape[0]
     if Xq.shape[1] != K:
@@ -179,15 +192,27 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
     if packed.numel() < pack_size(cfg, N, K):
         raise ValueError("packed buffer too small")
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=Xq.device)
-    _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
-                                      _dev(packed, "packed"), N, K, _dev(Y, "Y"), _stream(stream),
-                                      path), "sdq_gemm")
+    ws_bytes = gemm_workspace_size(cfg, M, N, K, path)
+    if ws_bytes == 0:
+        _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
+                                          _dev(packed, "packed"), N, K, _dev(Y, "Y"),
+                                          _stream(stream), path), "sdq_gemm")
+        return Y
+    ws = workspace if workspace is not None else torch.empty(ws_bytes, dtype=torch.uint8,
+                                                             device=Xq.device)
+    _lib.check(_lib.lib().sdq_gemm_ws(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
+                                      _dev(packed, "packed"), N, K, _dev(Y, "Y"),
+                                      _dev(ws, "workspace"), ws.numel() * ws.element_size(),
+                                      _stream(stream), path), "sdq_gemm_ws")
     return Y
 
 
-def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=None, stream=None):
+def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=None, stream=None,
+           workspace=None):
     """Quantize X per token and multiply: returns (Y, Xq, s_a).  One fused
-    kernel on the decode path; otherwise the two kernels back to back."""
+    kernel on the decode path (sdq_linear); sdq_quantize_act then
+    sdq_gemm_ws where the GEMM takes a workspace; otherwise sdq_linear's two
+    kernels back to back."""
     import torch
     M = X.shape[0]
     if X.shape[1] != K:
@@ -201,13 +226,20 @@ def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=Non
     Xq = xq if xq is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
     s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
     Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=X.device)
+    if gemm_workspace_size(cfg, M, N, K) > 0:
+        quantize_act(X, cfg, out=Xq, scales=s_a, stream=stream)
+        gemm(Xq, s_a, packed, N, K, cfg, out=Y, stream=stream, workspace=workspace)
+        return Y, Xq, s_a
     _lib.check(_lib.lib().sdq_linear(C.byref(cfg.c()), _dev(X, "X"), dt, M, _dev(Xq, "Xq"),
                                      _dev(s_a, "s_a"), _dev(packed, "packed"), N, K, _dev(Y, "Y"),
                                      _stream(stream)), "sdq_linear")
     return Y, Xq, s_a
 
 
-def gemm_path(cfg: Config, M: int, N: int, K: int) -> int:
+def gemm_path(cfg: Config, M: int, N: int, K: int, workspace: bool = False) -> int:
+    """The path sdq_gemm takes (or sdq_gemm_ws, with workspace=True)."""
+    if workspace and gemm_workspace_size(cfg, M, N, K) > 0:
+        return PATH_DENSE
     p = C.c_int32()
     _lib.check(_lib.lib().sdq_gemm_path(C.byref(cfg.c()), M, N, K, C.byref(p)), "sdq_gemm_path")
     return p.value

@@ -17,13 +17,13 @@ FAMILY_INT, FAMILY_MX = 0, 1
 FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
 METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
 DTYPE_F32, DTYPE_BF16 = 0, 1
-PATH_AUTO, PATH_DECODE, PATH_MFMA = 0, 1, 2
+PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE = 0, 1, 2, 3
 
 # Every exported symbol, as declared in include/sdq.h.
 EXPORTS = (
     "sdq_status_string", "sdq_check", "sdq_pack_size", "sdq_logical_bytes", "sdq_pack",
     "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
-    "sdq_gemm_path", "sdq_linear",
+    "sdq_gemm_path", "sdq_linear", "sdq_gemm_workspace_size", "sdq_gemm_ws",
 )
 
 
@@ -65,6 +65,9 @@ def lib() -> C.CDLL:
             "sdq_gemm": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp]),
             "sdq_gemm_ex": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),
             "sdq_gemm_path": (C.c_int, [cfgp, i64, i64, i64, P(C.c_int32)]),
+            "sdq_gemm_workspace_size": (C.c_int, [cfgp, i64, i64, i64, C.c_int32, P(C.c_size_t)]),
+            "sdq_gemm_ws": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_size_t, vp,
+                                      C.c_int32]),
             "sdq_linear": (C.c_int, [cfgp, vp, C.c_int32, i64, vp, vp, vp, i64, i64, vp, vp]),
         }
         for name, (res, args) in sig.items():

@@ -27,6 +27,7 @@ SOURCES = [
     "gemm_int_decode.hip",
     "gemm_int_mfma.hip",
     "gemm_mx_mfma.hip",
+    "gemm_mx_dense.hip",
 ]
 
 COMMON = [

@@ -23,6 +23,13 @@ int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
   return SDQ_PATH_MFMA;
 }
 
+// The path of sdq_gemm_ws: the two-pass form where its one expansion per
+// weight beats one per weight and 128 tokens.
+int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t K) {
+  if (c.mx && c.n_o > 0 && M >= kDenseMinM) return SDQ_PATH_DENSE;
+  return auto_path(c, M, K);
+}
+
 }  // namespace
 
 extern "C" const char* sdq_status_string(sdq_status s) {
@@ -76,7 +83,8 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
-  if (path != SDQ_PATH_AUTO && path != SDQ_PATH_DECODE && path != SDQ_PATH_MFMA) return SDQ_ERR_CONFIG;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path == SDQ_PATH_DENSE) return SDQ_ERR_UNSUPPORTED;  // needs a workspace: sdq_gemm_ws
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16)
@@ -101,6 +109,46 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   if (log_enabled())
     std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s\n", (long long)M, (long long)N,
                  (long long)K, name);
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N,
+                                              int64_t K, int32_t path, size_t* bytes) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!bytes) return SDQ_ERR_NULL;
+  if (M < 0) return SDQ_ERR_SHAPE;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, K);
+  if (path == SDQ_PATH_DENSE && !(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
+  *bytes = path == SDQ_PATH_DENSE ? mx_dense_workspace_bytes(N, K) : 0;
+  return SDQ_OK;
+}
+
+extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a,
+                                  int64_t M, const void* packed, int64_t N, int64_t K, float* Y,
+                                  void* workspace, size_t ws_bytes, void* stream, int32_t path) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, K);
+  if (path != SDQ_PATH_DENSE) return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
+  if (!(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
+  if (M == 0) return SDQ_OK;
+  if (!Xq || !s_a || !packed || !Y || !workspace) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
+      reinterpret_cast<uintptr_t>(workspace) % 16)
+    return SDQ_ERR_SHAPE;
+  if (ws_bytes < mx_dense_workspace_bytes(N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  const hipError_t e = launch_mx_dense(c, static_cast<const uint8_t*>(Xq), s_a, M,
+                                       static_cast<const uint8_t*>(packed), N, K, Y, workspace,
+                                       static_cast<hipStream_t>(stream));
+  if (log_enabled())
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> mx_dense (two passes)\n", (long long)M,
+                 (long long)N, (long long)K);
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 

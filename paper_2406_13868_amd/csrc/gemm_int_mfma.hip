@@ -22,6 +22,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
+#include "tile_out.h"
 
 namespace sdq {
 namespace {
@@ -212,13 +213,12 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+  const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
+  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + ms * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-      if (m < a.M) a.Y[size_t(m) * a.N + n] = a.s_a[m] * fmaf(so, acco[ms][e], acc[ms][e]);
-    }
+    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, acco[ms][e], acc[ms][e]));
 }
 
 // Split-K form for few tokens (M <= 64): one 32-row tile of W per workgroup,
@@ -358,13 +358,12 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+  const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
+  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + ms * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
-      if (m < a.M) a.Y[size_t(m) * a.N + n] = a.s_a[m] * fmaf(so, acco[ms][e], acc[ms][e]);
-    }
+    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, acco[ms][e], acc[ms][e]));
 }
 
 template <int MS, int NI, int NW>

@@ -1,0 +1,343 @@
+// MX-family decomposed GEMM for many tokens, in two passes.  Section 5.1
+// computes Y = s_a * Xq (W_o + W_i)^T with both branches accumulated into one
+// fp32 accumulator per output.
+//
+// The one-pass kernel (gemm_mx_mfma.hip) expands every packed weight fragment
+// into its merged e4m3 form once per block of tokens.  At prefill sizes that
+// vector work, repeated for every 128 tokens, costs more issue cycles than the
+// matrix instructions it feeds.  Here every weight is expanded once:
+//   pass 1, mx_densify_kernel: every (32-row tile, 128-K chunk) unit of the
+//     blob becomes its two merged e4m3 B fragments (mx_frag.h), written to a
+//     workspace in the order the matrix instruction reads them;
+//   pass 2, mx_dense_kernel: an fp8 x fp8 scaled-MFMA GEMM over the
+//     workspace, the outlier scales (Eo, the merged fragments' e8m0 scales)
+//     read from the blob's scale words.
+// Blocks whose inliers cannot merge (Ei - Eo outside [-5, 6]) carry only their
+// outliers in the merged fragments; pass 2 adds their inliers after its main
+// loop with the fp8 x fp4 instruction, when the scale words it read show one.
+//
+// Workspace layout, one 16-byte piece per lane:
+//   uint4 frag[n_tiles][n_chunks][2 steps][2 halves][64 lanes]
+// half 0 holds dwords 0-3 and half 1 dwords 4-7 of lane l's fp8 B operand for
+// 64-K step s of the chunk, so that every load of a wave is 1 KB contiguous.
+//
+// Pass 2 tiling: a workgroup of 4 waves (one per SIMD) owns 128 tokens and 8
+// row tiles (256 outputs); each wave owns 2 tiles x 4 sub-tiles of 32 tokens
+// (8 accumulators of 32x32), so every A fragment read from LDS feeds two
+// matrix instructions.  Activations are staged per 128-K chunk in LDS (double
+// buffered, XOR-swizzled); B fragments go from the workspace straight into
+// registers, requested three 64-K steps ahead.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+#include "mx_frag.h"
+#include "tile_out.h"
+
+namespace sdq {
+namespace {
+
+using namespace mx;
+
+constexpr int kUnitPieces = 256;  // uint4 pieces per (tile, chunk) in the workspace
+constexpr int kDWaves = 4;
+constexpr int kDThreads = kDWaves * 64;
+constexpr int kDTiles = 2 * kDWaves;  // row tiles per workgroup
+constexpr int kDMS = 4;               // 32-token sub-tiles per wave
+constexpr int kDBM = 32 * kDMS;       // tokens per workgroup
+
+// ---- pass 1 ----------------------------------------------------------------
+// One wave per (tile, chunk) unit u = tile * n_chunks + chunk, the order of
+// the blob's words and scale words, so reads and writes both stream.
+template <int NI>
+__global__ __launch_bounds__(256) void mx_densify_kernel(const uint8_t* __restrict__ blob,
+                                                         int64_t scales_off, int n_units,
+                                                         uint4* __restrict__ frag) {
+  const int lane = threadIdx.x & 63;
+  const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (u >= n_units) return;  // whole waves
+  const uint8_t* wp = blob + size_t(u) * kWordBytesPerTC + lane * 16;
+  const uint4 w0 = *reinterpret_cast<const uint4*>(wp);
+  const uint4 w1 = *reinterpret_cast<const uint4*>(wp + 1024);
+  const uint32_t sc =
+      *reinterpret_cast<const uint32_t*>(blob + scales_off + size_t(u) * kMxScaleBytesPerTC + lane * 4);
+  uint4* out = frag + size_t(u) * kUnitPieces + lane;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const MergedFrag f = expand_merged<NI>(s ? w1 : w0, sc, s);
+    out[s * 128] = make_uint4(f.b[0], f.b[1], f.b[2], f.b[3]);
+    out[s * 128 + 64] = make_uint4(f.b[4], f.b[5], f.b[6], f.b[7]);
+  }
+}
+
+// ---- pass 2 ----------------------------------------------------------------
+struct DenseArgs {
+  const uint8_t* Xq;
+  const float* s_a;
+  const uint8_t* blob;
+  const uint4* frag;
+  float* Y;
+  int M, N, K, n_chunks, n_tiles;
+  int64_t scales_off;
+  int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
+};
+
+typedef int i4v __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane through a buffer resource (tile_out.h)
+__device__ __forceinline__ i4v load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+
+// whether a lane's scale word (Eo, Ei of its block in steps 0 and 1) holds a
+// block that did not merge its inliers
+__device__ __forceinline__ bool unmerged(uint32_t sc) {
+  const int d0 = int((sc >> 8) & 0xFFu) - int(sc & 0xFFu);
+  const int d1 = int((sc >> 24) & 0xFFu) - int((sc >> 16) & 0xFFu);
+  return d0 < -5 || d0 > 6 || d1 < -5 || d1 > 6;
+}
+
+template <int NI>
+__global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
+  // fp8 activations of one 128-K chunk: 128 rows of 128 bytes, 16-byte piece
+  // p of row r at piece p ^ lds_swizzle(r)
+  __shared__ __align__(16) uint8_t xs[2][kDBM * kChunkK];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, h = lane >> 5;
+  // every XCD takes a contiguous range of tile groups and all their M blocks,
+  // so that a tile's fragments are reused from that XCD's L2
+  const int work = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int group = work / a.m_blocks;
+  const int m0 = (work - group * a.m_blocks) * kDBM;
+  const int KC = a.n_chunks;
+  const int last = KC - 1;
+
+  int tile[2];
+  bool tok[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int t = group * kDTiles + 2 * wave + j;
+    tok[j] = t < a.n_tiles;
+    tile[j] = min(t, a.n_tiles - 1);  // spare waves recompute the last tile
+  }
+
+  // ---- activations of this block's rows (rows past M read 0, never stored)
+  const __amdgpu_buffer_rsrc_t xr_rsrc =
+      buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, kDBM)) * uint32_t(a.K));
+  // thread tid moves piece tid & 7 of rows (tid >> 3) + 32 i, i < 4; rows r
+  // and r + 32 i share their swizzle
+  const uint32_t xoff = uint32_t(tid >> 3) * uint32_t(a.K) + (tid & 7) * 16;
+  const uint32_t xrow32 = 32u * uint32_t(a.K);
+  const uint32_t xdst0 = uint32_t((tid >> 3) * kChunkK + (((tid & 7) ^ lds_swizzle(tid >> 3)) << 4));
+  // two register sets: even chunks in X0, odd chunks in X1, each loaded two
+  // chunks before its products and stored to LDS one chunk before them
+  struct XRegs { i4v r0, r1, r2, r3; };
+  auto load_x = [&](int c, XRegs& x) __attribute__((always_inline)) {
+    const uint32_t so = uint32_t(c) * kChunkK;
+    x.r0 = load16(xr_rsrc, xoff, so);
+    x.r1 = load16(xr_rsrc, xoff + xrow32, so);
+    x.r2 = load16(xr_rsrc, xoff + 2 * xrow32, so);
+    x.r3 = load16(xr_rsrc, xoff + 3 * xrow32, so);
+  };
+  auto store_x = [&](int buf, const XRegs& x) __attribute__((always_inline)) {
+    *reinterpret_cast<i4v*>(&xs[buf][xdst0]) = x.r0;
+    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 32 * kChunkK]) = x.r1;
+    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 64 * kChunkK]) = x.r2;
+    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 96 * kChunkK]) = x.r3;
+  };
+
+  // ---- B fragments and scale words of the wave's two tiles
+  __amdgpu_buffer_rsrc_t fr[2], sr[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    fr[j] = buffer_rsrc(a.frag + size_t(tile[j]) * KC * kUnitPieces, uint32_t(KC) * kUnitPieces * 16);
+    sr[j] = buffer_rsrc(a.blob + a.scales_off + size_t(tile[j]) * KC * kMxScaleBytesPerTC,
+                        uint32_t(KC) * kMxScaleBytesPerTC);
+  }
+  const uint32_t boff = uint32_t(lane) * 16, soff_l = uint32_t(lane) * 4;
+  struct BStep { i8v b[2]; };
+  auto load_b = [&](int c, int s, BStep& r) __attribute__((always_inline)) {
+    const uint32_t so = (uint32_t(c) * 2 + s) * 2048;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const i4v q0 = load16(fr[j], boff, so);
+      const i4v q1 = load16(fr[j], boff + 1024, so);
+      r.b[j] = __builtin_shufflevector(q0, q1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  };
+  struct Scales { uint32_t w[2]; };
+  auto load_sc = [&](int c, Scales& r) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      r.w[j] = __builtin_amdgcn_raw_buffer_load_b32(sr[j], soff_l, uint32_t(c) * kMxScaleBytesPerTC, 0);
+  };
+
+  f16v acc[2][kDMS];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int ms = 0; ms < kDMS; ++ms)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
+
+  // A-fragment byte offsets of this lane in a chunk buffer: row ms*32 + col,
+  // logical pieces 4s + h and 4s + h + 2 for step s
+  uint32_t aoff[2][2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      aoff[s][u] = uint32_t(col * kChunkK + (((4 * s + h + 2 * u) ^ lds_swizzle(col)) << 4));
+
+  bool bad = false;  // this lane saw a block whose inliers did not merge
+  auto mfmas = [&](int buf, int s, const BStep& B, const Scales& S) __attribute__((always_inline)) {
+    int e[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) e[j] = int((S.w[j] >> (16 * s)) & 0xFFu);  // Eo of block 2s + h
+#pragma unroll
+    for (int ms = 0; ms < kDMS; ++ms) {
+      const i4v a0 = *reinterpret_cast<const i4v*>(&xs[buf][aoff[s][0] + ms * 32 * kChunkK]);
+      const i4v a1 = *reinterpret_cast<const i4v*>(&xs[buf][aoff[s][1] + ms * 32 * kChunkK]);
+      const i8v av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[j][ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, B.b[j], acc[j][ms], 0, 0, 0, 127, 0, e[j]);
+    }
+  };
+
+  // The products of a chunk stay before its barrier: the matrix intrinsic has
+  // no memory effects, so without this the compiler sinks them past the
+  // barrier and the loads of the next chunk no longer overlap them.
+  auto pin_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int ms = 0; ms < kDMS; ++ms) asm volatile("" : "+a"(acc[j][ms]));
+  };
+
+  // ---- pipeline.  Chunk c uses LDS buffer c & 1, B step sets B0, B1 (even
+  //      chunks) or B2, B3 (odd chunks) and scale set S0 or S1; a set is
+  //      refilled for chunk c + 2 right after its products.  Activations of
+  //      chunk c + 1 go from registers to LDS after the products of chunk c,
+  //      and those of chunk c + 3 are requested then.  Loads past the last
+  //      chunk re-read it (never used).
+  BStep B0, B1, B2, B3;
+  Scales S0, S1;
+  XRegs X0, X1;
+  load_x(0, X0);
+  load_x(min(1, last), X1);
+  load_b(0, 0, B0);
+  load_b(0, 1, B1);
+  load_sc(0, S0);
+  load_b(min(1, last), 0, B2);
+  load_b(min(1, last), 1, B3);
+  load_sc(min(1, last), S1);
+  store_x(0, X0);
+  load_x(min(2, last), X0);
+  __syncthreads();
+  for (int c = 0; c + 1 < KC; c += 2) {  // one exit, so the accumulators stay in place
+    mfmas(0, 0, B0, S0);
+    load_b(min(c + 2, last), 0, B0);
+    mfmas(0, 1, B1, S0);
+    load_b(min(c + 2, last), 1, B1);
+    bad |= unmerged(S0.w[0]) || unmerged(S0.w[1]);
+    load_sc(min(c + 2, last), S0);
+    store_x(1, X1);
+    load_x(min(c + 3, last), X1);
+    pin_acc();
+    __syncthreads();
+    mfmas(1, 0, B2, S1);
+    load_b(min(c + 3, last), 0, B2);
+    mfmas(1, 1, B3, S1);
+    load_b(min(c + 3, last), 1, B3);
+    bad |= unmerged(S1.w[0]) || unmerged(S1.w[1]);
+    load_sc(min(c + 3, last), S1);
+    store_x(0, X0);
+    load_x(min(c + 4, last), X0);
+    pin_acc();
+    __syncthreads();
+  }
+  if (KC & 1) {  // the last chunk of an odd count, in LDS buffer 0
+    mfmas(0, 0, B0, S0);
+    mfmas(0, 1, B1, S0);
+    bad |= unmerged(S0.w[0]) || unmerged(S0.w[1]);
+  }
+
+  // ---- inliers of blocks that did not merge (rare; wave-uniform branches):
+  //      fp8 x fp4 products, A read from global memory
+  if (__any(bad)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const __amdgpu_buffer_rsrc_t wr =
+          buffer_rsrc(a.blob + size_t(tile[j]) * KC * kWordBytesPerTC, uint32_t(KC) * kWordBytesPerTC);
+      for (int c = 0; c < KC; ++c) {
+        const uint32_t sc = __builtin_amdgcn_raw_buffer_load_b32(sr[j], soff_l, uint32_t(c) * kMxScaleBytesPerTC, 0);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const uint32_t q = sc >> (16 * s);
+          const int d = int((q >> 8) & 0xFFu) - int(q & 0xFFu);
+          if (!__any(d < -5 || d > 6)) continue;
+          const i4v wv = load16(wr, boff + s * 1024, uint32_t(c) * kWordBytesPerTC);
+          i8v bi;
+          int ei;
+          split_inliers_fp4<NI>(make_uint4(wv[0], wv[1], wv[2], wv[3]), sc, s, bi, ei);
+#pragma unroll
+          for (int ms = 0; ms < kDMS; ++ms) {
+            const uint32_t ao = uint32_t(ms * 32 + col) * uint32_t(a.K) + s * 64 + h * 16;
+            const i4v a0 = load16(xr_rsrc, ao, uint32_t(c) * kChunkK);
+            const i4v a1 = load16(xr_rsrc, ao + 32, uint32_t(c) * kChunkK);
+            const i8v av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+            acc[j][ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bi, acc[j][ms], 0, 4, 0, 127, 0, ei);
+          }
+        }
+      }
+    }
+  }
+
+  const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
+  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, kDBM);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (!tok[j]) continue;
+    const int n = tile[j] * kTileN + col;
+    if (n >= a.N) continue;
+#pragma unroll
+    for (int ms = 0; ms < kDMS; ++ms)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * acc[j][ms][e]);
+  }
+}
+
+template <int NI>
+hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8_t* blob,
+                     const Layout& L, int64_t N, int64_t K, float* Y, uint4* frag, hipStream_t st) {
+  const int n_units = int(L.n_tiles * L.n_chunks);
+  hipLaunchKernelGGL((mx_densify_kernel<NI>), dim3(unsigned((n_units + 3) / 4)), dim3(256), 0, st,
+                     blob, L.scales_off, n_units, frag);
+  DenseArgs a{Xq, s_a, blob, frag, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
+              L.scales_off, int((M + kDBM - 1) / kDBM)};
+  const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
+  hipLaunchKernelGGL((mx_dense_kernel<NI>), dim3(unsigned(groups * a.m_blocks)), dim3(kDThreads), 0,
+                     st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t mx_dense_workspace_bytes(int64_t N, int64_t K) {
+  const Layout L = make_layout(true, N, K);
+  return size_t(L.n_tiles) * size_t(L.n_chunks) * kUnitPieces * sizeof(uint4);
+}
+
+hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                           const uint8_t* blob, int64_t N, int64_t K, float* Y, void* workspace,
+                           hipStream_t st) {
+  const Layout L = make_layout(true, N, K);
+  uint4* frag = static_cast<uint4*>(workspace);
+  if (c.n_i == 1) return launch_ni<1>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
+  if (c.n_i == 2) return launch_ni<2>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
+  return launch_ni<3>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
+}
+
+}  // namespace sdq

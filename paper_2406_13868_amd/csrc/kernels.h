@@ -44,4 +44,13 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                           const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
 
+// MX family with outliers, two passes for many tokens: the blob is expanded
+// once into dense merged fp8 fragments in `workspace` (at least
+// mx_dense_workspace_bytes(N, K) bytes, 16-byte aligned), then multiplied.
+constexpr int64_t kDenseMinM = 256;
+size_t mx_dense_workspace_bytes(int64_t N, int64_t K);
+hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                           const uint8_t* blob, int64_t N, int64_t K, float* Y, void* workspace,
+                           hipStream_t st);
+
 }  // namespace sdq

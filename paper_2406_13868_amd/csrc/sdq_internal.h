@@ -30,7 +30,9 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   // What the kernels implement.
   if (c->m_i != 8 || c->n_i > 3) return SDQ_ERR_UNSUPPORTED;
   if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
-  if (N <= 0 || K <= 0 || K % 128 != 0) return SDQ_ERR_SHAPE;
+  // upper bounds keep every per-block offset of the kernels in 32 bits
+  if (N <= 0 || K <= 0 || K % 128 != 0 || N > (int64_t(1) << 21) || K > (int64_t(1) << 22))
+    return SDQ_ERR_SHAPE;
   if (N > (int64_t(1) << 31) || K > (int64_t(1) << 24)) return SDQ_ERR_SHAPE;
   if (out) {
     out->mx = mx;

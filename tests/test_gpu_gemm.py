@@ -60,9 +60,11 @@ def check(Y, Yref, X, W, cfg_o, what=""):
     return assert_close(Y, Yref, what)
 
 
-def _paths(fam, M):
+def _paths(fam, M, n_o=1):
     if fam == "int" and M <= 8:
         return [sdq.PATH_DECODE, sdq.PATH_MFMA]
+    if fam == "mx" and n_o:
+        return [sdq.PATH_MFMA, sdq.PATH_DENSE]
     return [sdq.PATH_MFMA]
 
 
@@ -75,7 +77,7 @@ def test_gemm_matches_oracle(c, M, N, K):
     X = synth.make_x(1, M, K)
     W = synth.make_w(1, 0, N, K)
     Yref, _, _, _ = S.reference(X, W, cfg_o)
-    for path in _paths(c[0], M):
+    for path in _paths(c[0], M, c[1]):
         say("gemm", _ids(c), M, N, K, "path", path)
         Y, _, _, _ = run_gpu(X, W, cfg, path)
         check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} path={path}")
@@ -85,16 +87,41 @@ def test_gemm_matches_oracle(c, M, N, K):
 @pytest.mark.parametrize("M,N,K", [(512, 256, 256), (600, 100, 384), (777, 544, 128),
                                    (1030, 288, 640)])
 def test_mx_many_rows(c, M, N, K):
-    """Row counts of large prefill batches: several 256-row blocks, a ragged last
-    block, column groups of eight 32-wide tiles with a ragged last group, and odd
-    and single chunk counts along K."""
+    """Row counts of large prefill batches: several token blocks, a ragged last
+    block, column groups of 32-wide tiles with a ragged last group, and odd and
+    single chunk counts along K, on both matrix-core paths."""
     cfg, cfg_o = _cfgs(*c)
     X = synth.make_x(3, M, K)
     W = synth.make_w(3, 1, N, K)
     Yref, _, _, _ = S.reference(X, W, cfg_o)
-    say("mx rows", _ids(c), M, N, K)
-    Y, _, _, _ = run_gpu(X, W, cfg)
-    check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K}")
+    for path in (sdq.PATH_AUTO, sdq.PATH_MFMA):
+        say("mx rows", _ids(c), M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} path={path}")
+
+
+@pytest.mark.parametrize("c", [MX_CFGS[0], MX_CFGS[1], MX_CFGS[2], MX_CFGS[3]], ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (40, 100, 384), (256, 288, 640), (300, 544, 128)])
+def test_dense_equals_one_pass(c, M, N, K):
+    """Where every block merges its inliers the two-pass path runs the same
+    matrix instructions per accumulator in the same order as the one-pass
+    kernel: the outputs agree bit for bit."""
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(3, M, K)
+    W = synth.make_w(3, 2, N, K)
+    L = S.pack_logical(W, cfg_o)
+    d = L["scale_i"].astype(int) - L["scale_o"].astype(int)
+    assert not np.any((d < -5) | (d > 6)), "the case holds an unmergeable block"
+    torch = torch_cuda()
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    Xq, s_a = sdq.quantize_act(torch.from_numpy(X).cuda(), cfg)
+    say("dense vs one pass", _ids(c), M, N, K)
+    Y1 = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=sdq.PATH_MFMA)
+    ws = torch.full((sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_DENSE),), 0xAB,
+                    dtype=torch.uint8, device="cuda")  # stale contents must not matter
+    Y2 = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=sdq.PATH_DENSE, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
 
 
 def _int_grid(rng, M, N, K, outlier_fmt):
@@ -141,9 +168,10 @@ def test_mx_grid_is_exact(M, N, K):
     W[:, 5::8] = (256 + 32 * rng.integers(0, 7, (N, K // 8))).astype(np.float32)  # e4m3-exact outliers, E = 0
     Yref, _, s_ref, L = S.reference(X, W, cfg_o)
     assert (s_ref == 1).all() and (L["scale_i"] == 127).all() and (L["scale_o"] == 127).all()
-    say("mx grid", M, N, K)
-    Y, _, _, _ = run_gpu(X, W, cfg)
-    assert np.array_equal(Y.astype(np.float64), Yref)
+    for path in (sdq.PATH_MFMA, sdq.PATH_DENSE):
+        say("mx grid", M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        assert np.array_equal(Y.astype(np.float64), Yref), f"path {path}"
 
 
 @pytest.mark.parametrize("c", [INT_CFGS[0], MX_CFGS[0]], ids=_ids)
@@ -170,9 +198,10 @@ def test_degenerate_inputs(c):
     blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
     Xq = torch.zeros((0, 256), dtype=torch.uint8, device="cuda")
     s_a = torch.zeros((0,), dtype=torch.float32, device="cuda")
-    Y = sdq.gemm(Xq, s_a, blob, 64, 256, cfg)
-    torch.cuda.synchronize()
-    assert Y.shape == (0, 64)
+    for path in _paths(c[0], 0, c[1]):
+        Y = sdq.gemm(Xq, s_a, blob, 64, 256, cfg, path=path)
+        torch.cuda.synchronize()
+        assert Y.shape == (0, 64)
 
 
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], MX_CFGS[0]], ids=_ids)
@@ -263,6 +292,39 @@ def test_hip_graph_replays_match_eager(c):
         torch.cuda.synchronize()
 
 
+def test_hip_graph_replays_match_eager_two_pass():
+    """The two-pass MX path (workspace allocated before capture) replays like eager."""
+    torch = torch_cuda()
+    cfg, _ = _cfgs(*MX_CFGS[1])
+    N, K, M = 544, 640, 300
+    X = torch.from_numpy(synth.make_x(2, M, K)).cuda()
+    blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
+    Xq, s_a = sdq.quantize_act(X, cfg)
+    assert sdq.gemm_workspace_size(cfg, M, N, K) > 0
+    ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K), dtype=torch.uint8, device="cuda")
+    Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    say("graph two-pass")
+    sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+    torch.cuda.synchronize()
+    ref = Y.clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+    for rep in range(4):
+        Y.fill_(float("nan"))
+        ws.fill_(0x5A)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y), workspace=ws)
+        torch.cuda.synchronize()
+
+
 def _split_case(kind, N, K, rng):
     """MX weights whose blocks cannot merge the inliers into the outliers' e4m3
     fragment (inlier/outlier exponent difference outside [-5, 6])."""
@@ -287,7 +349,8 @@ def _split_case(kind, N, K, rng):
 @pytest.mark.parametrize("kind", ["product", "zero_inliers", "huge_outliers"])
 @pytest.mark.parametrize("n_i", [2, 3])
 @pytest.mark.parametrize("M,N,K", [(64, 96, 512), (256, 64, 1024), (520, 96, 384)])
-def test_mx_unmergeable_blocks(kind, n_i, M, N, K):
+@pytest.mark.parametrize("path", [sdq.PATH_MFMA, sdq.PATH_DENSE])
+def test_mx_unmergeable_blocks(kind, n_i, M, N, K, path):
     """The matrix kernel's correction path for blocks that stay split."""
     rng = np.random.default_rng(7)
     metric = "product" if kind == "product" else "magnitude"
@@ -299,11 +362,11 @@ def test_mx_unmergeable_blocks(kind, n_i, M, N, K):
     L = S.pack_logical(W, cfg_o, an)
     d = L["scale_i"].astype(int) - L["scale_o"].astype(int)
     assert np.any((d < -5) | (d > 6)), "no unmergeable block in the case"
-    say("mx split", kind, n_i, M, N, K)
+    say("mx split", kind, n_i, M, N, K, "path", path)
     torch = torch_cuda()
     blob = torch.from_numpy(sdq.pack(W, cfg, act_norm=an)).cuda()
     Xq, s_a = sdq.quantize_act(torch.from_numpy(X).cuda(), cfg)
-    Y = sdq.gemm(Xq, s_a, blob, N, K, cfg).cpu().numpy()
+    Y = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path).cpu().numpy()
     Yref, _, _, _ = S.reference(X, W, cfg_o, an)
     A = np.abs(S.dequant_act(*S.quantize_act(X, cfg_o), cfg_o))
     T = A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T

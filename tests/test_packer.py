@@ -217,6 +217,36 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(sdq.Config.mx_family(), 1, 4096, 4096) == sdq.PATH_MFMA
 
 
+def test_gemm_workspace_size_and_validation():
+    """The two-pass MX path: its workspace is one byte per weight position of
+    the 32-row tiles, its automatic choice, and the checks that run before any
+    GPU work."""
+    mx, mx_no = sdq.Config.mx_family(), sdq.Config("mx", 0, 8, "e4m3", 2, 8, "e2m1", "e4m3")
+    it = sdq.Config.int_family()
+    assert sdq.gemm_workspace_size(mx, 2048, 11008, 4096) == 11008 * 4096
+    assert sdq.gemm_workspace_size(mx, 256, 100, 384) == 128 * 384      # N padded to 32
+    assert sdq.gemm_workspace_size(mx, 255, 100, 384) == 0               # one pass below 256 tokens
+    assert sdq.gemm_workspace_size(mx, 1, 100, 384, sdq.PATH_DENSE) == 128 * 384
+    assert sdq.gemm_workspace_size(mx, 4096, 100, 384, sdq.PATH_MFMA) == 0
+    assert sdq.gemm_workspace_size(mx_no, 4096, 100, 384) == 0           # no outlier branch
+    assert sdq.gemm_workspace_size(it, 4096, 100, 384) == 0
+    for cfg in (mx_no, it):
+        with pytest.raises(sdq.SDQError) as e:
+            sdq.gemm_workspace_size(cfg, 4096, 100, 384, sdq.PATH_DENSE)
+        assert e.value.status == -6
+    L = _lib.lib()
+    c = mx.c()
+    p = C.c_void_p(256)  # never dereferenced: every call below fails its checks first
+    need = 128 * 384
+    assert L.sdq_gemm_ws(C.byref(c), p, p, 300, p, 100, 384, p, p, need - 1, None, 3) == -4
+    assert L.sdq_gemm_ws(C.byref(c), p, p, 300, p, 100, 384, p, None, need, None, 3) == -1
+    assert L.sdq_gemm_ws(C.byref(c), p, p, 300, p, 100, 384, p, C.c_void_p(264), need, None, 3) == -2
+    assert L.sdq_gemm_ws(C.byref(c), p, p, 300, p, 100, 384, p, p, need, None, 9) == -3
+    assert L.sdq_gemm_ws(C.byref(c), p, p, 0, p, 100, 384, p, None, 0, None, 3) == 0   # M = 0
+    assert L.sdq_gemm_ws(C.byref(it.c()), p, p, 300, p, 100, 384, p, p, need, None, 3) == -6
+    assert L.sdq_gemm_ex(C.byref(c), p, p, 300, p, 100, 384, p, None, 3) == -6  # needs a workspace
+
+
 @pytest.mark.parametrize("c", [c for c in CONFIGS if c[1] == 0 or c[2] == 16], ids=_ids)
 def test_absent_outlier_position_is_free(c):
     """A group word without an outlier (1:16 words, or no outlier branch) keeps
