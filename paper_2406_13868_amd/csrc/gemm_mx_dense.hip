@@ -105,11 +105,9 @@ __global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, h = lane >> 5;
-  // every XCD takes a contiguous range of tile groups and all their M blocks,
-  // so that a tile's fragments are reused from that XCD's L2
-  const int work = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int group = work / a.m_blocks;
-  const int m0 = (work - group * a.m_blocks) * kDBM;
+  int group, mblock;
+  tile_work(blockIdx.x, gridDim.x / a.m_blocks, a.m_blocks, group, mblock);
+  const int m0 = mblock * kDBM;
   const int KC = a.n_chunks;
   const int last = KC - 1;
 
@@ -236,6 +234,10 @@ __global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
   store_x(0, X0);
   load_x(min(2, last), X0);
   __syncthreads();
+  // Every request of the prologue complete before the loop: the wait counts
+  // the compiler derives at the loop head then come from the loop's own
+  // order of requests alone, not from the stricter ones of the prologue.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   for (int c = 0; c + 1 < KC; c += 2) {  // one exit, so the accumulators stay in place
     mfmas(0, 0, B0, S0);
     load_b(min(c + 2, last), 0, B0);

@@ -50,11 +50,9 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, h = lane >> 5;
-  // every XCD takes a contiguous range of tile groups and all their M blocks,
-  // so a tile's weights are reused from that XCD's L2
-  const int work = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int group = work / a.m_blocks;
-  const int m0 = (work - group * a.m_blocks) * BM;
+  int group, mblock;
+  tile_work(blockIdx.x, gridDim.x / a.m_blocks, a.m_blocks, group, mblock);
+  const int m0 = mblock * BM;
   const int tile = min(group * kWaves + wave, a.n_tiles - 1);  // spare waves recompute the last tile
   const bool tile_ok = group * kWaves + wave < a.n_tiles;
   const int KC = a.n_chunks;

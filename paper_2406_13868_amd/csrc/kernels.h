@@ -19,6 +19,26 @@ __device__ __forceinline__ int xcd_contiguous(int b, int G) {
   return x * q + min(x, rem) + i;
 }
 
+// (tile group, token block) of workgroup b in a grid of G x MB.  The items go
+// to the XCDs in contiguous ranges of the order (token half, group, token
+// block): with 8 or more token blocks the first four XCDs serve the first
+// half of the tokens and the other four the second, so each XCD's L2 holds the
+// activations of half the tokens while the weights of a group are read by
+// one XCD per half.  Below 8 token blocks it is plain (group, token block).
+// A bijection on [0, G * MB).
+__device__ __forceinline__ void tile_work(int b, int G, int MB, int& group, int& mblock) {
+  const int L = xcd_contiguous(b, G * MB);
+  const int h0 = MB >= 8 ? (MB + 1) / 2 : MB;  // token blocks of the first half
+  if (L < G * h0) {
+    group = L / h0;
+    mblock = L - group * h0;
+  } else {
+    const int L1 = L - G * h0, h1 = MB - h0;
+    group = L1 / h1;
+    mblock = h0 + (L1 - group * h1);
+  }
+}
+
 hipError_t launch_act_quant(const Cfg& c, const void* X, int x_dtype, int64_t M, int64_t K,
                             uint8_t* Xq, float* s_a, hipStream_t st);
 
@@ -47,7 +67,7 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
 // MX family with outliers, two passes for many tokens: the blob is expanded
 // once into dense merged fp8 fragments in `workspace` (at least
 // mx_dense_workspace_bytes(N, K) bytes, 16-byte aligned), then multiplied.
-constexpr int64_t kDenseMinM = 256;
+constexpr int64_t kDenseMinM = 512;
 size_t mx_dense_workspace_bytes(int64_t N, int64_t K);
 hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, float* Y, void* workspace,

@@ -296,7 +296,7 @@ def test_hip_graph_replays_match_eager_two_pass():
     """The two-pass MX path (workspace allocated before capture) replays like eager."""
     torch = torch_cuda()
     cfg, _ = _cfgs(*MX_CFGS[1])
-    N, K, M = 544, 640, 300
+    N, K, M = 544, 640, 600
     X = torch.from_numpy(synth.make_x(2, M, K)).cuda()
     blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
     Xq, s_a = sdq.quantize_act(X, cfg)

@@ -224,8 +224,8 @@ def test_gemm_workspace_size_and_validation():
     mx, mx_no = sdq.Config.mx_family(), sdq.Config("mx", 0, 8, "e4m3", 2, 8, "e2m1", "e4m3")
     it = sdq.Config.int_family()
     assert sdq.gemm_workspace_size(mx, 2048, 11008, 4096) == 11008 * 4096
-    assert sdq.gemm_workspace_size(mx, 256, 100, 384) == 128 * 384      # N padded to 32
-    assert sdq.gemm_workspace_size(mx, 255, 100, 384) == 0               # one pass below 256 tokens
+    assert sdq.gemm_workspace_size(mx, 512, 100, 384) == 128 * 384      # N padded to 32
+    assert sdq.gemm_workspace_size(mx, 511, 100, 384) == 0               # one pass below 512 tokens
     assert sdq.gemm_workspace_size(mx, 1, 100, 384, sdq.PATH_DENSE) == 128 * 384
     assert sdq.gemm_workspace_size(mx, 4096, 100, 384, sdq.PATH_MFMA) == 0
     assert sdq.gemm_workspace_size(mx_no, 4096, 100, 384) == 0           # no outlier branch
