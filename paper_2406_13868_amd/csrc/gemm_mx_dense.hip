@@ -21,13 +21,17 @@
 // half 0 holds dwords 0-3 and half 1 dwords 4-7 of lane l's fp8 B operand for
 // 64-K step s of the chunk, so that every load of a wave is 1 KB contiguous.
 //
-// Pass 2 tiling: a workgroup of 4 waves (one per SIMD) owns 128 tokens and 8
-// row tiles (256 outputs); each wave owns 2 tiles x 4 sub-tiles of 32 tokens
-// (8 accumulators of 32x32), so every A fragment read from LDS feeds two
-// matrix instructions.  Activations are staged per 128-K chunk in LDS (double
-// buffered, XOR-swizzled); B fragments go from the workspace straight into
-// registers, requested three 64-K steps ahead.
+// Pass 2 tiling: a workgroup of 4 waves owns 128 tokens and 8 row tiles (256
+// outputs); each wave owns 2 tiles x 4 sub-tiles of 32 tokens (8 accumulators
+// of 32x32), so every A fragment read from LDS feeds two matrix instructions.
+// Activations are staged per 128-K chunk in LDS (double buffered,
+// XOR-swizzled); B fragments go from the workspace straight into registers.
+// A grid with at least two workgroups per CU runs two per CU (two waves per
+// SIMD hide each other's waits) with a one-chunk pipeline; a smaller grid runs
+// one per CU and requests its data four chunks ahead instead.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "kernels.h"
 #include "mx_frag.h"
@@ -44,6 +48,7 @@ constexpr int kDThreads = kDWaves * 64;
 constexpr int kDTiles = 2 * kDWaves;  // row tiles per workgroup
 constexpr int kDMS = 4;               // 32-token sub-tiles per wave
 constexpr int kDBM = 32 * kDMS;       // tokens per workgroup
+constexpr unsigned kCUs = 256;        // compute units of an MI355X
 
 // ---- pass 1 ----------------------------------------------------------------
 // One wave per (tile, chunk) unit u = tile * n_chunks + chunk, the order of
@@ -96,8 +101,10 @@ __device__ __forceinline__ bool unmerged(uint32_t sc) {
   return d0 < -5 || d0 > 6 || d1 < -5 || d1 > 6;
 }
 
-template <int NI>
-__global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
+// DEEP: one workgroup per CU (a grid that cannot fill two per CU), loads four
+// chunks ahead; otherwise two workgroups per CU with a one-chunk pipeline.
+template <int NI, bool DEEP>
+__global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(DenseArgs a) {
   // fp8 activations of one 128-K chunk: 128 rows of 128 bytes, 16-byte piece
   // p of row r at piece p ^ lds_swizzle(r)
   __shared__ __align__(16) uint8_t xs[2][kDBM * kChunkK];
@@ -128,8 +135,8 @@ __global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
   const uint32_t xoff = uint32_t(tid >> 3) * uint32_t(a.K) + (tid & 7) * 16;
   const uint32_t xrow32 = 32u * uint32_t(a.K);
   const uint32_t xdst0 = uint32_t((tid >> 3) * kChunkK + (((tid & 7) ^ lds_swizzle(tid >> 3)) << 4));
-  // two register sets: even chunks in X0, odd chunks in X1, each loaded two
-  // chunks before its products and stored to LDS one chunk before them
+  // activation register sets, each loaded four chunks before its products
+  // and stored to LDS one chunk before them
   struct XRegs { i4v r0, r1, r2, r3; };
   auto load_x = [&](int c, XRegs& x) __attribute__((always_inline)) {
     const uint32_t so = uint32_t(c) * kChunkK;
@@ -214,61 +221,117 @@ __global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
       for (int ms = 0; ms < kDMS; ++ms) asm volatile("" : "+a"(acc[j][ms]));
   };
 
-  // ---- pipeline.  Chunk c uses LDS buffer c & 1, B step sets B0, B1 (even
-  //      chunks) or B2, B3 (odd chunks) and scale set S0 or S1; a set is
-  //      refilled for chunk c + 2 right after its products.  Activations of
-  //      chunk c + 1 go from registers to LDS after the products of chunk c,
-  //      and those of chunk c + 3 are requested then.  Loads past the last
-  //      chunk re-read it (never used).
-  BStep B0, B1, B2, B3;
-  Scales S0, S1;
-  XRegs X0, X1;
-  load_x(0, X0);
-  load_x(min(1, last), X1);
-  load_b(0, 0, B0);
-  load_b(0, 1, B1);
-  load_sc(0, S0);
-  load_b(min(1, last), 0, B2);
-  load_b(min(1, last), 1, B3);
-  load_sc(min(1, last), S1);
-  store_x(0, X0);
-  load_x(min(2, last), X0);
-  __syncthreads();
-  // Every request of the prologue complete before the loop: the wait counts
-  // the compiler derives at the loop head then come from the loop's own
-  // order of requests alone, not from the stricter ones of the prologue.
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  for (int c = 0; c + 1 < KC; c += 2) {  // one exit, so the accumulators stay in place
-    mfmas(0, 0, B0, S0);
-    load_b(min(c + 2, last), 0, B0);
-    mfmas(0, 1, B1, S0);
-    load_b(min(c + 2, last), 1, B1);
-    bad |= unmerged(S0.w[0]) || unmerged(S0.w[1]);
-    load_sc(min(c + 2, last), S0);
-    store_x(1, X1);
-    load_x(min(c + 3, last), X1);
-    pin_acc();
+  if constexpr (DEEP) {
+    // ---- pipeline, four chunks deep.  Chunk c uses LDS buffer c & 1, B step
+    //      sets B[2(c & 3)] and B[2(c & 3) + 1], scale set S[c & 3] and, for its
+    //      activations, register set X[c & 3]; each set is refilled for chunk
+    //      c + 4 right after its use.  Activations of chunk c + 1 go from
+    //      registers to LDS after the products of chunk c.  Loads past the last
+    //      chunk re-read it (never used).
+    BStep B[8];
+    Scales S[4];
+    XRegs X[4];
+    load_x(0, X[0]);
+  #pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      load_b(min(i, last), 0, B[2 * i]);
+      load_b(min(i, last), 1, B[2 * i + 1]);
+      load_sc(min(i, last), S[i]);
+      if (i > 0) load_x(min(i, last), X[i]);
+    }
+    store_x(0, X[0]);
+    load_x(min(4, last), X[0]);
     __syncthreads();
-    mfmas(1, 0, B2, S1);
-    load_b(min(c + 3, last), 0, B2);
-    mfmas(1, 1, B3, S1);
-    load_b(min(c + 3, last), 1, B3);
-    bad |= unmerged(S1.w[0]) || unmerged(S1.w[1]);
-    load_sc(min(c + 3, last), S1);
+    // Every request of the prologue complete before the loop: the wait counts
+    // the compiler derives at the loop head then come from the loop's own
+    // order of requests alone, not from the stricter ones of the prologue.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    // chunk c = base + I, I = c & 3 (a compile-time index into the sets)
+    auto chunk = [&](auto I, int c) __attribute__((always_inline)) {
+      constexpr int i = decltype(I)::value, buf = i & 1, nx = (i + 1) & 3;
+      mfmas(buf, 0, B[2 * i], S[i]);
+      load_b(min(c + 4, last), 0, B[2 * i]);
+      mfmas(buf, 1, B[2 * i + 1], S[i]);
+      load_b(min(c + 4, last), 1, B[2 * i + 1]);
+      bad |= unmerged(S[i].w[0]) || unmerged(S[i].w[1]);
+      load_sc(min(c + 4, last), S[i]);
+      store_x(buf ^ 1, X[nx]);  // chunk c + 1
+      load_x(min(c + 5, last), X[nx]);
+      pin_acc();
+      __syncthreads();
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    int c = 0;
+    for (; c + 3 < KC; c += 4) {  // one exit, so the accumulators stay in place
+      chunk(I0{}, c);
+      chunk(I1{}, c + 1);
+      chunk(I2{}, c + 2);
+      chunk(I3{}, c + 3);
+    }
+    const int rem = KC - c;  // 0..3 chunks left, wave-uniform
+    if (rem > 0) chunk(I0{}, c);
+    if (rem > 1) chunk(I1{}, c + 1);
+    if (rem > 2) chunk(I2{}, c + 2);
+  } else {
+    // ---- pipeline for two workgroups per CU (two waves per SIMD hide each
+    //      other's waits): one B step set per step and one activation set,
+    //      each refilled for the next chunk right after its use
+    BStep BA, BB;
+    Scales S0;
+    XRegs X0;
+    load_b(0, 0, BA);
+    load_b(0, 1, BB);
+    load_sc(0, S0);
+    load_x(0, X0);
     store_x(0, X0);
-    load_x(min(c + 4, last), X0);
-    pin_acc();
+    load_x(min(1, last), X0);
     __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as above
+    for (int c = 0; c < KC; ++c) {  // one exit, so the accumulators stay in place
+      const int buf = c & 1;
+      mfmas(buf, 0, BA, S0);
+      load_b(min(c + 1, last), 0, BA);
+      mfmas(buf, 1, BB, S0);
+      load_b(min(c + 1, last), 1, BB);
+      bad |= unmerged(S0.w[0]) || unmerged(S0.w[1]);
+      load_sc(min(c + 1, last), S0);
+      store_x(buf ^ 1, X0);  // chunk c + 1
+      load_x(min(c + 2, last), X0);
+      pin_acc();
+      __syncthreads();
+    }
   }
-  if (KC & 1) {  // the last chunk of an odd count, in LDS buffer 0
-    mfmas(0, 0, B0, S0);
-    mfmas(0, 1, B1, S0);
-    bad |= unmerged(S0.w[0]) || unmerged(S0.w[1]);
+
+  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, kDBM);
+  // ---- outputs
+  {
+    const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (!tok[j]) continue;
+      const int n = tile[j] * kTileN + col;
+      if (n >= a.N) continue;
+#pragma unroll
+      for (int ms = 0; ms < kDMS; ++ms)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * acc[j][ms][e]);
+    }
   }
 
   // ---- inliers of blocks that did not merge (rare; wave-uniform branches):
-  //      fp8 x fp4 products, A read from global memory
+  //      their fp8 x fp4 products accumulate from zero, A read from global
+  //      memory, and are added to the stored outputs.  (Kept apart from the
+  //      main accumulators, which would otherwise need a second copy.)
   if (__any(bad)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int ms = 0; ms < kDMS; ++ms)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const __amdgpu_buffer_rsrc_t wr =
@@ -295,19 +358,23 @@ __global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
         }
       }
     }
-  }
-
-  const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, kDBM);
+    // this wave's output stores complete (in L2) before they are read back
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    if (!tok[j]) continue;
-    const int n = tile[j] * kTileN + col;
-    if (n >= a.N) continue;
+    for (int j = 0; j < 2; ++j) {
+      if (!tok[j]) continue;
+      const int n = tile[j] * kTileN + col;
+      if (n >= a.N) continue;
 #pragma unroll
-    for (int ms = 0; ms < kDMS; ++ms)
+      for (int ms = 0; ms < kDMS; ++ms)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * acc[j][ms][e]);
+        for (int e = 0; e < 16; ++e) {
+          const uint32_t off = (uint32_t(ms * 32 + tile_row(e, h)) * uint32_t(a.N) + uint32_t(n)) * 4u;
+          const float y = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(yr, off, 0, 1));  // glc: from L2
+          store_out(yr, a.N, n, ms, e, h, y + rs.v[ms][e] * acc[j][ms][e]);
+        }
+    }
   }
 }
 
@@ -320,8 +387,11 @@ hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8
   DenseArgs a{Xq, s_a, blob, frag, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
               L.scales_off, int((M + kDBM - 1) / kDBM)};
   const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
-  hipLaunchKernelGGL((mx_dense_kernel<NI>), dim3(unsigned(groups * a.m_blocks)), dim3(kDThreads), 0,
-                     st, a);
+  const unsigned wgs = unsigned(groups * a.m_blocks);
+  if (wgs < 2 * kCUs)
+    hipLaunchKernelGGL((mx_dense_kernel<NI, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((mx_dense_kernel<NI, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
   return hipGetLastError();
 }
 

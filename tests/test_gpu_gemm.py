@@ -85,7 +85,7 @@ def test_gemm_matches_oracle(c, M, N, K):
 
 @pytest.mark.parametrize("c", [MX_CFGS[0], MX_CFGS[1], MX_CFGS[3]], ids=_ids)
 @pytest.mark.parametrize("M,N,K", [(512, 256, 256), (600, 100, 384), (777, 544, 128),
-                                   (1030, 288, 640)])
+                                   (1030, 288, 640), (4100, 4128, 128)])
 def test_mx_many_rows(c, M, N, K):
     """Row counts of large prefill batches: several token blocks, a ragged last
     block, column groups of 32-wide tiles with a ragged last group, and odd and
@@ -101,11 +101,13 @@ def test_mx_many_rows(c, M, N, K):
 
 
 @pytest.mark.parametrize("c", [MX_CFGS[0], MX_CFGS[1], MX_CFGS[2], MX_CFGS[3]], ids=_ids)
-@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (40, 100, 384), (256, 288, 640), (300, 544, 128)])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (40, 100, 384), (256, 288, 640), (300, 544, 128),
+                                   (4096, 4096, 256)])
 def test_dense_equals_one_pass(c, M, N, K):
     """Where every block merges its inliers the two-pass path runs the same
     matrix instructions per accumulator in the same order as the one-pass
-    kernel: the outputs agree bit for bit."""
+    kernel: the outputs agree bit for bit (one workgroup per CU below 512
+    workgroups, two from there)."""
     cfg, cfg_o = _cfgs(*c)
     X = synth.make_x(3, M, K)
     W = synth.make_w(3, 2, N, K)
