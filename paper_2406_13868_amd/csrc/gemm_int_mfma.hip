@@ -244,33 +244,36 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   const int tile = blockIdx.x;
   const int KC = a.n_chunks;
 
-  // groups 8h + i of row col: word ((h'*32 + col)*2 + h)*4 + q with i = 2q + h'
-  const uint8_t* wbase = a.blob + size_t(tile) * KC * kWordBytesPerTC + size_t(col * 2 + h) * 16;
-  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile) * KC * kIntScaleBytesPerTC + col * 16;
-  const uint8_t* xrow[MS];
-  bool mok[MS];
-#pragma unroll
-  for (int ms = 0; ms < MS; ++ms) {
-    const int m = m0 + ms * 32 + col;
-    mok[ms] = m < a.M;
-    xrow[ms] = a.Xq + size_t(mok[ms] ? m : 0) * a.K + h * 64;
-  }
+  // groups 8h + i of row col: word ((h'*32 + col)*2 + h)*4 + q with i = 2q + h'.
+  // Buffer resources over the tile's words and scales and over the block's
+  // activation rows (rows past M read 0): wave-uniform bases, 32-bit offsets.
+  const __amdgpu_buffer_rsrc_t wr =
+      buffer_rsrc(a.blob + size_t(tile) * KC * kWordBytesPerTC, uint32_t(KC) * kWordBytesPerTC);
+  const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(
+      a.blob + a.scales_off + size_t(tile) * KC * kIntScaleBytesPerTC, uint32_t(KC) * kIntScaleBytesPerTC);
+  const __amdgpu_buffer_rsrc_t xr =
+      buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, BM)) * uint32_t(a.K));
+  const uint32_t woff = uint32_t(col * 2 + h) * 16, soff = uint32_t(col) * 16;
+  const uint32_t xoff = uint32_t(col) * uint32_t(a.K) + uint32_t(h) * 64;
 
   struct Stage {
     uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's eight fp16 block scales
     uint4 x[MS][4];     // 64 activation bytes per sub-tile
   };
-  auto load = [&](int c, Stage& st) {
-    const uint8_t* wp = wbase + size_t(c) * kWordBytesPerTC;
-    st.w0 = *reinterpret_cast<const uint4*>(wp);
-    st.w1 = *reinterpret_cast<const uint4*>(wp + 1024);
-    st.sc = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kIntScaleBytesPerTC);
+  auto ld16 = [](__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t so) __attribute__((always_inline)) {
+    typedef unsigned int u4_ __attribute__((ext_vector_type(4)));
+    const u4_ q = __builtin_bit_cast(u4_, __builtin_amdgcn_raw_buffer_load_b128(r, v, so, 0));
+    return make_uint4(q[0], q[1], q[2], q[3]);
+  };
+  auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
+    st.w0 = ld16(wr, woff, uint32_t(c) * kWordBytesPerTC);
+    st.w1 = ld16(wr, woff + 1024, uint32_t(c) * kWordBytesPerTC);
+    st.sc = ld16(sr, soff, uint32_t(c) * kIntScaleBytesPerTC);
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        st.x[ms][u] = mok[ms] ? *reinterpret_cast<const uint4*>(xrow[ms] + size_t(c) * kChunkK + u * 16)
-                              : make_uint4(0, 0, 0, 0);
+        st.x[ms][u] = ld16(xr, xoff + uint32_t(ms * 32) * uint32_t(a.K) + u * 16, uint32_t(c) * kChunkK);
   };
 
   f16v acc[MS], acco[MS];
@@ -311,26 +314,22 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
     }
   };
 
-  // two stages in flight: chunk c is computed while c + NW and c + 2*NW land
+  // two stages in flight: wave w takes chunks w, w + NW, w + 2 NW, ...; stage
+  // s0 holds its even-numbered chunks and s1 its odd ones, each refilled
+  // right after its products (a copy would wait for the load).  Loads past
+  // the last chunk re-read it (in bounds, never used), so none is conditional.
+  const int last = KC - 1;
   Stage s0, s1;
+  load(min(wave, last), s0);
+  load(min(wave + NW, last), s1);
   int c = wave;
-  if (c < KC) load(c, s0);
-  if (c + NW < KC) load(c + NW, s1);
-  while (c < KC) {
-    {
-      const Stage cur = s0;
-      if (c + 2 * NW < KC) load(c + 2 * NW, s0);
-      compute(cur);
-    }
-    c += NW;
-    if (c >= KC) break;
-    {
-      const Stage cur = s1;
-      if (c + 2 * NW < KC) load(c + 2 * NW, s1);
-      compute(cur);
-    }
-    c += NW;
+  for (; c + NW < KC; c += 2 * NW) {  // one exit, so the accumulators stay in place
+    compute(s0);
+    load(min(c + 2 * NW, last), s0);
+    compute(s1);
+    load(min(c + 3 * NW, last), s1);
   }
+  if (c < KC) compute(s0);  // a last chunk of odd rank
 
   // ---- tree over the waves: in round r, wave w + 2^r hands its partial to w
 #pragma unroll
