@@ -33,6 +33,7 @@ typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
+constexpr int64_t kCUs = 256;                      // compute units of an MI355X
 constexpr int kRowPad = 8;                        // f16 elements of padding per LDS row
 constexpr int kLdsRow = kChunkK + kRowPad;        // 136 f16 = 272 bytes
 constexpr uint32_t kOutPosMagic = (1u << 21) | (1u << 14) | (1u << 7);
@@ -408,7 +409,10 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   MfmaArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
              L.scales_off, L.rows_off};
   if (M <= 32) return launch_ms<1>(c, a, st);
-  if (M <= 64) return launch_ms<2>(c, a, st);
+  // 33..64 tokens: one 64-token block expands every weight once; when that
+  // leaves fewer workgroups than compute units, two 32-token blocks fill the
+  // GPU instead (each weight is then expanded twice)
+  if (M <= 64) return L.n_tiles < kCUs ? launch_ms<1>(c, a, st) : launch_ms<2>(c, a, st);
   return launch_ms<4>(c, a, st);
 }
 
