@@ -21,6 +21,8 @@
 // l%32 and the 8-group 2*kb + l/32 of every 16-K block kb.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 #include "tile_out.h"
 
@@ -109,6 +111,14 @@ __device__ __forceinline__ h8 outlier_f16(uint32_t w) {
 #pragma unroll
   for (int v = 0; v < 4; ++v) out[v] = d == uint32_t(v) ? val : 0u;
   return __builtin_bit_cast(h8, out);
+}
+
+// Dense int8 outlier bytes of one group word (position p at byte p of lo:hi).
+__device__ __forceinline__ void outlier_i8(uint32_t w, uint32_t& lo, uint32_t& hi) {
+  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
+  const uint32_t v = (w >> 24) << ((pos & 3u) << 3);
+  lo = pos < 4u ? v : 0u;
+  hi = pos < 4u ? 0u : v;
 }
 
 template <int MS, int NI, bool OUT_INT8>
@@ -277,11 +287,18 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
         st.x[ms][u] = ld16(xr, xoff + uint32_t(ms * 32) * uint32_t(a.K) + u * 16, uint32_t(c) * kChunkK);
   };
 
-  f16v acc[MS], acco[MS];
+  // the outlier branch: int8 outliers accumulate exactly in int32 through
+  // the int8 matrix instruction (activation bytes as they are); e4m3
+  // outliers through the f16 one
+  typedef int i4v_ __attribute__((ext_vector_type(4)));
+  typedef int i16v_ __attribute__((ext_vector_type(16)));
+  using OAcc = std::conditional_t<OUT_INT8, i16v_, f16v>;
+  f16v acc[MS];
+  OAcc acco[MS];
 #pragma unroll
   for (int s = 0; s < MS; ++s)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) { acc[s][e] = 0.f; acco[s][e] = 0.f; }
+    for (int e = 0; e < 16; ++e) { acc[s][e] = 0.f; acco[s][e] = 0; }
 
   auto compute = [&](const Stage& st) {
     const uint32_t wv[2][4] = {{st.w0.x, st.w0.y, st.w0.z, st.w0.w}, {st.w1.x, st.w1.y, st.w1.z, st.w1.w}};
@@ -295,7 +312,6 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
       const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
       h8 bh, bl;
       scaled_hi_lo(inlier_f16<NI>(w), s, bh, bl);
-      const h8 bo = outlier_f16<OUT_INT8>(w);
       h8 av[MS];
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
@@ -308,8 +324,27 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
       }
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bh, acc[ms], 0, 0, 0);
+      if constexpr (OUT_INT8) {
+        // steps i, i + 1 (i even) in one int8 instruction over 32 K: a lane's
+        // 16 activation bytes of the two groups are the uint4 st.x[ms][i/2]
+        // as loaded, and its outlier bytes follow the same order
+        if ((i & 1) == 0) {
+          uint32_t o0, o1, o2, o3;
+          outlier_i8(w, o0, o1);
+          outlier_i8(wv[1][i >> 1], o2, o3);
+          const i4v_ bo = {int(o0), int(o1), int(o2), int(o3)};
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
+          for (int ms = 0; ms < MS; ++ms) {
+            const uint4 xv = st.x[ms][i >> 1];
+            const i4v_ ax = {int(xv.x), int(xv.y), int(xv.z), int(xv.w)};
+            acco[ms] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ax, bo, acco[ms], 0, 0, 0);
+          }
+        }
+      } else {
+        const h8 bo = outlier_f16<false>(w);
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
+      }
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
     }
@@ -333,26 +368,35 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   if (c < KC) compute(s0);  // a last chunk of odd rank
 
   // ---- tree over the waves: in round r, wave w + 2^r hands its partial to w
+  // (the int32 outlier partials travel through the same buffer as bits)
+  // (elements are copied to scalars first: a bit cast of a vector element
+  // in place reads element 0)
+  auto tree = [&](auto& v) __attribute__((always_inline)) {
+#pragma unroll
+    for (int stride = NW / 2; stride >= 1; stride >>= 1) {
+      const bool sender = wave >= stride && wave < 2 * stride;
+      if (sender) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const auto x = v[e];
+          red[wave - stride][e][lane] = __builtin_bit_cast(float, x);
+        }
+      }
+      __syncthreads();
+      if (wave < stride) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float r = red[wave][e][lane];
+          v[e] += __builtin_bit_cast(decltype(v[e] + 0), r);
+        }
+      }
+      __syncthreads();
+    }
+  };
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms) {
-#pragma unroll
-    for (int which = 0; which < 2; ++which) {
-      f16v& v = which ? acco[ms] : acc[ms];
-#pragma unroll
-      for (int stride = NW / 2; stride >= 1; stride >>= 1) {
-        const bool sender = wave >= stride && wave < 2 * stride;
-        if (sender) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) red[wave - stride][e][lane] = v[e];
-        }
-        __syncthreads();
-        if (wave < stride) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) v[e] += red[wave][e][lane];
-        }
-        __syncthreads();
-      }
-    }
+    tree(acc[ms]);
+    tree(acco[ms]);
   }
   if (wave > 0) return;
   const int n = tile * kTileN + col;
@@ -363,7 +407,7 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, acco[ms][e], acc[ms][e]));
+    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, float(acco[ms][e]), acc[ms][e]));
 }
 
 template <int MS, int NI, int NW>
