@@ -59,6 +59,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--context", action="store_true",
                    help="also time cache-resident and eager GEMM launches (context figures)")
+    p.add_argument("--no-vendor", action="store_true",
+                   help="skip the vendor dense-GEMM context figures (torch.matmul bf16, torch._scaled_mm fp8)")
     p.add_argument("--counters", type=int, default=0, metavar="L",
                    help="counter-collection mode: L eager GEMM launches over the rotated "
                         "weight copies, no graphs, no JSON line")
@@ -260,6 +262,8 @@ def main():
     # kernels per GEMM call: the two-pass path's time is both passes together
     roof["kernels_per_call"] = 2 if sdq.PATH_DENSE in paths else 1
 
+    vendor = None if a.no_vendor else vendor_context(torch, Ls, M, a.rotate_mb, max(a.steps, 20))
+
     # ---------------------------------------------------------------- CPU oracle
     cpu = None
     if not a.no_cpu_baseline:
@@ -288,6 +292,7 @@ def main():
         "gemm_us_eager": gemm_b2b_us,
         "gemm_us_cache_resident": gemm_hot_us,
         "gemm_dense_equiv_tflops": round(flops / (gemm_us * 1e-6) / 1e12, 3),
+        "vendor_dense_context": vendor,
         "logical_bytes": int(logical),
         "physical_bytes": int(phys),
         "algorithmic_bytes_per_launch": int(alg_bytes),
@@ -297,6 +302,66 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(line))
+
+
+def vendor_context(torch, Ls, M, rotate_mb, n):
+    """Dense GEMMs of the same shapes through the vendor library, timed like the
+    SDQ GEMM (HIP graph of n launches over rotated weight copies, HIP events):
+    a linear layer in bf16 (weight [N, K]), torch._scaled_mm in fp8 e4m3 with per-tensor scales
+    (fp32 output), and with e8m0 scales per 32 K (MXFP8).  Context only: these
+    read 16 or 8 bits per weight where the decomposed format reads 3.6-5."""
+    dev = torch.device("cuda:0")
+    out = {}
+    for L in Ls:
+        key = f"{M}x{L.N}x{L.K}"
+        if key in out:
+            continue
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        a16 = torch.randn(M, L.K, device=dev, generator=g).to(torch.bfloat16)
+        R = max(2, math.ceil(rotate_mb * 1e6 / (2 * L.N * L.K)))
+        w16 = [torch.randn(L.N, L.K, device=dev, generator=g).to(torch.bfloat16) for _ in range(R)]
+        a8 = a16.to(torch.float8_e4m3fn)
+        w8 = [w.to(torch.float8_e4m3fn) for w in w16[: max(2, (R + 1) // 2)]]
+        one = torch.ones((), device=dev)
+        sa = torch.full((M, L.K // 32), 127, device=dev, dtype=torch.uint8).view(torch.float8_e8m0fnu)
+        sb = torch.full((L.N, L.K // 32), 127, device=dev, dtype=torch.uint8).view(torch.float8_e8m0fnu)
+        fl = 2.0 * M * L.N * L.K
+        cases = {
+            "bf16_linear": lambda i: torch.nn.functional.linear(a16, w16[i % len(w16)]),
+            "fp8_scaled_mm_fp32_out": lambda i: torch._scaled_mm(a8, w8[i % len(w8)].t(), scale_a=one, scale_b=one,
+                                                                 out_dtype=torch.float32),
+            "mxfp8_scaled_mm_bf16_out": lambda i: torch._scaled_mm(a8, w8[i % len(w8)].t(), scale_a=sa, scale_b=sb,
+                                                                   out_dtype=torch.bfloat16),
+        }
+        res = {}
+        for name, f in cases.items():
+            try:
+                f(0)
+                torch.cuda.synchronize()
+                gr = torch.cuda.CUDAGraph()
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    f(1)
+                torch.cuda.current_stream().wait_stream(side)
+                with torch.cuda.graph(gr):
+                    for i in range(n):
+                        f(i)
+                gr.replay()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                gr.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                us = e0.elapsed_time(e1) * 1e3 / n
+                res[name] = {"us": round(us, 3), "tflops": round(fl / (us * 1e-6) / 1e12, 1)}
+            except Exception as e:  # a shape or dtype the library does not take
+                res[name] = {"error": repr(e)[:160]}
+        out[key] = res
+        del w16, w8
+    return out
 
 
 def cpu_baseline(Ws, Xs, fmt, M, seconds):
