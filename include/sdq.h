@@ -64,6 +64,16 @@ typedef enum {
 enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1 };
 enum { SDQ_FMT_INT8 = 1, SDQ_FMT_INT4 = 2, SDQ_FMT_E4M3 = 3, SDQ_FMT_E2M1 = 4 };
 enum { SDQ_METRIC_MAGNITUDE = 0, SDQ_METRIC_PRODUCT = 1 };
+/* Decomposition metric (which kept weights become the outliers) and the
+ * order it is taken in; see sdq_config. */
+enum {
+  SDQ_DECOMP_SAME = 0,         /* the significance metric                      */
+  SDQ_DECOMP_MAGNITUDE = 1,    /* |W|                                          */
+  SDQ_DECOMP_PRODUCT = 2,      /* |W| * act_norm[k]                            */
+  SDQ_DECOMP_ERROR = 3,        /* |W - Q_i(W)|, Q_i the inlier quantizer       */
+  SDQ_DECOMP_OUTPUT_ERROR = 4  /* |W - Q_i(W)| * act_norm[k]                   */
+};
+enum { SDQ_ORDER_LARGE = 0, SDQ_ORDER_SMALL = 1 };
 enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
 /* sdq_gemm_ex / sdq_gemm_ws kernel choice. */
 enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3 };
@@ -76,15 +86,25 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  *   n_i:m_i inlier sparsity, n_i in {1, 2, 3}, m_i = 8
  *   fmt_i   INT: SDQ_FMT_INT4;  MX: SDQ_FMT_E2M1
  *   fmt_a   INT: SDQ_FMT_INT8;  MX: SDQ_FMT_E4M3
- *   metric  significance used to pick outliers and inliers (Section 5,
- *           Stages 1-2): |W| (SDQ_METRIC_MAGNITUDE) or |W| * act_norm[k]
- *           (SDQ_METRIC_PRODUCT, Wanda's weight-activation product). */
+ *   metric  significance used to sparsify (Section 5, Stage 1): |W|
+ *           (SDQ_METRIC_MAGNITUDE) or |W| * act_norm[k] (SDQ_METRIC_PRODUCT,
+ *           Wanda's weight-activation product)
+ *   decomp  metric that picks the outliers among the kept weights (Section
+ *           5, Stage 2; the variants of Section 7's decomposition study):
+ *           SDQ_DECOMP_SAME (the significance metric), _MAGNITUDE, _PRODUCT,
+ *           _ERROR (the error the inlier quantizer would make on the weight)
+ *           or _OUTPUT_ERROR (that error times act_norm[k])
+ *   order   SDQ_ORDER_LARGE: the outliers are the kept weights with the
+ *           largest decomp metric ("Large"); SDQ_ORDER_SMALL: the smallest
+ * decomp = SAME with order = LARGE (both zero) is the default; any other
+ * choice needs n_o = 1. */
 typedef struct {
   int32_t family;
   int32_t n_o, m_o, fmt_o;
   int32_t n_i, m_i, fmt_i;
   int32_t fmt_a;
   int32_t metric;
+  int32_t decomp, order;
 } sdq_config;
 
 /* Static description of an error code (never NULL). */
@@ -107,13 +127,26 @@ sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t
 /* Offline pack (Section 5, Stages 1-3), on the host.
  *   W         host, [N, K] fp32 row-major, finite values
  *   act_norm  host, [K] fp32 (per-input-channel activation norm), required
- *             for SDQ_METRIC_PRODUCT and ignored otherwise (may be NULL)
+ *             for SDQ_METRIC_PRODUCT, SDQ_DECOMP_PRODUCT and
+ *             SDQ_DECOMP_OUTPUT_ERROR and ignored otherwise (may be NULL)
  *   packed    host, caller-owned, at least sdq_pack_size() bytes; copy it to
  *             the device unchanged before calling sdq_gemm
  *   n_threads host threads to use (<= 0: one per hardware thread)
- * Selection: in every m_o-group the n_o most significant positions are the
- * outliers; in every m_i-group the n_i most significant remaining positions
- * are the inliers; the rest are pruned.  Ties go to the lower k.
+ * Selection with the default decomposition (decomp SAME, order LARGE): in
+ * every m_o-group the n_o most significant positions are the outliers; in
+ * every m_i-group the n_i most significant remaining positions are the
+ * inliers; the rest are pruned.  Ties go to the lower k.
+ * Any other decomposition follows the paper's stage order:
+ *   1. every 8-group keeps its n_o + n_i most significant positions;
+ *   2. the error metrics quantize the kept positions as inliers (the inlier
+ *      rule below, scales over the kept positions of each block) and take
+ *      D = |W - deq| in fp32 (times act_norm[k] for OUTPUT_ERROR);
+ *   3. in every m_o-group the n_o kept positions first by (-D, k) (LARGE) or
+ *      (D, k) (SMALL) are the outliers;
+ *   4. in every 8-group the n_i most significant kept positions that are not
+ *      outliers are the inliers (with m_o = 16 the 8-group without the
+ *      outlier drops its least significant kept position).
+ * With decomp SAME and order LARGE the two procedures select the same sets.
  * Quantization (IEEE fp32 arithmetic, round-to-nearest-even):
  *   INT outliers: s_o[n] = amax_row / qmax (qmax 127 or 448), q = enc(W / s_o)
  *   INT inliers:  s = fp16(amax_block16 / 7), q = clamp(rne(W / s), -7, 7)
@@ -121,7 +154,8 @@ sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t
  *                 e2m1), q = enc(W / 2^E) saturating
  *   an all-zero block gets a zero scale (E = -127) and zero codes.
  * Returns SDQ_ERR_VALUE if W holds a non-finite value or an inlier scale
- * overflows fp16. */
+ * overflows fp16 (also the provisional scales of the error metrics).
+ * Scratch: each worker thread holds 2K floats and K/4 bytes. */
 sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
                     const float* act_norm, void* packed, size_t bytes, int n_threads);
 

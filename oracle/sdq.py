@@ -15,6 +15,11 @@ Paper passages followed (Jeong et al., SDQ):
   the inliers, themselves n_i:m structured (Section 4 and Section 5,
   "Stage 2").  Selecting the top n_o first and then the next n_i equals
   sparsifying to (n_o+n_i):m first and then extracting n_o:m outliers.
+* The decomposition metric may differ from the significance metric and be
+  taken in either order: magnitude, weight-activation product, or the error
+  the inlier quantizer makes on the weight (alone or times the activation
+  norm), "Large" or "Small" (Section 5, "Stage 2", and Section 7's
+  decomposition study).  These run the two stages in the paper's order.
 * Stage 3 quantizes each branch with per-vector (VS-Quant) scale factors,
   outliers at a higher precision than inliers; activations are quantized too
   (Section 3.3 and Section 5, "Stage 3").
@@ -54,7 +59,15 @@ class Config:
     m_i: int
     fmt_i: str         # "int4" | "e2m1"
     fmt_a: str         # "int8" | "e4m3"
-    metric: str = "magnitude"  # "magnitude" | "product"
+    metric: str = "magnitude"  # significance (Stage 1): "magnitude" | "product"
+    decomp: str = "same"       # outlier metric (Stage 2): "same" | "magnitude" | "product"
+    #                            | "error" | "output_error"
+    order: str = "large"       # outliers have the largest ("large") or smallest ("small") metric
+
+    @property
+    def staged(self) -> bool:
+        """Whether Stage 2 uses its own metric or order (not the default)."""
+        return self.decomp != "same" or self.order != "large"
 
     @property
     def qv_i(self) -> int:
@@ -86,12 +99,18 @@ class Config:
         m_o = self.m_o if self.n_o else self.m_i
         for d in (self.m_i, self.qv_i, m_o, 32 if self.family == "mx" else 1):
             assert K % d == 0, f"K={K} not divisible by {d}"
+        assert self.decomp in ("same", "magnitude", "product", "error", "output_error")
+        assert self.order in ("large", "small")
+        if self.staged:
+            # outliers are chosen among the positions kept by sparsification
+            assert self.n_o > 0 and self.m_o % self.m_i == 0
+            assert self.n_o * (self.m_o // self.m_i) <= self.m_o and self.n_o + self.n_i <= self.m_i
 
 
-def config_from(fmt, metric: str = "magnitude") -> Config:
+def config_from(fmt, metric: str = "magnitude", decomp: str = "same", order: str = "large") -> Config:
     """Build an oracle Config from a plain format description (duck-typed)."""
     return Config(fmt.family, fmt.n_o, fmt.m_o, fmt.fmt_o, fmt.n_i, fmt.m_i,
-                  fmt.fmt_i, fmt.fmt_a, metric)
+                  fmt.fmt_i, fmt.fmt_a, metric, decomp, order)
 
 
 # ---------------------------------------------------------------------------
@@ -128,10 +147,79 @@ def top_n_per_group(S: np.ndarray, allowed: np.ndarray, m: int, n: int):
     return mask.reshape(N, K), np.sort(chosen, axis=-1).astype(np.int64)
 
 
+def top_n_by_key(key: np.ndarray, allowed: np.ndarray, m: int, n: int):
+    """In every m-group pick the first n allowed positions by (key, k), key
+    ascending.  Returns (mask [N, K] bool, positions [N, K/m, n] ascending)."""
+    N, K = key.shape
+    G = K // m
+    k = np.where(allowed.reshape(N, G, m), key.reshape(N, G, m).astype(np.float64), np.inf)
+    order = np.argsort(k, axis=-1, kind="stable")
+    chosen = order[..., :n]
+    assert np.take_along_axis(allowed.reshape(N, G, m), chosen, axis=-1).all(), \
+        "fewer candidates than slots in a group"
+    mask = np.zeros((N, G, m), dtype=bool)
+    np.put_along_axis(mask, chosen, True, axis=-1)
+    return mask.reshape(N, K), np.sort(chosen, axis=-1).astype(np.int64)
+
+
+def inlier_error(W: np.ndarray, keep: np.ndarray, cfg: Config) -> np.ndarray:
+    """|W - deq Q_i(W)| on the kept positions (0 elsewhere), fp32: the error the
+    inlier quantizer (scales over the kept positions of each block) makes on
+    every kept weight -- the quantization error of Section 7's error-based
+    decomposition metric."""
+    W = np.asarray(W, dtype=np.float32)
+    q, scale = quantize_inliers(W, keep, cfg)
+    if cfg.family == "int":
+        deq = q.astype(np.float32) * np.repeat(scale.astype(np.float32), cfg.qv_i, axis=1)
+    else:
+        deq = (F.e2m1_decode(q) * np.repeat(F.e8m0_value(scale), cfg.qv_i, axis=1)).astype(np.float32)
+    return np.where(keep, np.abs(W - deq), np.float32(0)).astype(np.float32)
+
+
+def decomposition_metric(W: np.ndarray, keep: np.ndarray, cfg: Config,
+                         act_norm: Optional[np.ndarray]) -> np.ndarray:
+    """Stage 2's metric D (fp32): the significance itself, |W|, |W| * c, the
+    inlier quantization error, or that error times c (c = act_norm)."""
+    W = np.asarray(W, dtype=np.float32)
+    if cfg.decomp == "same":
+        return significance(W, act_norm if cfg.metric == "product" else None)
+    if cfg.decomp == "magnitude":
+        return np.abs(W)
+    c = None if act_norm is None else np.asarray(act_norm, dtype=np.float32)[None, :]
+    if cfg.decomp == "product":
+        return (np.abs(W) * c).astype(np.float32)
+    e = inlier_error(W, keep, cfg)
+    return e if cfg.decomp == "error" else (e * c).astype(np.float32)
+
+
+def decompose_staged(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = None):
+    """Stages 1 and 2 in the paper's order (Section 5): sparsify, then extract
+    the outliers from what was kept.  Returns (mask_o, pos_o, mask_i, pos_i)."""
+    N, K = W.shape
+    assert cfg.n_o > 0 and cfg.m_o % cfg.m_i == 0
+    S = significance(W, act_norm if cfg.metric == "product" else None)
+    # Stage 1: sparsify every m_i-group to its n_o + n_i most significant positions
+    keep, _ = top_n_per_group(S, np.ones((N, K), dtype=bool), cfg.m_i, cfg.n_o + cfg.n_i)
+    # Stage 2: n_o outliers per m_o-group among the kept, by D largest or smallest first
+    D = decomposition_metric(W, keep, cfg, act_norm).astype(np.float64)
+    mask_o, pos_o = top_n_by_key(-D if cfg.order == "large" else D, keep, cfg.m_o, cfg.n_o)
+    # the kept positions that are not outliers are the inliers; an m_i-group
+    # left with more than n_i of them keeps its n_i most significant
+    mask_i, pos_i = top_n_per_group(S, keep & ~mask_o, cfg.m_i, cfg.n_i)
+    return mask_o, pos_o, mask_i, pos_i
+
+
 def decompose(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = None):
-    """Outlier and inlier supports.  Returns (mask_o, pos_o, mask_i, pos_i)."""
+    """Outlier and inlier supports.  Returns (mask_o, pos_o, mask_i, pos_i).
+
+    Default decomposition (the significance metric, largest first): the n_o
+    most significant positions of every m_o-group are the outliers and the
+    n_i most significant remaining positions of every m_i-group the inliers.
+    Any other decomposition metric or order runs ``decompose_staged``."""
     N, K = W.shape
     cfg.check(K)
+    if cfg.staged:
+        return decompose_staged(W, cfg, act_norm)
     S = significance(W, act_norm if cfg.metric == "product" else None)
     everything = np.ones((N, K), dtype=bool)
     if cfg.n_o:

@@ -43,7 +43,9 @@ class Config:
     m_i: int = 8
     fmt_i: str = "int4"      # "int4" | "e2m1"
     fmt_a: str = "int8"      # "int8" | "e4m3"
-    metric: str = "magnitude"  # "magnitude" | "product"
+    metric: str = "magnitude"  # significance: "magnitude" | "product"
+    decomp: str = "same"       # outlier metric: "same" | "magnitude" | "product" | "error" | "output_error"
+    order: str = "large"       # outliers by the largest ("large") or smallest ("small") decomp metric
 
     @staticmethod
     def int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, metric="magnitude") -> "Config":
@@ -67,7 +69,8 @@ class Config:
         return _lib.sdq_config(FAMILY_MX if self.mx else FAMILY_INT, self.n_o, self.m_o,
                                _FMT[self.fmt_o], self.n_i, self.m_i, _FMT[self.fmt_i],
                                _FMT[self.fmt_a],
-                               METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE)
+                               METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE,
+                               _lib.DECOMP[self.decomp], _lib.ORDER[self.order])
 
 
 def _p(a) -> C.c_void_p:

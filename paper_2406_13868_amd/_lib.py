@@ -16,6 +16,8 @@ STATUS = {
 FAMILY_INT, FAMILY_MX = 0, 1
 FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
 METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
+DECOMP = {"same": 0, "magnitude": 1, "product": 2, "error": 3, "output_error": 4}
+ORDER = {"large": 0, "small": 1}
 DTYPE_F32, DTYPE_BF16 = 0, 1
 PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE = 0, 1, 2, 3
 
@@ -30,7 +32,8 @@ EXPORTS = (
 class sdq_config(C.Structure):
     _fields_ = [("family", C.c_int32), ("n_o", C.c_int32), ("m_o", C.c_int32),
                 ("fmt_o", C.c_int32), ("n_i", C.c_int32), ("m_i", C.c_int32),
-                ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32)]
+                ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32),
+                ("decomp", C.c_int32), ("order", C.c_int32)]
 
 
 class SDQError(RuntimeError):

@@ -5,7 +5,11 @@
 //              every 8-group the n_i most significant remaining positions
 //              become the inliers; everything else is pruned.  Significance
 //              is |w| or |w| * act_norm[k] (Wanda's product metric); ties go
-//              to the lower k.
+//              to the lower k.  With a separate decomposition metric (the
+//              variants of Section 7's decomposition study) the stages run in
+//              the paper's order instead: sparsify every 8-group to
+//              n_o + n_i kept positions, then extract the outliers among the
+//              kept ones by that metric, largest or smallest first.
 //   Stage 3    Per-vector quantization of each branch (VS-Quant style), with
 //              the formats of the configuration's family.
 //
@@ -137,6 +141,113 @@ uint32_t top_n(const float* S, uint32_t allowed, int m, int n) {
   return mask;
 }
 
+// ---------------------------------------------------------------- selection
+// Per-thread scratch of the row packer.
+struct Scratch {
+  std::vector<float> S, D;          // significance, decomposition key (K each)
+  std::vector<uint8_t> om8, im8;    // outlier / inlier position masks per 8-group
+  explicit Scratch(int64_t K)
+      : S(size_t(K)), D(size_t(K)), om8(size_t(K / 8)), im8(size_t(K / 8)) {}
+};
+
+// The inlier quantizer applied to the positions `keep8` of row w, and the
+// error it makes on each of them: D[k] = |w[k] - deq[k]| (fp32), 0 off the
+// kept positions.  Same scale rules as the final inlier quantization.
+sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* keep8, float* D) {
+  const int qv = c.mx ? 32 : 16;
+  for (int64_t k0 = 0; k0 < K; k0 += qv) {
+    float a = 0.f;
+    for (int kk = 0; kk < qv; ++kk) {
+      const int64_t k = k0 + kk;
+      if ((keep8[k / 8] >> (k % 8)) & 1u) a = std::fmax(a, std::fabs(w[k]));
+    }
+    for (int kk = 0; kk < qv; ++kk) {
+      const int64_t k = k0 + kk;
+      float deq = 0.f;
+      if (c.mx) {
+        if (a > 0.f) {
+          const int E = clamp_int(floor_log2f(a) - 2, -127, 127);
+          const uint8_t q = enc_e2m1(std::ldexp(double(w[k]), -E));
+          static const float mag[8] = {0.f, 0.5f, 1.f, 1.5f, 2.f, 3.f, 4.f, 6.f};
+          deq = std::ldexp((q & 8u) ? -mag[q & 7u] : mag[q & 7u], E);
+        }
+      } else {
+        const uint16_t h = f32_to_f16_bits(a / 7.0f);
+        if ((h & 0x7C00u) == 0x7C00u) return SDQ_ERR_VALUE;  // scale overflows fp16
+        const float sc = f16_bits_to_f32(h);
+        if (sc != 0.f) deq = float(clamp_int(int(std::nearbyint(w[k] / sc)), -7, 7)) * sc;
+      }
+      D[k] = ((keep8[k / 8] >> (k % 8)) & 1u) ? std::fabs(w[k] - deq) : 0.f;
+    }
+  }
+  return SDQ_OK;
+}
+
+// Outlier and inlier masks of every 8-group of row w into sc.om8 / sc.im8.
+sdq_status select_row(const Cfg& c, const float* w, const float* act_norm, int64_t K, Scratch& sc) {
+  float* S = sc.S.data();
+  float* D = sc.D.data();
+  uint8_t* om8 = sc.om8.data();
+  uint8_t* im8 = sc.im8.data();
+  const int64_t G8 = K / 8, Go = K / c.m_o;
+  for (int64_t k = 0; k < K; ++k) {
+    if (!std::isfinite(w[k])) return SDQ_ERR_VALUE;
+    S[k] = std::fabs(w[k]);
+    if (c.metric == SDQ_METRIC_PRODUCT) S[k] = S[k] * act_norm[k];
+  }
+  auto set_outliers = [&](int64_t go, uint32_t mk) {
+    if (c.m_o == 8) {
+      om8[go] = uint8_t(mk);
+    } else {  // m_o == 16
+      om8[2 * go] = uint8_t(mk & 0xFFu);
+      om8[2 * go + 1] = uint8_t(mk >> 8);
+    }
+  };
+  const bool staged = c.decomp != SDQ_DECOMP_SAME || c.order != SDQ_ORDER_LARGE;
+  if (!staged) {
+    // outliers first over each whole m_o-group, then inliers among the rest
+    for (int64_t g = 0; g < G8; ++g) om8[g] = 0;
+    if (c.n_o)
+      for (int64_t go = 0; go < Go; ++go) set_outliers(go, top_n(S + go * c.m_o, (1u << c.m_o) - 1u, c.m_o, c.n_o));
+    for (int64_t g = 0; g < G8; ++g) im8[g] = uint8_t(top_n(S + g * 8, 0xFFu & ~uint32_t(om8[g]), 8, c.n_i));
+  } else {
+    // Stage 1: every 8-group keeps its n_o + n_i most significant positions
+    // (held in im8 until the inliers are chosen)
+    for (int64_t g = 0; g < G8; ++g) im8[g] = uint8_t(top_n(S + g * 8, 0xFFu, 8, c.n_o + c.n_i));
+    // Stage 2: the decomposition key, negated for the smallest-first order
+    switch (c.decomp) {
+      case SDQ_DECOMP_SAME:
+        for (int64_t k = 0; k < K; ++k) D[k] = S[k];
+        break;
+      case SDQ_DECOMP_MAGNITUDE:
+        for (int64_t k = 0; k < K; ++k) D[k] = std::fabs(w[k]);
+        break;
+      case SDQ_DECOMP_PRODUCT:
+        for (int64_t k = 0; k < K; ++k) D[k] = std::fabs(w[k]) * act_norm[k];
+        break;
+      default: {
+        const sdq_status st = inlier_error(c, w, K, im8, D);
+        if (st != SDQ_OK) return st;
+        if (c.decomp == SDQ_DECOMP_OUTPUT_ERROR)
+          for (int64_t k = 0; k < K; ++k) D[k] = D[k] * act_norm[k];
+      }
+    }
+    if (c.order == SDQ_ORDER_SMALL)
+      for (int64_t k = 0; k < K; ++k) D[k] = -D[k];
+    for (int64_t go = 0; go < Go; ++go) {
+      const uint32_t kept = c.m_o == 8 ? uint32_t(im8[go]) : (uint32_t(im8[2 * go]) | (uint32_t(im8[2 * go + 1]) << 8));
+      set_outliers(go, top_n(D + go * c.m_o, kept, c.m_o, c.n_o));
+    }
+    for (int64_t g = 0; g < G8; ++g) im8[g] = uint8_t(top_n(S + g * 8, uint32_t(im8[g]) & ~uint32_t(om8[g]), 8, c.n_i));
+  }
+  for (int64_t g = 0; g < G8; ++g) {
+    int cnt = 0;
+    for (int p = 0; p < 8; ++p) cnt += (im8[g] >> p) & 1;
+    if (cnt != c.n_i) return SDQ_ERR_CONFIG;  // fewer candidates than slots
+  }
+  return SDQ_OK;
+}
+
 // ---------------------------------------------------------------- one row
 // Everything the packer decides for one row of W.
 struct RowSink {
@@ -148,30 +259,23 @@ struct RowSink {
   const Layout* lay;
 };
 
-// Packs row n.  `S` is scratch of K floats.
+// Packs row n with the per-thread scratch sc.
 sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t K, int64_t n,
-                    float* S, const RowSink& out) {
-  for (int64_t k = 0; k < K; ++k) {
-    if (!std::isfinite(w[k])) return SDQ_ERR_VALUE;
-    S[k] = std::fabs(w[k]);
-    if (c.metric == SDQ_METRIC_PRODUCT) S[k] = S[k] * act_norm[k];
+                    Scratch& sc, const RowSink& out) {
+  {
+    const sdq_status st = select_row(c, w, act_norm, K, sc);
+    if (st != SDQ_OK) return st;
   }
+  const uint8_t* om8 = sc.om8.data();
+  const uint8_t* im8 = sc.im8.data();
   const int64_t G8 = K / 8, Go = K / c.m_o;
-  // Outlier masks per m_o-group and inlier masks per 8-group (bit p = position p).
-  // Stored per 8-group: omask8[g] holds the outlier bits that fall in 8-group g.
-  auto omask_of_group = [&](int64_t go) -> uint32_t {
-    return c.n_o ? top_n(S + go * c.m_o, (1u << c.m_o) - 1u, c.m_o, c.n_o) : 0u;
-  };
 
   // ---- outlier row scale (INT family) needs the row amax over the outliers
   float s_o = 0.f;
   if (!c.mx && c.n_o) {
     float a = 0.f;
-    for (int64_t go = 0; go < Go; ++go) {
-      const uint32_t mk = omask_of_group(go);
-      for (int p = 0; p < c.m_o; ++p)
-        if ((mk >> p) & 1u) a = std::fmax(a, std::fabs(w[go * c.m_o + p]));
-    }
+    for (int64_t k = 0; k < K; ++k)
+      if ((om8[k / 8] >> (k % 8)) & 1u) a = std::fmax(a, std::fabs(w[k]));
     s_o = a / (c.fmt_o == SDQ_FMT_INT8 ? 127.0f : 448.0f);
     if (out.scale_o) static_cast<float*>(out.scale_o)[n] = s_o;
   }
@@ -180,23 +284,9 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
   const int64_t r = n % kTileN, t = n / kTileN;
   for (int64_t k0 = 0; k0 < K; k0 += 32) {
     uint32_t om[4], im[4];  // per 8-group position masks
-    for (int gg = 0; gg < 4; ++gg) om[gg] = 0;
-    if (c.n_o) {
-      if (c.m_o == 8) {
-        for (int gg = 0; gg < 4; ++gg) om[gg] = omask_of_group(k0 / 8 + gg);
-      } else {  // m_o == 16
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t mk = omask_of_group(k0 / 16 + hh);
-          om[2 * hh] = mk & 0xFFu;
-          om[2 * hh + 1] = (mk >> 8) & 0xFFu;
-        }
-      }
-    }
     for (int gg = 0; gg < 4; ++gg) {
-      im[gg] = top_n(S + k0 + 8 * gg, 0xFFu & ~om[gg], 8, c.n_i);
-      int cnt = 0;
-      for (int p = 0; p < 8; ++p) cnt += (im[gg] >> p) & 1;
-      if (cnt != c.n_i) return SDQ_ERR_CONFIG;  // fewer candidates than slots
+      om[gg] = om8[k0 / 8 + gg];
+      im[gg] = im8[k0 / 8 + gg];
     }
 
     // ---- scales and codes
@@ -342,9 +432,9 @@ sdq_status run_rows(const Cfg& c, const float* W, int64_t N, int64_t K, const fl
   const int T = resolve_threads(n_threads, N);
   std::atomic<int> err{SDQ_OK};
   auto work = [&](int64_t r0, int64_t r1) {
-    std::vector<float> S(static_cast<size_t>(K));
+    Scratch sc(K);
     for (int64_t n = r0; n < r1 && err.load(std::memory_order_relaxed) == SDQ_OK; ++n) {
-      const sdq_status s = pack_row(c, W + n * K, act_norm, K, n, S.data(), sink);
+      const sdq_status s = pack_row(c, W + n * K, act_norm, K, n, sc, sink);
       if (s != SDQ_OK) {
         int expect = SDQ_OK;
         err.compare_exchange_strong(expect, s);
@@ -363,7 +453,7 @@ sdq_status run_rows(const Cfg& c, const float* W, int64_t N, int64_t K, const fl
 }
 
 sdq_status check_act_norm(const Cfg& c, const float* act_norm, int64_t K) {
-  if (c.metric != SDQ_METRIC_PRODUCT) return SDQ_OK;
+  if (!needs_act_norm(c)) return SDQ_OK;
   if (!act_norm) return SDQ_ERR_NULL;
   for (int64_t k = 0; k < K; ++k)
     if (!std::isfinite(act_norm[k]) || act_norm[k] < 0.f) return SDQ_ERR_VALUE;

@@ -8,8 +8,14 @@ namespace sdq {
 
 struct Cfg {
   bool mx;
-  int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric;
+  int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric, decomp, order;
 };
+
+// Whether packing this configuration reads act_norm.
+inline bool needs_act_norm(const Cfg& c) {
+  return c.metric == SDQ_METRIC_PRODUCT || c.decomp == SDQ_DECOMP_PRODUCT ||
+         c.decomp == SDQ_DECOMP_OUTPUT_ERROR;
+}
 
 // Validates a configuration and shape; fills `out` on success.
 inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* out) {
@@ -19,6 +25,10 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   if (c->n_o < 0 || c->n_i < 0 || c->m_o <= 0 || c->m_i <= 0) return SDQ_ERR_CONFIG;
   if (c->n_o > c->m_o || c->n_i > c->m_i || c->n_i == 0) return SDQ_ERR_CONFIG;
   if (c->metric != SDQ_METRIC_MAGNITUDE && c->metric != SDQ_METRIC_PRODUCT) return SDQ_ERR_CONFIG;
+  if (c->decomp < SDQ_DECOMP_SAME || c->decomp > SDQ_DECOMP_OUTPUT_ERROR) return SDQ_ERR_CONFIG;
+  if (c->order != SDQ_ORDER_LARGE && c->order != SDQ_ORDER_SMALL) return SDQ_ERR_CONFIG;
+  // a decomposition other than the default chooses among outliers
+  if ((c->decomp != SDQ_DECOMP_SAME || c->order != SDQ_ORDER_LARGE) && c->n_o == 0) return SDQ_ERR_CONFIG;
   if (mx) {
     if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
       return SDQ_ERR_CONFIG;
@@ -44,6 +54,8 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
     out->fmt_i = c->fmt_i;
     out->fmt_a = c->fmt_a;
     out->metric = c->metric;
+    out->decomp = c->decomp;
+    out->order = c->order;
   }
   return SDQ_OK;
 }

@@ -373,3 +373,35 @@ def test_mx_unmergeable_blocks(kind, n_i, M, N, K, path):
     A = np.abs(S.dequant_act(*S.quantize_act(X, cfg_o), cfg_o))
     T = A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
     assert_close_terms(Y, Yref, T, f"{kind} n_i={n_i} M={M}")
+
+
+@pytest.mark.parametrize("fam,fmt_o,decomp,order", [("int", "e4m3", "output_error", "small"),
+                                                    ("int", "int8", "error", "large"),
+                                                    ("mx", "e4m3", "product", "small"),
+                                                    ("mx", "e4m3", "error", "large")])
+def test_decomposition_variants_end_to_end(fam, fmt_o, decomp, order):
+    """Weights packed with another decomposition metric and order (Section 7's
+    decomposition study) go through the same kernels: the GEMM matches the
+    oracle's product of its own decomposition on every path."""
+    import dataclasses
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(fam, 1, 8, fmt_o, 3 if fam == "int" else 2)
+    cfg = dataclasses.replace(cfg, metric="product", decomp=decomp, order=order)
+    cfg_o = dataclasses.replace(cfg_o, metric="product", decomp=decomp, order=order)
+    N, K = 96, 384
+    W = synth.make_w(1, 0, N, K)
+    an = S.activation_norm(synth.make_x(2, 64, K))  # calibration tokens
+    blob = torch.from_numpy(sdq.pack(W, cfg, act_norm=an)).cuda()
+    cases = [(M, path) for M in (4, 40) for path in _paths(fam, M, 1)]
+    for M, path in cases:
+        X = synth.make_x(1, M, K)
+        Yref = S.reference(X, W, cfg_o, act_norm=an)[0]
+        Xq, s_a = sdq.quantize_act(torch.from_numpy(X).cuda(), cfg)
+        say("variant", fam, fmt_o, decomp, order, M, N, K, "path", path)
+        ws = None
+        if path == sdq.PATH_DENSE:
+            ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K, path), dtype=torch.uint8,
+                             device="cuda")
+        Y = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path, workspace=ws)
+        torch.cuda.synchronize()
+        check(Y.cpu().numpy(), Yref, X, W, cfg_o, f"{fam} {decomp} {order} M={M} path={path}")

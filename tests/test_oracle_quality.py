@@ -1,0 +1,24 @@
+"""The output-error report of the decomposition variants (oracle only)."""
+import numpy as np
+
+import synth
+from oracle import quality as Q
+from oracle import sdq as S
+
+
+def test_report_rows_and_identities():
+    W = synth.make_w(2, 0, 32, 512)
+    X = synth.make_x(2, 8, 512)
+    X_cal = synth.make_x(2, 40, 512)[8:]
+    rows = dict(Q.report(W, X, X_cal, "int", n_is=(3,)))
+    assert len(rows) == 1 + 2 * len(Q.DECOMPS) * len(Q.ORDERS)
+    assert all(np.isfinite(e) and e > 0 for e in rows.values())
+    # the default decomposition is the staged one with the significance metric, largest first
+    assert rows["SDQ 1:8+3:8, product significance, default decomposition"] == \
+        rows["SDQ 1:8+3:8, product significance, product large"]
+    assert rows["SDQ 1:8+3:8, magnitude significance, default decomposition"] == \
+        rows["SDQ 1:8+3:8, magnitude significance, magnitude large"]
+    # the dense baseline keeps every weight: its only errors are the quantizers'
+    L = S.pack_logical(W, Q.dense_baseline("int"))
+    assert L["mask_i"].all() and not L["mask_o"].any()
+    assert rows[next(k for k in rows if k.startswith("dense"))] == Q.rel_error(X, W, Q.dense_baseline("int"))

@@ -262,3 +262,46 @@ def test_absent_outlier_position_is_free(c):
     for j in range(cfg_o.n_i):
         pj = (w >> (8 * j)) & 7
         assert not np.any(absent & (po == pj)), f"slot {j}"
+
+
+# ---- decomposition-metric variants (Section 5, "Stage 2"; Section 7's study)
+DECOMPS = [(d, o) for d in ("same", "magnitude", "product", "error", "output_error")
+           for o in ("large", "small") if (d, o) != ("same", "large")]
+
+
+@pytest.mark.parametrize("decomp,order", DECOMPS, ids=lambda v: str(v))
+@pytest.mark.parametrize("c", [c for c in CONFIGS if c[1] == 1], ids=_ids)
+def test_decomposition_variants_match_oracle(c, decomp, order):
+    fam, n_o, m_o, fmt_o, n_i = c
+    lib, ora = _cfgs(fam, n_o, m_o, fmt_o, n_i, "product")
+    import dataclasses
+    lib = dataclasses.replace(lib, decomp=decomp, order=order)
+    ora = dataclasses.replace(ora, decomp=decomp, order=order)
+    N, K = 40, 256
+    W = synth.make_w(1, 0, N, K)
+    W[3, 10:14] = W[3, 2]           # ties inside groups
+    W[5, :8] = 0.0                  # an all-zero group
+    an = np.exp(np.random.default_rng(7).standard_normal(K)).astype(np.float32)
+    _compare_logical(sdq.pack_logical(W, lib, act_norm=an), S.pack_logical(W, ora, act_norm=an), ora)
+    # and the kernel layout carries the same codes
+    blob = sdq.pack(W, lib, act_norm=an)
+    U = sdq.unpack_dense(blob, lib, N, K)
+    Lo = S.pack_logical(W, ora, act_norm=an)
+    assert np.array_equal(U["code_o_dense"], Lo["code_o_dense"])
+
+
+def test_decomposition_variant_errors():
+    W = np.zeros((32, 128), np.float32)
+    with pytest.raises(sdq.SDQError) as e:   # a variant needs an outlier branch
+        sdq.pack(W, sdq.Config("int", 0, 8, "e4m3", 3, decomp="error"))
+    assert e.value.status == -3
+    for d in ("product", "output_error"):     # these read the activation norms
+        with pytest.raises(sdq.SDQError) as e:
+            sdq.pack(W, sdq.Config("int", 1, 8, "e4m3", 3, decomp=d))
+        assert e.value.status == -1
+    cfg = sdq.Config("int", 1, 8, "e4m3", 3).c()
+    cfg.decomp = 5
+    n = C.c_size_t()
+    assert _lib.lib().sdq_pack_size(C.byref(cfg), 32, 128, C.byref(n)) == -3
+    cfg.decomp, cfg.order = 0, 2
+    assert _lib.lib().sdq_pack_size(C.byref(cfg), 32, 128, C.byref(n)) == -3
