@@ -185,6 +185,8 @@ def decomposition_metric(W: np.ndarray, keep: np.ndarray, cfg: Config,
         return significance(W, act_norm if cfg.metric == "product" else None)
     if cfg.decomp == "magnitude":
         return np.abs(W)
+    if cfg.decomp in ("product", "output_error"):
+        assert act_norm is not None, f"the {cfg.decomp} metric needs act_norm"
     c = None if act_norm is None else np.asarray(act_norm, dtype=np.float32)[None, :]
     if cfg.decomp == "product":
         return (np.abs(W) * c).astype(np.float32)
@@ -197,6 +199,7 @@ def decompose_staged(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] 
     the outliers from what was kept.  Returns (mask_o, pos_o, mask_i, pos_i)."""
     N, K = W.shape
     assert cfg.n_o > 0 and cfg.m_o % cfg.m_i == 0
+    assert cfg.metric != "product" or act_norm is not None, "the product metric needs act_norm"
     S = significance(W, act_norm if cfg.metric == "product" else None)
     # Stage 1: sparsify every m_i-group to its n_o + n_i most significant positions
     keep, _ = top_n_per_group(S, np.ones((N, K), dtype=bool), cfg.m_i, cfg.n_o + cfg.n_i)
@@ -220,6 +223,7 @@ def decompose(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = None)
     cfg.check(K)
     if cfg.staged:
         return decompose_staged(W, cfg, act_norm)
+    assert cfg.metric != "product" or act_norm is not None, "the product metric needs act_norm"
     S = significance(W, act_norm if cfg.metric == "product" else None)
     everything = np.ones((N, K), dtype=bool)
     if cfg.n_o:

@@ -46,17 +46,17 @@ def run_gpu(X, W, cfg, path=sdq.PATH_AUTO, x_bf16=False):
     return Y.cpu().numpy(), Xq, s_a, blob
 
 
-def abs_terms(X, W, cfg_o):
+def abs_terms(X, W, cfg_o, act_norm=None):
     """sum_k |s_a x_k| |w_k| per output (the scale of a dot product's rounding)."""
     Xq, s_a = S.quantize_act(X, cfg_o)
-    L = S.pack_logical(W, cfg_o)
+    L = S.pack_logical(W, cfg_o, act_norm)
     A = np.abs(S.dequant_act(Xq, s_a, cfg_o))
     return A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
 
 
-def check(Y, Yref, X, W, cfg_o, what=""):
+def check(Y, Yref, X, W, cfg_o, what="", act_norm=None):
     if cfg_o.family == "mx":
-        return assert_close_terms(Y, Yref, abs_terms(X, W, cfg_o), what)
+        return assert_close_terms(Y, Yref, abs_terms(X, W, cfg_o, act_norm), what)
     return assert_close(Y, Yref, what)
 
 
@@ -404,4 +404,4 @@ def test_decomposition_variants_end_to_end(fam, fmt_o, decomp, order):
                              device="cuda")
         Y = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path, workspace=ws)
         torch.cuda.synchronize()
-        check(Y.cpu().numpy(), Yref, X, W, cfg_o, f"{fam} {decomp} {order} M={M} path={path}")
+        check(Y.cpu().numpy(), Yref, X, W, cfg_o, f"{fam} {decomp} {order} M={M} path={path}", an)
