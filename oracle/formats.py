@@ -13,6 +13,10 @@ VS-Quant).  The exact encodings follow the public format definitions:
   values 0, 0.5, 1, 1.5, 2, 3, 4, 6.
 * E8M0 (OCP MX shared scale): an unsigned biased exponent, value 2^(c-127);
   code 255 is NaN.
+* ufp8 E6M2 (the unsigned scale format of the paper's quantization study,
+  Section 7): 6 exponent bits with bias 31, 2 mantissa bits, no sign;
+  exponent field 0 encodes subnormals m/4 * 2^-30; every code is finite
+  (the largest is 1.75 * 2^32).
 * fp16: IEEE binary16 (numpy's float16 cast is round-to-nearest-even).
 * integers: round-to-nearest-even (``numpy.rint``) followed by a clamp.
 
@@ -104,6 +108,31 @@ def e2m1_decode(codes: np.ndarray) -> np.ndarray:
 def e2m1_encode(x: np.ndarray) -> np.ndarray:
     """fp32/fp64 -> E2M1 code (low nibble), nearest-even, saturating to +-6."""
     return _encode_nearest_even(x, _E2M1_POS, 0x8, E2M1_MAX)
+
+
+# --------------------------------------------------------------------------
+# ufp8 E6M2 (unsigned)
+# --------------------------------------------------------------------------
+def ue6m2_value(code: int) -> float:
+    code = int(code) & 0xFF
+    e, m = code >> 2, code & 0x3
+    if e == 0:
+        return (m / 4.0) * 2.0 ** -30
+    return (1.0 + m / 4.0) * 2.0 ** (e - 31)
+
+
+UE6M2_TABLE = np.array([ue6m2_value(c) for c in range(256)], dtype=np.float64)
+UE6M2_MAX = float(UE6M2_TABLE[255])
+
+
+def ue6m2_decode(codes: np.ndarray) -> np.ndarray:
+    return UE6M2_TABLE[np.asarray(codes, dtype=np.uint8)]
+
+
+def ue6m2_encode(x: np.ndarray) -> np.ndarray:
+    """Non-negative fp32/fp64 -> ufp8 E6M2 code, nearest-even, saturating."""
+    assert not np.signbit(np.asarray(x, dtype=np.float64)).any(), "E6M2 is unsigned"
+    return _encode_nearest_even(x, UE6M2_TABLE, 0, UE6M2_MAX)
 
 
 # --------------------------------------------------------------------------

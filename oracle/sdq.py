@@ -63,6 +63,9 @@ class Config:
     decomp: str = "same"       # outlier metric (Stage 2): "same" | "magnitude" | "product"
     #                            | "error" | "output_error"
     order: str = "large"       # outliers have the largest ("large") or smallest ("small") metric
+    sfmt_i: str = ""           # inlier scale format (int family): "" = fp16 | "e4m3" (two-level,
+    #                            with a power-of-two scale per row) | "ue6m2"; mx family: e8m0
+    qv: int = 0                # dense K positions per inlier scale; 0 = the family's (16 / 32)
 
     @property
     def staged(self) -> bool:
@@ -72,7 +75,12 @@ class Config:
     @property
     def qv_i(self) -> int:
         """Dense-K positions that share one inlier scale."""
-        return 16 if self.family == "int" else 32
+        return self.qv or (16 if self.family == "int" else 32)
+
+    @property
+    def sfmt(self) -> str:
+        """The inlier scale format: "f16", "e4m3", "ue6m2" or "e8m0"."""
+        return self.sfmt_i or ("f16" if self.family == "int" else "e8m0")
 
     @property
     def qv_o(self) -> int:
@@ -100,6 +108,10 @@ class Config:
         for d in (self.m_i, self.qv_i, m_o, 32 if self.family == "mx" else 1):
             assert K % d == 0, f"K={K} not divisible by {d}"
         assert self.decomp in ("same", "magnitude", "product", "error", "output_error")
+        if self.family == "int":
+            assert self.sfmt in ("f16", "e4m3", "ue6m2") and self.qv_i in (16, 32, 64)
+        else:
+            assert self.sfmt == "e8m0" and self.qv_i == 32
         assert self.order in ("large", "small")
         if self.staged:
             # outliers are chosen among the positions kept by sparsification
@@ -107,10 +119,11 @@ class Config:
             assert self.n_o * (self.m_o // self.m_i) <= self.m_o and self.n_o + self.n_i <= self.m_i
 
 
-def config_from(fmt, metric: str = "magnitude", decomp: str = "same", order: str = "large") -> Config:
+def config_from(fmt, metric: str = "magnitude", decomp: str = "same", order: str = "large",
+                sfmt_i: str = "") -> Config:
     """Build an oracle Config from a plain format description (duck-typed)."""
     return Config(fmt.family, fmt.n_o, fmt.m_o, fmt.fmt_o, fmt.n_i, fmt.m_i,
-                  fmt.fmt_i, fmt.fmt_a, metric, decomp, order)
+                  fmt.fmt_i, fmt.fmt_a, metric, decomp, order, sfmt_i or getattr(fmt, "sfmt_i", ""))
 
 
 # ---------------------------------------------------------------------------
@@ -168,11 +181,8 @@ def inlier_error(W: np.ndarray, keep: np.ndarray, cfg: Config) -> np.ndarray:
     every kept weight -- the quantization error of Section 7's error-based
     decomposition metric."""
     W = np.asarray(W, dtype=np.float32)
-    q, scale = quantize_inliers(W, keep, cfg)
-    if cfg.family == "int":
-        deq = q.astype(np.float32) * np.repeat(scale.astype(np.float32), cfg.qv_i, axis=1)
-    else:
-        deq = (F.e2m1_decode(q) * np.repeat(F.e8m0_value(scale), cfg.qv_i, axis=1)).astype(np.float32)
+    q, scale, row = quantize_inliers(W, keep, cfg)
+    deq = dequant_inliers(dict(cfg=cfg, code_i_dense=q, scale_i=scale, scale_i_row=row)).astype(np.float32)
     return np.where(keep, np.abs(W - deq), np.float32(0)).astype(np.float32)
 
 
@@ -273,13 +283,31 @@ def quantize_outliers(W: np.ndarray, mask_o: np.ndarray, cfg: Config):
     return code, (E + 127).astype(np.uint8)
 
 
+def row_scale_exponent(vmax: np.ndarray) -> np.ndarray:
+    """Per row, the smallest E with vmax <= 448 * 2^E (vmax = the row's largest
+    vector scale), so that every vector scale divided by 2^E fits e4m3; 0 for
+    an all-zero row.  Exact comparisons, no rounding."""
+    vmax = np.asarray(vmax, dtype=np.float64)
+    fl = F.floor_log2(np.where(vmax > 0, vmax, 1.0))
+    E = fl - 8                                         # 448 * 2^(fl-8) = 1.75 * 2^fl
+    E = np.where(vmax > np.ldexp(F.E4M3_MAX, E), E + 1, E)
+    return np.where(vmax > 0, E, 0).astype(np.int64)
+
+
 def quantize_inliers(W: np.ndarray, mask_i: np.ndarray, cfg: Config):
     """Inlier codes (dense [N, K], zero off-support) and scales.
 
-    int family: int4 in [-7, 7] with s = fp16(amax/7) per 16 dense K,
-                q = clamp(rne(W / s), -7, 7) using the stored fp16 scale.
+    int family: int4 in [-7, 7] with a scale per qv dense K (16 by default),
+                q = clamp(rne(W / s), -7, 7) using the stored scale s:
+                  fp16:  s = fp16(amax/7);
+                  e4m3:  VS-Quant's two levels, s = e4m3(v / 2^E) * 2^E with
+                         v = amax/7 (fp32) and 2^E the smallest power of two
+                         that puts the row's largest v within e4m3's 448;
+                  ue6m2: s = ue6m2(amax/7).
     mx family:  fp4 e2m1 with E = floor(log2 amax) - 2 per 32 dense K.
-    Returns codes as int8 values (int family) or e2m1 nibbles (mx family).
+    Returns (codes, stored scales, row scales): codes as int8 values (int
+    family) or e2m1 nibbles (mx family); the stored scale codes per block; the
+    power-of-two second-level scale per row (fp32) for e4m3 scales, else None.
     """
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
@@ -287,21 +315,33 @@ def quantize_inliers(W: np.ndarray, mask_i: np.ndarray, cfg: Config):
     qv = cfg.qv_i
     a = _block_amax(absW, mask_i, qv)
     if cfg.family == "int":
-        s16 = F.f16_round((a / np.float32(7.0)).astype(np.float32))  # fp32 divide, fp16 RNE
-        if not np.isfinite(s16).all():
-            raise ValueError("inlier scale overflows fp16")
-        s32 = s16.astype(np.float32)
+        v_blk = (a / np.float32(7.0)).astype(np.float32)               # fp32 divide
+        row = None
+        if cfg.sfmt == "f16":
+            stored = F.f16_round(v_blk)                                  # fp16 RNE
+            if not np.isfinite(stored).all():
+                raise ValueError("inlier scale overflows fp16")
+            s32 = stored.astype(np.float32)
+        elif cfg.sfmt == "e4m3":
+            E = row_scale_exponent(v_blk.max(axis=1) if v_blk.size else np.zeros(N, np.float32))
+            stored = F.e4m3_encode(np.ldexp(v_blk.astype(np.float64), -E[:, None]))   # exact scaling
+            s32 = np.ldexp(F.e4m3_decode(stored), E[:, None]).astype(np.float32)      # exact
+            row = np.where(v_blk.max(axis=1) > 0, np.ldexp(1.0, E), 0.0).astype(np.float32) \
+                if v_blk.size else np.zeros(N, np.float32)
+        else:  # ue6m2
+            stored = F.ue6m2_encode(v_blk)
+            s32 = F.ue6m2_decode(stored).astype(np.float32)                            # exact
         safe = np.where(s32 == 0, np.float32(1), s32)
         v = (W / np.repeat(safe, qv, axis=1)).astype(np.float32)      # fp32 divide
         q = F.int_rne_clamp(v, 7)
         q = np.where(mask_i & np.repeat(s32 != 0, qv, axis=1), q, 0).astype(np.int8)
-        return q, s16
+        return q, stored, (row if cfg.sfmt == "e4m3" else None)
     E = np.clip(F.floor_log2(np.where(a > 0, a, 1.0)) - 2, -127, 127)
     E = np.where(a > 0, E, -127)
     scale = np.ldexp(1.0, np.repeat(E, qv, axis=1))
     code = F.e2m1_encode(W.astype(np.float64) / scale)
     code = np.where(mask_i & np.repeat(a > 0, qv, axis=1), code, 0).astype(np.uint8)
-    return code, (E + 127).astype(np.uint8)
+    return code, (E + 127).astype(np.uint8), None
 
 
 def _gather(dense: np.ndarray, pos: np.ndarray, m: int) -> np.ndarray:
@@ -318,13 +358,13 @@ def pack_logical(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = No
     mask_o, pos_o, mask_i, pos_i = decompose(W, cfg, act_norm)
     code_o_dense, scale_o = quantize_outliers(W, mask_o, cfg) if cfg.n_o else (
         np.zeros((N, K), np.uint8), np.zeros(N, np.float32))
-    code_i_dense, scale_i = quantize_inliers(W, mask_i, cfg)
+    code_i_dense, scale_i, scale_i_row = quantize_inliers(W, mask_i, cfg)
     return dict(
         N=N, K=K, cfg=cfg,
         pos_o=pos_o, code_o=_gather(code_o_dense, pos_o, cfg.m_o) if cfg.n_o else pos_o.astype(np.uint8),
         scale_o=scale_o,
         pos_i=pos_i, code_i=_gather(code_i_dense, pos_i, cfg.m_i),
-        scale_i=scale_i,
+        scale_i=scale_i, scale_i_row=scale_i_row,
         mask_o=mask_o, mask_i=mask_i,
         code_o_dense=code_o_dense, code_i_dense=code_i_dense,
     )
@@ -345,12 +385,24 @@ def dequant_outliers(L: Dict) -> np.ndarray:
     return F.e4m3_decode(c) * np.repeat(F.e8m0_value(L["scale_o"]), 32, axis=1)
 
 
+def inlier_scale_values(L: Dict) -> np.ndarray:
+    """The effective inlier scale of every block, [N, K/qv], fp64 (exact)."""
+    cfg: Config = L["cfg"]
+    sc = L["scale_i"]
+    if cfg.sfmt == "f16":
+        return sc.astype(np.float64)
+    if cfg.sfmt == "e4m3":
+        return F.e4m3_decode(sc) * L["scale_i_row"].astype(np.float64)[:, None]
+    if cfg.sfmt == "ue6m2":
+        return F.ue6m2_decode(sc)
+    return F.e8m0_value(sc)
+
+
 def dequant_inliers(L: Dict) -> np.ndarray:
     cfg: Config = L["cfg"]
     c = L["code_i_dense"]
-    if cfg.family == "int":
-        return c.astype(np.float64) * np.repeat(L["scale_i"].astype(np.float64), 16, axis=1)
-    return F.e2m1_decode(c) * np.repeat(F.e8m0_value(L["scale_i"]), 32, axis=1)
+    v = c.astype(np.float64) if cfg.family == "int" else F.e2m1_decode(c)
+    return v * np.repeat(inlier_scale_values(L), cfg.qv_i, axis=1)
 
 
 # ---------------------------------------------------------------------------
@@ -399,7 +451,7 @@ def gemm_fp64(Xq: np.ndarray, s_a: np.ndarray, L: Dict):
 def int_partials(Xq: np.ndarray, L: Dict):
     """Exact integer partials of the int family.
 
-    P_i[m, n, kb] = sum_{k in block kb} Xq[m,k] * q_i[n,k] over 16-K blocks;
+    P_i[m, n, kb] = sum_{k in block kb} Xq[m,k] * q_i[n,k] over the qv-K scale blocks;
     P_o[m, n] = sum_k Xq[m,k] * q_o[n,k] when outliers are int8 (else None).
     """
     cfg: Config = L["cfg"]
@@ -408,7 +460,8 @@ def int_partials(Xq: np.ndarray, L: Dict):
     Qi = L["code_i_dense"].astype(np.int64)
     M, K = X.shape
     N = Qi.shape[0]
-    P_i = np.einsum("mbk,nbk->mnb", X.reshape(M, K // 16, 16), Qi.reshape(N, K // 16, 16))
+    qv = cfg.qv_i
+    P_i = np.einsum("mbk,nbk->mnb", X.reshape(M, K // qv, qv), Qi.reshape(N, K // qv, qv))
     P_o = None
     if cfg.n_o and cfg.fmt_o == "int8":
         P_o = X @ L["code_o_dense"].view(np.int8).astype(np.int64).T
@@ -425,6 +478,7 @@ def sparse_gemm_loops(Xq: np.ndarray, s_a: np.ndarray, L: Dict) -> np.ndarray:
     A = dequant_act(Xq, s_a, cfg)
     M = A.shape[0]
     N, K = L["N"], L["K"]
+    sv = inlier_scale_values(L)
     Y = np.zeros((M, N))
     for n in range(N):
         for m in range(M):
@@ -445,9 +499,9 @@ def sparse_gemm_loops(Xq: np.ndarray, s_a: np.ndarray, L: Dict) -> np.ndarray:
                     k = g * cfg.m_i + int(L["pos_i"][n, g, j])
                     c = int(L["code_i"][n, g, j])
                     if cfg.family == "int":
-                        w = c * float(L["scale_i"][n, k // 16])
+                        w = (c - 256 if c > 127 else c) * float(sv[n, k // cfg.qv_i])
                     else:
-                        w = F.e2m1_value(c) * 2.0 ** (int(L["scale_i"][n, k // 32]) - 127)
+                        w = F.e2m1_value(c) * float(sv[n, k // 32])
                     acc += A[m, k] * w
             Y[m, n] = acc
     return Y
