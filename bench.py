@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--layer", type=int, default=0, help="block-sweep layer index (0..6)")
     p.add_argument("--M", type=int, default=1, help="block-sweep token count")
     p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
+    p.add_argument("--inlier-scale", default="", choices=["", "e4m3"],
+                   help="INT family: two-level e4m3 inlier scales instead of the workload's fp16 "
+                        "(the quantized scale format of the paper's Section 7 study)")
     p.add_argument("--rotate-mb", type=float, default=512.0)
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -129,6 +132,12 @@ def main():
         wl_name = synth.WORKLOADS[wid].name
     W_def = synth.WORKLOADS[wid]
     cfg = sdq.Config.of(fmt)
+    if a.inlier_scale:
+        import dataclasses
+        if cfg.family != "int":
+            raise SystemExit("--inlier-scale applies to the INT family only")
+        cfg = dataclasses.replace(cfg, sfmt_i=a.inlier_scale)
+        wl_name += f", {a.inlier_scale} inlier scales (two-level)"
 
     # ---------------------------------------------------------------- inputs
     Ls = [W_def.layers[i] for i in layers]
@@ -257,6 +266,8 @@ def main():
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
     tkey = a.workload if a.workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
+    if a.inlier_scale:
+        tkey += f"_{a.inlier_scale}_scales"
     roof["traffic"] = measured_traffic(tkey)
     roof["kernel_us"] = round(gemm_us / len(Ls), 3)
     # kernels per GEMM call: the two-pass path's time is both passes together
@@ -267,7 +278,7 @@ def main():
     # ---------------------------------------------------------------- CPU oracle
     cpu = None
     if not a.no_cpu_baseline:
-        cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds)
+        cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds, a.inlier_scale)
 
     value = flops / (ms_step * 1e-3) / 1e12
     line = {
@@ -364,7 +375,7 @@ def vendor_context(torch, Ls, M, rotate_mb, n):
     return out
 
 
-def cpu_baseline(Ws, Xs, fmt, M, seconds):
+def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
     """The oracle as it stands, on this host: activation quantization plus the
     fp64 decomposed product of every layer, repeated for about `seconds`."""
     from oracle import sdq as S
@@ -373,7 +384,7 @@ def cpu_baseline(Ws, Xs, fmt, M, seconds):
         threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
-    cfg_o = S.config_from(fmt)
+    cfg_o = S.config_from(fmt, sfmt_i=sfmt_i)
     # bound the sample: at most 64 tokens per layer
     ms = min(M, 64)
     packs = [S.pack_logical(W, cfg_o) for W in Ws]  # offline stage, not timed

@@ -74,6 +74,8 @@ enum {
   SDQ_DECOMP_OUTPUT_ERROR = 4  /* |W - Q_i(W)| * act_norm[k]                   */
 };
 enum { SDQ_ORDER_LARGE = 0, SDQ_ORDER_SMALL = 1 };
+/* Inlier scale format (sdq_config.sfmt_i). */
+enum { SDQ_SCALE_DEFAULT = 0, SDQ_SCALE_E4M3 = 1 };
 enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
 /* sdq_gemm_ex / sdq_gemm_ws kernel choice. */
 enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3 };
@@ -97,7 +99,13 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  *   order   SDQ_ORDER_LARGE: the outliers are the kept weights with the
  *           largest decomp metric ("Large"); SDQ_ORDER_SMALL: the smallest
  * decomp = SAME with order = LARGE (both zero) is the default; any other
- * choice needs n_o = 1. */
+ * choice needs n_o = 1.
+ *   sfmt_i  inlier scale format (Section 3.3: scales are quantized too;
+ *           Section 7 compares 8-bit scale formats): SDQ_SCALE_DEFAULT (INT
+ *           fp16 per 16 K, MX e8m0 per 32 K) or, INT family only,
+ *           SDQ_SCALE_E4M3: VS-Quant's two levels, an fp8-e4m3 scale per 16
+ *           K times one power-of-two scale 2^E per row, E the smallest with
+ *           every vector scale amax/7 of the row <= 448 * 2^E. */
 typedef struct {
   int32_t family;
   int32_t n_o, m_o, fmt_o;
@@ -105,6 +113,7 @@ typedef struct {
   int32_t fmt_a;
   int32_t metric;
   int32_t decomp, order;
+  int32_t sfmt_i;
 } sdq_config;
 
 /* Static description of an error code (never NULL). */
@@ -149,7 +158,10 @@ sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t
  * With decomp SAME and order LARGE the two procedures select the same sets.
  * Quantization (IEEE fp32 arithmetic, round-to-nearest-even):
  *   INT outliers: s_o[n] = amax_row / qmax (qmax 127 or 448), q = enc(W / s_o)
- *   INT inliers:  s = fp16(amax_block16 / 7), q = clamp(rne(W / s), -7, 7)
+ *   INT inliers:  s = fp16(amax_block16 / 7), q = clamp(rne(W / s), -7, 7);
+ *                 with SDQ_SCALE_E4M3, v = amax_block16 / 7 (fp32), the row's
+ *                 E as in sdq_config, code = e4m3(v * 2^-E), s = value(code)
+ *                 * 2^E (exact), q as above
  *   MX:           E = floor(log2 amax_block32) - emax (8 for e4m3, 2 for
  *                 e2m1), q = enc(W / 2^E) saturating
  *   an all-zero block gets a zero scale (E = -127) and zero codes.
@@ -166,20 +178,24 @@ sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
  *   scale_o        INT: float [N];  MX: uint8 e8m0 [N][K/32]
  *   pos_i, code_i  uint8 [N][K/m_i][n_i]  (int4 codes as int8 bits, e2m1
  *                  codes as the low nibble)
- *   scale_i        INT: uint16 fp16 bits [N][K/16];  MX: uint8 e8m0 [N][K/32]
+ *   scale_i        INT: uint16 fp16 bits [N][K/16] (SDQ_SCALE_E4M3: uint8
+ *                  e4m3 codes [N][K/16]);  MX: uint8 e8m0 [N][K/32]
+ *   scale_i_row    SDQ_SCALE_E4M3 only: float [N], the row scale 2^E (0 for
+ *                  a row without inlier magnitude); may be NULL
  * Any pointer for a branch with n = 0 may be NULL. */
 sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
                             const float* act_norm, uint8_t* pos_o, uint8_t* code_o,
                             void* scale_o, uint8_t* pos_i, uint8_t* code_i, void* scale_i,
-                            int n_threads);
+                            float* scale_i_row, int n_threads);
 
 /* Decode a packed blob (host copy) back to dense code arrays: code_o_dense
  * and code_i_dense are uint8 [N][K] holding each stored code at its position
- * and 0 elsewhere; scale_o / scale_i as in sdq_pack_logical.  Used to check
+ * and 0 elsewhere; scale_o / scale_i / scale_i_row as in sdq_pack_logical.  Used to check
  * that the kernel layout round-trips. */
 sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed, size_t bytes,
                             int64_t N, int64_t K, uint8_t* code_o_dense,
-                            uint8_t* code_i_dense, void* scale_o, void* scale_i);
+                            uint8_t* code_i_dense, void* scale_o, void* scale_i,
+                            float* scale_i_row);
 
 /* Per-token activation quantization (Section 5, Stage 3; the activations
  * are quantized to match the weights).  For each row m:

@@ -46,6 +46,7 @@ class Config:
     metric: str = "magnitude"  # significance: "magnitude" | "product"
     decomp: str = "same"       # outlier metric: "same" | "magnitude" | "product" | "error" | "output_error"
     order: str = "large"       # outliers by the largest ("large") or smallest ("small") decomp metric
+    sfmt_i: str = ""           # inlier scales: "" (int fp16 / mx e8m0) | "e4m3" (int, two-level)
 
     @staticmethod
     def int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, metric="magnitude") -> "Config":
@@ -70,7 +71,8 @@ class Config:
                                _FMT[self.fmt_o], self.n_i, self.m_i, _FMT[self.fmt_i],
                                _FMT[self.fmt_a],
                                METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE,
-                               _lib.DECOMP[self.decomp], _lib.ORDER[self.order])
+                               _lib.DECOMP[self.decomp], _lib.ORDER[self.order],
+                               _lib.SCALE[self.sfmt_i])
 
 
 def _p(a) -> C.c_void_p:
@@ -121,12 +123,13 @@ def pack_logical(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = No
         scale_i = np.zeros((N, K // 32), np.uint8)
     else:
         scale_o = np.zeros(N, np.float32)
-        scale_i = np.zeros((N, K // 16), np.uint16)
+        scale_i = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
+    scale_i_row = np.zeros(N, np.float32)
     _lib.check(_lib.lib().sdq_pack_logical(
         C.byref(cfg.c()), _p(W), N, K, _p(an), _p(pos_o), _p(code_o), _p(scale_o), _p(pos_i),
-        _p(code_i), _p(scale_i), n_threads), "sdq_pack_logical")
+        _p(code_i), _p(scale_i), _p(scale_i_row), n_threads), "sdq_pack_logical")
     return dict(pos_o=pos_o, code_o=code_o, scale_o=scale_o, pos_i=pos_i, code_i=code_i,
-                scale_i=scale_i)
+                scale_i=scale_i, scale_i_row=scale_i_row)
 
 
 def unpack_dense(blob: np.ndarray, cfg: Config, N: int, K: int) -> Dict[str, np.ndarray]:
@@ -136,10 +139,12 @@ def unpack_dense(blob: np.ndarray, cfg: Config, N: int, K: int) -> Dict[str, np.
     if cfg.mx:
         so, si = np.zeros((N, K // 32), np.uint8), np.zeros((N, K // 32), np.uint8)
     else:
-        so, si = np.zeros(N, np.float32), np.zeros((N, K // 16), np.uint16)
+        so = np.zeros(N, np.float32)
+        si = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
+    sr = np.zeros(N, np.float32)
     _lib.check(_lib.lib().sdq_unpack_dense(C.byref(cfg.c()), _p(blob), blob.nbytes, N, K, _p(co),
-                                           _p(ci), _p(so), _p(si)), "sdq_unpack_dense")
-    return dict(code_o_dense=co, code_i_dense=ci, scale_o=so, scale_i=si)
+                                           _p(ci), _p(so), _p(si), _p(sr)), "sdq_unpack_dense")
+    return dict(code_o_dense=co, code_i_dense=ci, scale_o=so, scale_i=si, scale_i_row=sr)
 
 
 # ----------------------------------------------------------------- device side

@@ -18,6 +18,7 @@ FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
 METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
 DECOMP = {"same": 0, "magnitude": 1, "product": 2, "error": 3, "output_error": 4}
 ORDER = {"large": 0, "small": 1}
+SCALE = {"": 0, "e4m3": 1}
 DTYPE_F32, DTYPE_BF16 = 0, 1
 PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE = 0, 1, 2, 3
 
@@ -33,7 +34,7 @@ class sdq_config(C.Structure):
     _fields_ = [("family", C.c_int32), ("n_o", C.c_int32), ("m_o", C.c_int32),
                 ("fmt_o", C.c_int32), ("n_i", C.c_int32), ("m_i", C.c_int32),
                 ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32),
-                ("decomp", C.c_int32), ("order", C.c_int32)]
+                ("decomp", C.c_int32), ("order", C.c_int32), ("sfmt_i", C.c_int32)]
 
 
 class SDQError(RuntimeError):
@@ -62,8 +63,8 @@ def lib() -> C.CDLL:
             "sdq_pack_size": (C.c_int, [cfgp, i64, i64, P(C.c_size_t)]),
             "sdq_logical_bytes": (C.c_int, [cfgp, i64, i64, P(C.c_size_t)]),
             "sdq_pack": (C.c_int, [cfgp, vp, i64, i64, vp, vp, C.c_size_t, C.c_int]),
-            "sdq_pack_logical": (C.c_int, [cfgp, vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, C.c_int]),
-            "sdq_unpack_dense": (C.c_int, [cfgp, vp, C.c_size_t, i64, i64, vp, vp, vp, vp]),
+            "sdq_pack_logical": (C.c_int, [cfgp, vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, C.c_int]),
+            "sdq_unpack_dense": (C.c_int, [cfgp, vp, C.c_size_t, i64, i64, vp, vp, vp, vp, vp]),
             "sdq_quantize_act": (C.c_int, [cfgp, vp, C.c_int32, i64, i64, vp, vp, vp]),
             "sdq_gemm": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp]),
             "sdq_gemm_ex": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),

@@ -61,7 +61,7 @@ struct DecodeArgs {
   const uint8_t* blob;
   float* Y;
   int M, N, K, n_chunks;
-  int64_t scales_off, rows_off;
+  int64_t scales_off, rows_off, irow_off;
 };
 
 // LDS bytes of one wave's activation region: MT tokens x (8S chunks + the zero chunk).
@@ -115,12 +115,14 @@ __device__ __forceinline__ uint2 quant8(const float* v, float inv) {
 
 struct StepBuf {
   uint4 w0, w1;  // group words of (row, j) for h = 0 and h = 1
-  uint2 sc;      // the four fp16 scales of blocks 4j..4j+3
+  uint2 sc;      // the four scales of blocks 4j..4j+3: fp16 pairs, or e4m3 bytes of .x
 };
 
 // FUSE: 0 = activations from Xq/s_a, 1 = quantize fp32 X, 2 = quantize bf16 X.
-template <int MT, bool OUT_INT8, int FUSE, int S, int KS, int SPW>
+// SC8: two-level inlier scales (e4m3 per block, a power of two per row).
+template <int MT, bool OUT_INT8, int FUSE, int S, int KS, int SPW, bool SC8>
 __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a) {
+  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
   constexpr int kWG = SPW * KS;                  // waves per workgroup
   extern __shared__ __align__(16) uint8_t xs[];  // [wave][MT][8S + 1][kXStride]
   __shared__ float red[kWG][kDecodeMaxM];
@@ -169,8 +171,9 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
   // ---- 2. the whole weight stream of the wave.  Chunks past K re-read the
   //         last chunk of the tile (in bounds) and meet the zero chunk.
   const uint8_t* tbase = a.blob + size_t(t) * KC * kWordBytesPerTC;
-  const uint8_t* sbase = a.blob + a.scales_off + size_t(t) * KC * kIntScaleBytesPerTC;
-  const uint32_t woff = uint32_t(row * 2 + j) * 16, soff = uint32_t(row * 16 + j * 8);
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(t) * KC * kSB;
+  const uint32_t woff = uint32_t(row * 2 + j) * 16;
+  const uint32_t soff = SC8 ? uint32_t(row * 8 + j * 4) : uint32_t(row * 16 + j * 8);
   StepBuf buf[S];
 #pragma unroll
   for (int d = 0; d < S; ++d) {
@@ -178,10 +181,15 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
     const uint8_t* wp = tbase + (uint32_t(c) * kWordBytesPerTC + woff);
     buf[d].w0 = *reinterpret_cast<const uint4*>(wp);
     buf[d].w1 = *reinterpret_cast<const uint4*>(wp + 1024);  // h = 1: 32 rows x 32 bytes further
-    buf[d].sc = *reinterpret_cast<const uint2*>(sbase + (uint32_t(c) * kIntScaleBytesPerTC + soff));
+    if constexpr (SC8)
+      buf[d].sc = make_uint2(*reinterpret_cast<const uint32_t*>(sbase + (uint32_t(c) * kSB + soff)), 0u);
+    else
+      buf[d].sc = *reinterpret_cast<const uint2*>(sbase + (uint32_t(c) * kSB + soff));
   }
   // 16 * s_o: the inlier dot products carry a factor 16, folded out at the end.
   const float so16 = 16.f * reinterpret_cast<const float*>(a.blob + a.rows_off)[t * kTileN + row];
+  // the inlier row scale of two-level scales (a power of two)
+  const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[t * kTileN + row] : 1.f;
 
   // LDS address of piece i of this lane inside the wave's region
   auto lds_piece = [&](int i) -> uint8_t* {
@@ -286,7 +294,18 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
     const StepBuf& cur = buf[d];
     const uint32_t wa[4] = {cur.w0.x, cur.w0.y, cur.w0.z, cur.w0.w};
     const uint32_t wb[4] = {cur.w1.x, cur.w1.y, cur.w1.z, cur.w1.w};
-    const _Float16 scl[4] = {f16lo(cur.sc.x), f16hi(cur.sc.x), f16lo(cur.sc.y), f16hi(cur.sc.y)};
+    float scl[4];
+    if constexpr (SC8) {
+      scl[0] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 0);
+      scl[1] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 1);
+      scl[2] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 2);
+      scl[3] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 3);
+    } else {
+      scl[0] = float(f16lo(cur.sc.x));
+      scl[1] = float(f16hi(cur.sc.x));
+      scl[2] = float(f16lo(cur.sc.y));
+      scl[3] = float(f16hi(cur.sc.y));
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int kb = 4 * j + q;  // 16-K block inside the chunk
@@ -315,7 +334,7 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
           acco[m] = fmaf((float)(int(g0) >> 24), wo_f[0], acco[m]);
           acco[m] = fmaf((float)(int(g1) >> 24), wo_f[1], acco[m]);
         }
-        acc[m] = fmaf((float)P, (float)scl[q], acc[m]);
+        acc[m] = fmaf((float)P, scl[q], acc[m]);
       }
     }
   }
@@ -325,7 +344,7 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     if constexpr (OUT_INT8) acco[m] = (float)po[m];
-    const float v = sum_lanes_mod4(fmaf(acco[m], so16, acc[m]));
+    const float v = sum_lanes_mod4(fmaf(acco[m], so16, SC8 ? gi * acc[m] : acc[m]));
     if (lane < kSliceRows) part[ws][kq][m][lane] = v;
   }
   __syncthreads();
@@ -367,14 +386,21 @@ template <int MT, int FUSE, int S, int KS>
 hipError_t launch_s(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
   constexpr int SPW = spw_for(MT, S, KS);
   static_assert((kTileN / kSliceRows) % SPW == 0, "slices per workgroup must divide a tile");
-  const Layout L = make_layout(false, a.N, a.K);
+  const Layout L = layout_for(c, a.N, a.K);
   const dim3 grid(unsigned(L.n_tiles * (kTileN / kSliceRows) / SPW));
   const dim3 block(SPW * KS * 64);
   const size_t lds = size_t(SPW) * KS * wave_lds_bytes(MT, S);
-  if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW>), grid, block, lds, st, a);
-  else
-    hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW>), grid, block, lds, st, a);
+  if (c.sc8) {
+    if (c.fmt_o == SDQ_FMT_INT8)
+      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW, true>), grid, block, lds, st, a);
+    else
+      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW, true>), grid, block, lds, st, a);
+  } else {
+    if (c.fmt_o == SDQ_FMT_INT8)
+      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW, false>), grid, block, lds, st, a);
+    else
+      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW, false>), grid, block, lds, st, a);
+  }
   return hipGetLastError();
 }
 
@@ -428,18 +454,18 @@ bool decode_fits(int64_t M, int64_t K) {
 
 hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                              const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
-  const Layout L = make_layout(false, N, K);
+  const Layout L = layout_for(c, N, K);
   DecodeArgs a{Xq, s_a, nullptr, nullptr, nullptr, blob, Y, int(M), int(N), int(K),
-               int(L.n_chunks), L.scales_off, L.rows_off};
+               int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
   return launch_fuse<0>(c, a, st);
 }
 
 hipError_t launch_int_decode_fused(const Cfg& c, const void* X, int x_dtype, int64_t M,
                                    uint8_t* Xq_out, float* s_a_out, const uint8_t* blob, int64_t N,
                                    int64_t K, float* Y, hipStream_t st) {
-  const Layout L = make_layout(false, N, K);
+  const Layout L = layout_for(c, N, K);
   DecodeArgs a{nullptr, nullptr, X, s_a_out, Xq_out, blob, Y, int(M), int(N), int(K),
-               int(L.n_chunks), L.scales_off, L.rows_off};
+               int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
   if (x_dtype == SDQ_DTYPE_BF16) return launch_fuse<2>(c, a, st);
   return launch_fuse<1>(c, a, st);
 }

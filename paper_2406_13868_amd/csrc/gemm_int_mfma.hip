@@ -46,8 +46,21 @@ struct MfmaArgs {
   const uint8_t* blob;
   float* Y;
   int M, N, K, n_chunks, n_tiles;
-  int64_t scales_off, rows_off;
+  int64_t scales_off, rows_off, irow_off;
 };
+
+// The fp16 inlier scale of block kb from a row's scale registers sv: fp16
+// pairs (two per dword), or with two-level e4m3 scales one e4m3 code per byte
+// (four per dword), converted exactly (every e4m3 value is an fp16 value).
+template <bool SC8>
+__device__ __forceinline__ _Float16 block_scale(const uint32_t* sv, int kb) {
+  if constexpr (SC8) {
+    return (_Float16)__builtin_amdgcn_cvt_f32_fp8(int(sv[kb >> 2] >> (8 * (kb & 3))), 0);
+  } else {
+    const uint32_t sw = sv[kb >> 1];
+    return __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+  }
+}
 
 // Four int8 -> four f16 (two dwords), exact: f16(1024 + (b ^ 0x80)) - 1152 = b.
 __device__ __forceinline__ void i8x4_to_f16x4(uint32_t x, uint32_t& lo, uint32_t& hi) {
@@ -121,8 +134,9 @@ __device__ __forceinline__ void outlier_i8(uint32_t w, uint32_t& lo, uint32_t& h
   hi = pos < 4u ? 0u : v;
 }
 
-template <int MS, int NI, bool OUT_INT8>
+template <int MS, int NI, bool OUT_INT8, bool SC8>
 __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
+  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
   constexpr int BM = 32 * MS;
   __shared__ __align__(16) _Float16 xs[2][BM * kLdsRow];
 
@@ -168,13 +182,18 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   // ---- weight stream of this wave's tile
   // lane (col, h): the 32 bytes at ((h*32 + col)*2 + j)*16, j = 0, 1
   const uint8_t* wbase = a.blob + size_t(tile_ok ? tile : 0) * KC * kWordBytesPerTC + size_t(lane) * 32;
-  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kIntScaleBytesPerTC + col * 16;
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kSB + col * (kSB / kTileN);
   uint4 wr0, wr1, sr;
   auto load_w = [&](int c) {
     if (tile_ok) {
       wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
       wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 16);
-      sr = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kIntScaleBytesPerTC);
+      if constexpr (SC8) {
+        const uint2 s8 = *reinterpret_cast<const uint2*>(sbase + size_t(c) * kSB);
+        sr = make_uint4(s8.x, s8.y, 0, 0);
+      } else {
+        sr = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kSB);
+      }
     } else {
       wr0 = wr1 = sr = make_uint4(0, 0, 0, 0);
     }
@@ -198,10 +217,16 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
     if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
 #pragma unroll 2
     for (int kb = 0; kb < 8; ++kb) {
-      const uint32_t sw = sv[kb >> 1];
-      const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      const _Float16 s = block_scale<SC8>(sv, kb);
       h8 bh, bl;
-      scaled_hi_lo(inlier_f16<NI>(wv[kb]), s, bh, bl);
+      if constexpr (SC8) {
+        // an int4 code times an e4m3 scale has at most 7 significant bits:
+        // exact in fp16, so one fragment carries the scaled inlier
+        const h8 sv8 = {s, s, s, s, s, s, s, s};
+        bh = inlier_f16<NI>(wv[kb]) * sv8;
+      } else {
+        scaled_hi_lo(inlier_f16<NI>(wv[kb]), s, bh, bl);
+      }
       const h8 bo = outlier_f16<OUT_INT8>(wv[kb]);
       h8 av[MS];
 #pragma unroll
@@ -211,8 +236,10 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
       for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bh, acc[ms], 0, 0, 0);
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
+      if constexpr (!SC8) {
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
+        for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
+      }
     }
     if (c + 1 < KC) {
       store_x(buf ^ 1);
@@ -224,12 +251,15 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+  // the inlier row scale of two-level e4m3 scales (a power of two: exact)
+  const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[n] : 1.f;
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
   const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, acco[ms][e], acc[ms][e]));
+    for (int e = 0; e < 16; ++e)
+      store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, acco[ms][e], gi * acc[ms][e]));
 }
 
 // Split-K form for few tokens (M <= 64): one 32-row tile of W per workgroup,
@@ -244,8 +274,9 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
 // takes group i on lane half 0 and group 8 + i on lane half 1, so that each
 // lane's activations for a chunk are 64 contiguous bytes (four 16-byte loads
 // per 32-token sub-tile) and its group words two 16-byte runs.
-template <int MS, int NI, bool OUT_INT8, int NW>
+template <int MS, int NI, bool OUT_INT8, int NW, bool SC8>
 __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a) {
+  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
   constexpr int BM = 32 * MS;
   __shared__ float red[NW / 2][16][64];
 
@@ -260,15 +291,15 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   // activation rows (rows past M read 0): wave-uniform bases, 32-bit offsets.
   const __amdgpu_buffer_rsrc_t wr =
       buffer_rsrc(a.blob + size_t(tile) * KC * kWordBytesPerTC, uint32_t(KC) * kWordBytesPerTC);
-  const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(
-      a.blob + a.scales_off + size_t(tile) * KC * kIntScaleBytesPerTC, uint32_t(KC) * kIntScaleBytesPerTC);
+  const __amdgpu_buffer_rsrc_t sr =
+      buffer_rsrc(a.blob + a.scales_off + size_t(tile) * KC * kSB, uint32_t(KC) * kSB);
   const __amdgpu_buffer_rsrc_t xr =
       buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, BM)) * uint32_t(a.K));
-  const uint32_t woff = uint32_t(col * 2 + h) * 16, soff = uint32_t(col) * 16;
+  const uint32_t woff = uint32_t(col * 2 + h) * 16, soff = uint32_t(col) * (kSB / kTileN);
   const uint32_t xoff = uint32_t(col) * uint32_t(a.K) + uint32_t(h) * 64;
 
   struct Stage {
-    uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's eight fp16 block scales
+    uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's eight block scales (fp16, or e4m3 in .x/.y)
     uint4 x[MS][4];     // 64 activation bytes per sub-tile
   };
   auto ld16 = [](__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t so) __attribute__((always_inline)) {
@@ -279,7 +310,13 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
     st.w0 = ld16(wr, woff, uint32_t(c) * kWordBytesPerTC);
     st.w1 = ld16(wr, woff + 1024, uint32_t(c) * kWordBytesPerTC);
-    st.sc = ld16(sr, soff, uint32_t(c) * kIntScaleBytesPerTC);
+    if constexpr (SC8) {
+      typedef unsigned int u2_ __attribute__((ext_vector_type(2)));
+      const u2_ q = __builtin_bit_cast(u2_, __builtin_amdgcn_raw_buffer_load_b64(sr, soff, uint32_t(c) * kSB, 0));
+      st.sc = make_uint4(q[0], q[1], 0, 0);
+    } else {
+      st.sc = ld16(sr, soff, uint32_t(c) * kSB);
+    }
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -306,12 +343,22 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const uint32_t w = wv[i & 1][i >> 1];
-      const int kb = 4 * h + (i >> 1);  // 16-K scale block of group 8h + i
-      // the scale of block kb: half (kb & 1) of word kb >> 1, with kb >> 1 = 2h + (i >> 2)
-      const uint32_t sw = h ? sv[2 + (i >> 2)] : sv[i >> 2];
-      const _Float16 s = __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      // the scale of 16-K block kb = 4h + (i >> 1) of group 8h + i
+      _Float16 s;
+      if constexpr (SC8) {
+        s = (_Float16)__builtin_amdgcn_cvt_f32_fp8(int((h ? sv[1] : sv[0]) >> (8 * ((i >> 1) & 3))), 0);
+      } else {
+        // half (kb & 1) = ((i >> 1) & 1) of dword kb >> 1 = 2h + (i >> 2)
+        const uint32_t sw = h ? sv[2 + (i >> 2)] : sv[i >> 2];
+        s = __builtin_bit_cast(_Float16, (unsigned short)(((i >> 1) & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+      }
       h8 bh, bl;
-      scaled_hi_lo(inlier_f16<NI>(w), s, bh, bl);
+      if constexpr (SC8) {
+        const h8 sv8 = {s, s, s, s, s, s, s, s};
+        bh = inlier_f16<NI>(w) * sv8;  // exact in fp16 (at most 7 significant bits)
+      } else {
+        scaled_hi_lo(inlier_f16<NI>(w), s, bh, bl);
+      }
       h8 av[MS];
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
@@ -345,8 +392,10 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
       }
+      if constexpr (!SC8) {
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
+        for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
+      }
     }
   };
 
@@ -402,56 +451,63 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+  const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[n] : 1.f;  // a power of two
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
   const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, float(acco[ms][e]), acc[ms][e]));
+    for (int e = 0; e < 16; ++e)
+      store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, float(acco[ms][e]), gi * acc[ms][e]));
 }
 
-template <int MS, int NI, int NW>
+template <int MS, int NI, int NW, bool SC8>
 hipError_t launch_splitk(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
   const dim3 block(NW * 64);
   if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, true, NW>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, true, NW, SC8>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, false, NW>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, false, NW, SC8>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
-template <int MS, int NI>
+template <int MS, int NI, bool SC8>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   if constexpr (MS <= 2) {
     // few tokens: split K inside the workgroup so that about 2048+ waves run
     const int64_t waves4 = int64_t(a.n_tiles) * 4 * ((a.M + 32 * MS - 1) / (32 * MS));
-    if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4>(c, a, st);
-    return launch_splitk<MS, NI, 8>(c, a, st);
+    if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SC8>(c, a, st);
+    return launch_splitk<MS, NI, 8, SC8>(c, a, st);
   }
   const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
   const dim3 block(kThreads);
   if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SC8>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false, SC8>), grid, block, 0, st, a);
   return hipGetLastError();
+}
+
+template <int MS, bool SC8>
+hipError_t launch_ms_sc(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
+  if (c.n_i == 1) return launch_ms_ni<MS, 1, SC8>(c, a, st);
+  if (c.n_i == 2) return launch_ms_ni<MS, 2, SC8>(c, a, st);
+  return launch_ms_ni<MS, 3, SC8>(c, a, st);
 }
 
 template <int MS>
 hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.n_i == 1) return launch_ms_ni<MS, 1>(c, a, st);
-  if (c.n_i == 2) return launch_ms_ni<MS, 2>(c, a, st);
-  return launch_ms_ni<MS, 3>(c, a, st);
+  return c.sc8 ? launch_ms_sc<MS, true>(c, a, st) : launch_ms_sc<MS, false>(c, a, st);
 }
 
 }  // namespace
 
 hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
-  const Layout L = make_layout(false, N, K);
+  const Layout L = layout_for(c, N, K);
   MfmaArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
-             L.scales_off, L.rows_off};
+             L.scales_off, L.rows_off, L.irow_off};
   if (M <= 32) return launch_ms<1>(c, a, st);
   // 33..64 tokens: one 64-token block expands every weight once; when that
   // leaves fewer workgroups than compute units, two 32-token blocks fill the

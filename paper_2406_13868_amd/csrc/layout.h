@@ -5,8 +5,10 @@
 // every (tile t, chunk c), in this order:
 //
 //   section A  group words     512 x 32-bit   [t][c] (2 KiB)
-//   section B  block scales    INT: 512 B, MX: 256 B   [t][c]
-//   section C  row scales      INT only: fp32 [t][32]
+//   section B  block scales    INT: 512 B (fp16) or 256 B (e4m3), MX: 256 B   [t][c]
+//   section C  row scales      INT only: fp32 [t][32] outlier scales, then
+//                              with e4m3 block scales fp32 [t][32] inlier
+//                              row scales (powers of two)
 //
 // One 32-bit *group word* describes one 8-wide group (m_i = 8) of one row:
 //
@@ -40,7 +42,8 @@
 //     so lane l = h*32 + r reads the four groups of 32-K block 2s+h of row r.
 //
 // Block scales inside a (tile, chunk):
-//   INT: fp16 scale of row r, 16-K block kb (0..7) at byte (r*8 + kb)*2
+//   INT: fp16 scale of row r, 16-K block kb (0..7) at byte (r*8 + kb)*2;
+//        with e4m3 scales, the code at byte r*8 + kb
 //   MX:  e8m0 of row r, 32-K block b = 2s+h at byte ((h*32 + r)*2 + s)*2 + br
 //        with br = 0 for the outlier branch and 1 for the inlier branch
 //
@@ -57,23 +60,26 @@ constexpr int kGroup = 8;
 constexpr int kWordsPerTC = kTileN * kChunkK / kGroup;            // 512
 constexpr int kWordBytesPerTC = kWordsPerTC * 4;                  // 2048
 constexpr int kIntScaleBytesPerTC = kTileN * (kChunkK / 16) * 2;  // 512
+constexpr int kInt8ScaleBytesPerTC = kTileN * (kChunkK / 16);     // 256 (e4m3 block scales)
 constexpr int kMxScaleBytesPerTC = kTileN * (kChunkK / 32) * 2;   // 256
 
 struct Layout {
   int64_t n_tiles = 0, n_chunks = 0;
-  int64_t words_off = 0, scales_off = 0, rows_off = 0, total = 0;
+  int64_t words_off = 0, scales_off = 0, rows_off = 0, irow_off = 0, total = 0;
   int scale_bytes_per_tc = 0;
 };
 
-inline Layout make_layout(bool mx, int64_t N, int64_t K) {
+// sc8: INT family with e4m3 block scales (and inlier row scales at irow_off)
+inline Layout make_layout(bool mx, int64_t N, int64_t K, bool sc8 = false) {
   Layout L;
   L.n_tiles = (N + kTileN - 1) / kTileN;
   L.n_chunks = K / kChunkK;
-  L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : kIntScaleBytesPerTC;
+  L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : sc8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
   L.words_off = 0;
   L.scales_off = L.n_tiles * L.n_chunks * kWordBytesPerTC;
   L.rows_off = L.scales_off + L.n_tiles * L.n_chunks * L.scale_bytes_per_tc;
-  L.total = L.rows_off + (mx ? 0 : L.n_tiles * kTileN * 4);
+  L.irow_off = L.rows_off + (mx ? 0 : L.n_tiles * kTileN * 4);
+  L.total = L.irow_off + (sc8 ? L.n_tiles * kTileN * 4 : 0);
   return L;
 }
 
@@ -87,6 +93,7 @@ inline int mx_word_index(int g, int r) {
   return ((s * 2 + h) * 32 + r) * 4 + i;
 }
 inline int int_scale_byte(int kb, int r) { return (r * 8 + kb) * 2; }
+inline int int8_scale_byte(int kb, int r) { return r * 8 + kb; }
 inline int mx_scale_byte(int b, int r, int branch) {
   const int s = b >> 1, h = b & 1;
   return ((h * 32 + r) * 2 + s) * 2 + branch;

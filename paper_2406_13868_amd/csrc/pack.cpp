@@ -97,6 +97,13 @@ uint8_t enc_e4m3(double x) {
   return uint8_t(s | ((E + 7) << 3) | mq);
 }
 
+// Value of a non-NaN OCP fp8 E4M3FN code.
+float e4m3_value(uint8_t code) {
+  const int e = (code >> 3) & 0xF, m = code & 7;
+  const float a = e ? std::ldexp(float(8 + m), e - 10) : std::ldexp(float(m), -9);
+  return (code & 0x80) ? -a : a;
+}
+
 // Nearest-even OCP fp4 E2M1 code (low nibble), saturating at +-6; keeps the sign.
 uint8_t enc_e2m1(double x) {
   const uint8_t s = std::signbit(x) ? 0x8 : 0x0;
@@ -146,15 +153,67 @@ uint32_t top_n(const float* S, uint32_t allowed, int m, int n) {
 struct Scratch {
   std::vector<float> S, D;          // significance, decomposition key (K each)
   std::vector<uint8_t> om8, im8;    // outlier / inlier position masks per 8-group
+  std::vector<float> V;             // INT: effective inlier scale per 16-K block
+  std::vector<uint16_t> SC;         // INT: stored scale per block (fp16 bits or e4m3 code)
   explicit Scratch(int64_t K)
-      : S(size_t(K)), D(size_t(K)), om8(size_t(K / 8)), im8(size_t(K / 8)) {}
+      : S(size_t(K)), D(size_t(K)), om8(size_t(K / 8)), im8(size_t(K / 8)),
+        V(size_t(K / 16)), SC(size_t(K / 16)) {}
 };
+
+// INT-family inlier scales of one row over the positions `mask8`: per 16-K
+// block v = amax / 7 (fp32) stored as fp16 (eff = that fp16 value) or, with
+// two-level e4m3 scales, as e4m3(v * 2^-E) with E the smallest exponent that
+// puts the row's largest v within 448 * 2^E (eff = value * 2^E, exact).
+// Writes eff to V and the stored scales to SC; returns the row scale 2^E
+// (0 for a row without inlier magnitude, always 0 for fp16 scales).
+sdq_status int_inlier_scales(const Cfg& c, const float* w, int64_t K, const uint8_t* mask8, float* V,
+                             uint16_t* SC, float* row_scale) {
+  const int64_t B = K / 16;
+  float vmax = 0.f;
+  for (int64_t b = 0; b < B; ++b) {
+    float a = 0.f;
+    for (int kk = 0; kk < 16; ++kk) {
+      const int64_t k = b * 16 + kk;
+      if ((mask8[k / 8] >> (k % 8)) & 1u) a = std::fmax(a, std::fabs(w[k]));
+    }
+    V[b] = a / 7.0f;
+    vmax = std::fmax(vmax, V[b]);
+  }
+  *row_scale = 0.f;
+  if (!c.sc8) {
+    for (int64_t b = 0; b < B; ++b) {
+      const uint16_t h = f32_to_f16_bits(V[b]);
+      if ((h & 0x7C00u) == 0x7C00u) return SDQ_ERR_VALUE;  // scale overflows fp16
+      SC[b] = h;
+      V[b] = f16_bits_to_f32(h);
+    }
+    return SDQ_OK;
+  }
+  int E = 0;
+  if (vmax > 0.f) {
+    E = floor_log2f(vmax) - 8;                        // 448 * 2^(fl - 8) = 1.75 * 2^fl
+    if (double(vmax) > std::ldexp(448.0, E)) ++E;
+    *row_scale = std::ldexp(1.0f, E);
+  }
+  for (int64_t b = 0; b < B; ++b) {
+    const uint8_t code = vmax > 0.f ? enc_e4m3(std::ldexp(double(V[b]), -E)) : uint8_t(0);
+    SC[b] = code;
+    V[b] = std::ldexp(e4m3_value(code), E);
+  }
+  return SDQ_OK;
+}
 
 // The inlier quantizer applied to the positions `keep8` of row w, and the
 // error it makes on each of them: D[k] = |w[k] - deq[k]| (fp32), 0 off the
 // kept positions.  Same scale rules as the final inlier quantization.
-sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* keep8, float* D) {
+sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* keep8, float* D,
+                        float* V, uint16_t* SC) {
   const int qv = c.mx ? 32 : 16;
+  if (!c.mx) {
+    float row;
+    const sdq_status st = int_inlier_scales(c, w, K, keep8, V, SC, &row);
+    if (st != SDQ_OK) return st;
+  }
   for (int64_t k0 = 0; k0 < K; k0 += qv) {
     float a = 0.f;
     for (int kk = 0; kk < qv; ++kk) {
@@ -172,9 +231,7 @@ sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* 
           deq = std::ldexp((q & 8u) ? -mag[q & 7u] : mag[q & 7u], E);
         }
       } else {
-        const uint16_t h = f32_to_f16_bits(a / 7.0f);
-        if ((h & 0x7C00u) == 0x7C00u) return SDQ_ERR_VALUE;  // scale overflows fp16
-        const float sc = f16_bits_to_f32(h);
+        const float sc = V[k0 / 16];
         if (sc != 0.f) deq = float(clamp_int(int(std::nearbyint(w[k] / sc)), -7, 7)) * sc;
       }
       D[k] = ((keep8[k / 8] >> (k % 8)) & 1u) ? std::fabs(w[k] - deq) : 0.f;
@@ -226,7 +283,7 @@ sdq_status select_row(const Cfg& c, const float* w, const float* act_norm, int64
         for (int64_t k = 0; k < K; ++k) D[k] = std::fabs(w[k]) * act_norm[k];
         break;
       default: {
-        const sdq_status st = inlier_error(c, w, K, im8, D);
+        const sdq_status st = inlier_error(c, w, K, im8, D, sc.V.data(), sc.SC.data());
         if (st != SDQ_OK) return st;
         if (c.decomp == SDQ_DECOMP_OUTPUT_ERROR)
           for (int64_t k = 0; k < K; ++k) D[k] = D[k] * act_norm[k];
@@ -253,7 +310,7 @@ sdq_status select_row(const Cfg& c, const float* w, const float* act_norm, int64
 struct RowSink {
   // logical outputs (any may be null)
   uint8_t* pos_o; uint8_t* code_o; void* scale_o;
-  uint8_t* pos_i; uint8_t* code_i; void* scale_i;
+  uint8_t* pos_i; uint8_t* code_i; void* scale_i; float* scale_i_row;
   // kernel layout output (may be null)
   uint8_t* blob;
   const Layout* lay;
@@ -278,6 +335,14 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
       if ((om8[k / 8] >> (k % 8)) & 1u) a = std::fmax(a, std::fabs(w[k]));
     s_o = a / (c.fmt_o == SDQ_FMT_INT8 ? 127.0f : 448.0f);
     if (out.scale_o) static_cast<float*>(out.scale_o)[n] = s_o;
+  }
+
+  // ---- inlier block scales of the row (INT family)
+  float s_irow = 0.f;
+  if (!c.mx) {
+    const sdq_status st = int_inlier_scales(c, w, K, im8, sc.V.data(), sc.SC.data(), &s_irow);
+    if (st != SDQ_OK) return st;
+    if (out.scale_i_row) out.scale_i_row[n] = s_irow;
   }
 
   // ---- walk 32-K spans (one MX block, two INT blocks, four 8-groups)
@@ -314,32 +379,31 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
       if (out.blob) {
         const int64_t ch = k0 / kChunkK;
         const int bb = int((k0 % kChunkK) / 32);
-        uint8_t* sc = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * kMxScaleBytesPerTC;
-        sc[mx_scale_byte(bb, int(r), 0)] = c.n_o ? uint8_t(Eo + 127) : 0;
-        sc[mx_scale_byte(bb, int(r), 1)] = uint8_t(Ei + 127);
+        uint8_t* sb = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * kMxScaleBytesPerTC;
+        sb[mx_scale_byte(bb, int(r), 0)] = c.n_o ? uint8_t(Eo + 127) : 0;
+        sb[mx_scale_byte(bb, int(r), 1)] = uint8_t(Ei + 127);
       }
     } else {
       for (int hb = 0; hb < 2; ++hb) {  // two 16-K blocks
-        float ai = 0.f;
-        for (int gg = 2 * hb; gg < 2 * hb + 2; ++gg)
-          for (int p = 0; p < 8; ++p)
-            if ((im[gg] >> p) & 1u) ai = std::fmax(ai, std::fabs(w[k0 + 8 * gg + p]));
-        const uint16_t h = f32_to_f16_bits(ai / 7.0f);
-        if ((h & 0x7C00u) == 0x7C00u) return SDQ_ERR_VALUE;  // scale overflows fp16
-        const float s = f16_bits_to_f32(h);
+        const int64_t kb = k0 / 16 + hb;
+        const float s = sc.V[kb];
+        const uint16_t h = sc.SC[kb];
         for (int gg = 2 * hb; gg < 2 * hb + 2; ++gg)
           for (int p = 0; p < 8; ++p)
             if (((im[gg] >> p) & 1u) && s != 0.f) {
               const float v = w[k0 + 8 * gg + p] / s;
               icode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(v)), -7, 7)));
             }
-        const int64_t kb = k0 / 16 + hb;
-        if (out.scale_i) static_cast<uint16_t*>(out.scale_i)[n * (K / 16) + kb] = h;
+        if (out.scale_i) {
+          if (c.sc8) static_cast<uint8_t*>(out.scale_i)[n * (K / 16) + kb] = uint8_t(h);
+          else static_cast<uint16_t*>(out.scale_i)[n * (K / 16) + kb] = h;
+        }
         if (out.blob) {
           const int64_t ch = k0 / kChunkK;
           const int kbl = int((k0 % kChunkK) / 16) + hb;
-          uint8_t* sc = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * kIntScaleBytesPerTC;
-          std::memcpy(sc + int_scale_byte(kbl, int(r)), &h, 2);
+          uint8_t* sb = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * out.lay->scale_bytes_per_tc;
+          if (c.sc8) sb[int8_scale_byte(kbl, int(r))] = uint8_t(h);
+          else std::memcpy(sb + int_scale_byte(kbl, int(r)), &h, 2);
         }
       }
       if (c.n_o && s_o != 0.f) {
@@ -415,6 +479,7 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
   if (out.blob && !c.mx) {
     float* rows = reinterpret_cast<float*>(out.blob + out.lay->rows_off);
     rows[n] = s_o;
+    if (c.sc8) reinterpret_cast<float*>(out.blob + out.lay->irow_off)[n] = s_irow;
   }
   return SDQ_OK;
 }
@@ -470,7 +535,7 @@ extern "C" sdq_status sdq_pack_size(const sdq_config* cfg, int64_t N, int64_t K,
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (!bytes) return SDQ_ERR_NULL;
-  *bytes = size_t(make_layout(c.mx, N, K).total);
+  *bytes = size_t(layout_for(c, N, K).total);
   return SDQ_OK;
 }
 
@@ -488,8 +553,9 @@ extern "C" sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_
     bits += (K / 32) * 8;               // inlier e8m0
     if (c.n_o) bits += (K / 32) * 8;    // outlier e8m0
   } else {
-    bits += (K / 16) * 16;              // inlier fp16
-    if (c.n_o) bits += 32;              // outlier fp32 per row
+    bits += (K / 16) * (c.sc8 ? 8 : 16);  // inlier fp16, or e4m3 ...
+    if (c.sc8) bits += 32;                // ... with an fp32 (power of two) per row
+    if (c.n_o) bits += 32;                // outlier fp32 per row
   }
   *bytes = size_t((bits * N + 7) / 8);
   return SDQ_OK;
@@ -501,11 +567,11 @@ extern "C" sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N,
   sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (!W || !packed) return SDQ_ERR_NULL;
-  const Layout lay = make_layout(c.mx, N, K);
+  const Layout lay = layout_for(c, N, K);
   if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
   if ((s = check_act_norm(c, act_norm, K)) != SDQ_OK) return s;
   std::memset(packed, 0, size_t(lay.total));
-  RowSink sink{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+  RowSink sink{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                static_cast<uint8_t*>(packed), &lay};
   return run_rows(c, W, N, K, act_norm, sink, n_threads);
 }
@@ -513,7 +579,7 @@ extern "C" sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N,
 extern "C" sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
                                        const float* act_norm, uint8_t* pos_o, uint8_t* code_o,
                                        void* scale_o, uint8_t* pos_i, uint8_t* code_i,
-                                       void* scale_i, int n_threads) {
+                                       void* scale_i, float* scale_i_row, int n_threads) {
   Cfg c;
   sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
@@ -524,18 +590,21 @@ extern "C" sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, in
     if (c.mx) std::memset(scale_o, 0, size_t(N * (K / 32)));
     else std::memset(scale_o, 0, size_t(N) * 4);
   }
-  RowSink sink{pos_o, code_o, scale_o, pos_i, code_i, scale_i, nullptr, nullptr};
+  if (scale_i_row && !c.sc8) std::memset(scale_i_row, 0, size_t(N) * 4);
+  RowSink sink{pos_o, code_o, scale_o, pos_i, code_i, scale_i, c.sc8 ? scale_i_row : nullptr,
+               nullptr, nullptr};
   return run_rows(c, W, N, K, act_norm, sink, n_threads);
 }
 
 extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed, size_t bytes,
                                        int64_t N, int64_t K, uint8_t* code_o_dense,
-                                       uint8_t* code_i_dense, void* scale_o, void* scale_i) {
+                                       uint8_t* code_i_dense, void* scale_o, void* scale_i,
+                                       float* scale_i_row) {
   Cfg c;
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (!packed || !code_o_dense || !code_i_dense || !scale_o || !scale_i) return SDQ_ERR_NULL;
-  const Layout lay = make_layout(c.mx, N, K);
+  const Layout lay = layout_for(c, N, K);
   if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
   const uint8_t* blob = static_cast<const uint8_t*>(packed);
   std::memset(code_o_dense, 0, size_t(N * K));
@@ -570,15 +639,20 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
         }
       } else {
         for (int kb = 0; kb < 8; ++kb) {
-          uint16_t h;
-          std::memcpy(&h, sc + int_scale_byte(kb, r), 2);
-          static_cast<uint16_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = h;
+          if (c.sc8) {
+            static_cast<uint8_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = sc[int8_scale_byte(kb, r)];
+          } else {
+            uint16_t h;
+            std::memcpy(&h, sc + int_scale_byte(kb, r), 2);
+            static_cast<uint16_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = h;
+          }
         }
       }
     }
     if (!c.mx) {
       const float* rows = reinterpret_cast<const float*>(blob + lay.rows_off);
       static_cast<float*>(scale_o)[n] = rows[n];
+      if (scale_i_row) scale_i_row[n] = c.sc8 ? reinterpret_cast<const float*>(blob + lay.irow_off)[n] : 0.f;
     }
   }
   return SDQ_OK;

@@ -2,6 +2,7 @@
 #pragma once
 #include <cstdint>
 
+#include "layout.h"
 #include "sdq.h"
 
 namespace sdq {
@@ -9,7 +10,10 @@ namespace sdq {
 struct Cfg {
   bool mx;
   int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric, decomp, order;
+  bool sc8;  // INT family with two-level e4m3 inlier scales
 };
+
+inline Layout layout_for(const Cfg& c, int64_t N, int64_t K) { return make_layout(c.mx, N, K, c.sc8); }
 
 // Whether packing this configuration reads act_norm.
 inline bool needs_act_norm(const Cfg& c) {
@@ -29,6 +33,8 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   if (c->order != SDQ_ORDER_LARGE && c->order != SDQ_ORDER_SMALL) return SDQ_ERR_CONFIG;
   // a decomposition other than the default chooses among outliers
   if ((c->decomp != SDQ_DECOMP_SAME || c->order != SDQ_ORDER_LARGE) && c->n_o == 0) return SDQ_ERR_CONFIG;
+  if (c->sfmt_i != SDQ_SCALE_DEFAULT && c->sfmt_i != SDQ_SCALE_E4M3) return SDQ_ERR_CONFIG;
+  if (c->sfmt_i == SDQ_SCALE_E4M3 && c->family != SDQ_FAMILY_INT) return SDQ_ERR_CONFIG;
   if (mx) {
     if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
       return SDQ_ERR_CONFIG;
@@ -56,6 +62,7 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
     out->metric = c->metric;
     out->decomp = c->decomp;
     out->order = c->order;
+    out->sc8 = c->sfmt_i == SDQ_SCALE_E4M3;
   }
   return SDQ_OK;
 }

@@ -405,3 +405,76 @@ def test_decomposition_variants_end_to_end(fam, fmt_o, decomp, order):
         Y = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path, workspace=ws)
         torch.cuda.synchronize()
         check(Y.cpu().numpy(), Yref, X, W, cfg_o, f"{fam} {decomp} {order} M={M} path={path}", an)
+
+
+# ---- two-level e4m3 inlier scales (Section 3.3: quantized scale factors)
+SC8_CFGS = [("int", 1, 8, "e4m3", 3), ("int", 1, 8, "int8", 3), ("int", 1, 16, "e4m3", 2),
+            ("int", 0, 8, "e4m3", 3)]
+
+
+def _sc8(c):
+    import dataclasses
+    cfg, cfg_o = _cfgs(*c)
+    return dataclasses.replace(cfg, sfmt_i="e4m3"), dataclasses.replace(cfg_o, sfmt_i="e4m3")
+
+
+@pytest.mark.parametrize("c", SC8_CFGS, ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(1, 256, 256), (2, 96, 384), (5, 256, 512), (8, 64, 128),
+                                   (16, 256, 256), (33, 160, 256), (64, 256, 2048),
+                                   (100, 70, 256), (130, 129, 384)])
+def test_e4m3_scales_match_oracle(c, M, N, K):
+    cfg, cfg_o = _sc8(c)
+    X = synth.make_x(1, M, K)
+    W = synth.make_w(1, 0, N, K)
+    W[min(3, N - 1), :] = 0.0                     # a row without inliers: row scale 0
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    for path in _paths("int", M):
+        say("e4m3 scales", _ids(c), M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        check(Y, Yref, X, W, cfg_o, f"e4m3 scales {_ids(c)} M={M} N={N} K={K} path={path}")
+
+
+@pytest.mark.parametrize("fmt_o", ["int8", "e4m3"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 4096), (16, 96, 1024), (64, 64, 4096), (96, 64, 512)])
+def test_e4m3_scales_integer_grid_is_exact(fmt_o, M, N, K):
+    """With every inlier block's amax 7 the two-level scale is e4m3(256) * 2^-8 = 1
+    exactly, so the integer grid must still come out exact."""
+    cfg, cfg_o = _sc8(("int", 1, 8, fmt_o, 3))
+    rng = np.random.default_rng(M * 5 + N)
+    X, W = _int_grid(rng, M, N, K, fmt_o)
+    Yref, _, s_ref, L = S.reference(X, W, cfg_o)
+    assert (s_ref == 1).all() and (S.inlier_scale_values(L) == 1).all()
+    for path in _paths("int", M):
+        say("e4m3 scales grid", fmt_o, M, N, K, "path", path)
+        Y, _, _, _ = run_gpu(X, W, cfg, path)
+        assert np.array_equal(Y.astype(np.float64), Yref), f"path {path}: not exact"
+
+
+@pytest.mark.parametrize("M,layer", [(1, 0), (64, 0), (64, 1)])
+def test_e4m3_scales_full_size_layers(M, layer):
+    """OPT-6.7B FFN shapes (fc1 16384x4096, fc2 4096x16384) with e4m3 scales,
+    every output against the oracle."""
+    cfg, cfg_o = _sc8(("int", 1, 8, "int8", 3))
+    L = synth.WORKLOADS[4].layers[layer]
+    X = synth.make_x(4, M, L.K)
+    W = synth.make_w(4, layer, L.N, L.K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    say("e4m3 scales full", M, L.N, L.K)
+    Y, _, _, _ = run_gpu(X, W, cfg, sdq.PATH_AUTO, x_bf16=True)
+    check(Y, Yref, X, W, cfg_o, f"e4m3 scales full M={M} {L.N}x{L.K}")
+
+
+@pytest.mark.parametrize("M", [1, 2])
+def test_e4m3_scales_fused_linear(M):
+    """sdq_linear (quantize fused into the decode GEMM) with e4m3 scales."""
+    torch = torch_cuda()
+    cfg, cfg_o = _sc8(("int", 1, 8, "e4m3", 3))
+    N, K = 256, 1024
+    X = synth.make_x(2, M, K)
+    W = synth.make_w(2, 0, N, K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    say("e4m3 scales linear", M, N, K)
+    Y, _, _ = sdq.linear(torch.from_numpy(X).cuda(), blob, N, K, cfg)
+    torch.cuda.synchronize()
+    check(Y.cpu().numpy(), Yref, X, W, cfg_o, f"e4m3 scales linear M={M}")

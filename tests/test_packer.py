@@ -305,3 +305,46 @@ def test_decomposition_variant_errors():
     assert _lib.lib().sdq_pack_size(C.byref(cfg), 32, 128, C.byref(n)) == -3
     cfg.decomp, cfg.order = 0, 2
     assert _lib.lib().sdq_pack_size(C.byref(cfg), 32, 128, C.byref(n)) == -3
+
+
+# ---- two-level e4m3 inlier scales (Section 3.3: quantized scale factors)
+@pytest.mark.parametrize("c", [c for c in CONFIGS if c[0] == "int"], ids=_ids)
+def test_e4m3_scales_match_oracle(c):
+    import dataclasses
+    fam, n_o, m_o, fmt_o, n_i = c
+    lib, ora = _cfgs(fam, n_o, m_o, fmt_o, n_i)
+    lib = dataclasses.replace(lib, sfmt_i="e4m3")
+    ora = dataclasses.replace(ora, sfmt_i="e4m3")
+    N, K = 40, 384
+    W = synth.make_w(1, 0, N, K)
+    W[5, :] = 0.0                   # a row without inlier magnitude: row scale 0
+    W[6, :32] *= np.float32(1e-6)   # blocks far below the row's largest: e4m3 subnormal scales
+    Lg, Lo = sdq.pack_logical(W, lib), S.pack_logical(W, ora)
+    assert np.array_equal(Lg["pos_i"], Lo["pos_i"].astype(np.uint8))
+    assert np.array_equal(Lg["code_i"].view(np.int8), Lo["code_i"].astype(np.int8))
+    assert np.array_equal(Lg["scale_i"], Lo["scale_i"])
+    assert np.array_equal(Lg["scale_i_row"].view(np.uint32), Lo["scale_i_row"].view(np.uint32))
+    if n_o:
+        assert np.array_equal(Lg["code_o"], Lo["code_o"])
+    U = sdq.unpack_dense(sdq.pack(W, lib), lib, N, K)
+    assert np.array_equal(U["scale_i"], Lo["scale_i"])
+    assert np.array_equal(U["scale_i_row"], Lo["scale_i_row"])
+    assert np.array_equal(U["code_i_dense"].view(np.int8), Lo["code_i_dense"].astype(np.int8))
+
+
+def test_e4m3_scales_sizes_and_validation():
+    lib = sdq.Config("int", 1, 8, "e4m3", 3, sfmt_i="e4m3")
+    N, K = 4096, 4096
+    n16 = C.c_size_t()
+    n8 = C.c_size_t()
+    L = _lib.lib()
+    assert L.sdq_logical_bytes(C.byref(sdq.Config("int", 1, 8, "e4m3", 3).c()), N, K, C.byref(n16)) == 0
+    assert L.sdq_logical_bytes(C.byref(lib.c()), N, K, C.byref(n8)) == 0
+    # 8 bits instead of 16 per 16-K block, plus 32 bits per row
+    assert n16.value - n8.value == N * (K // 16) - N * 4
+    ps16, ps8 = C.c_size_t(), C.c_size_t()
+    L.sdq_pack_size(C.byref(sdq.Config("int", 1, 8, "e4m3", 3).c()), N, K, C.byref(ps16))
+    L.sdq_pack_size(C.byref(lib.c()), N, K, C.byref(ps8))
+    assert ps16.value - ps8.value == N * (K // 16) - N * 4
+    mx = sdq.Config("mx", 1, 8, "e4m3", 2, 8, "e2m1", "e4m3", sfmt_i="e4m3").c()
+    assert L.sdq_pack_size(C.byref(mx), 32, 128, C.byref(ps8)) == -3   # INT family only
