@@ -15,7 +15,12 @@ decomposed and quantized weights (Section 5.1), for
     output error) in each order (Large, Small) of Section 7's study, with
     the magnitude or the product significance metric for sparsification.
 
-    python -m oracle.quality            # prints a markdown table
+It also reports, for the int family, the inlier scale format (fp16, the
+two-level e4m3 of VS-Quant, ufp8-e6m2; Section 7's quantization study) and
+the Q-Vector size (16, 32, 64 dense positions per scale; Section 3.3) next to
+the resulting logical bits per weight.
+
+    python -m oracle.quality            # prints markdown tables
 """
 from __future__ import annotations
 
@@ -24,6 +29,7 @@ import sys
 
 import numpy as np
 
+from . import accounting as A
 from . import sdq as S
 
 DECOMPS = ("same", "magnitude", "product", "error", "output_error")
@@ -65,6 +71,31 @@ def report(W: np.ndarray, X: np.ndarray, X_cal: np.ndarray, family: str, n_is=(3
     return rows
 
 
+SCALE_BITS = {"f16": 16, "e4m3": 8, "ue6m2": 8}
+
+
+def bits_per_weight(cfg: S.Config, K: int) -> float:
+    """Logical bits per dense weight (values, indices, scales), int family."""
+    b = A.sdq_bits_per_weight(cfg.n_o, cfg.m_o, 8, cfg.n_i, cfg.m_i, 4, 32, 0,
+                              SCALE_BITS[cfg.sfmt], cfg.qv_i, K)
+    if cfg.sfmt == "e4m3":
+        b += A.Fraction(32, K)  # the power-of-two row scale
+    return float(b)
+
+
+def scale_report(W: np.ndarray, X: np.ndarray, X_cal: np.ndarray, n_is=(3, 6)):
+    """Rows (n_i, scale format, qv, bits per weight, error), int family with
+    product significance and the default decomposition."""
+    an = S.activation_norm(X_cal)
+    K = W.shape[1]
+    rows = []
+    for n_i, sfmt, qv in itertools.product(n_is, ("f16", "e4m3", "ue6m2"), (16, 32, 64)):
+        cfg = S.Config("int", 1, 8, "e4m3", n_i, 8, "int4", "int8", "product",
+                       sfmt_i="" if sfmt == "f16" else sfmt, qv=qv)
+        rows.append((n_i, sfmt, qv, bits_per_weight(cfg, K), rel_error(X, W, cfg, an)))
+    return rows
+
+
 def main(argv=None) -> None:
     import synth
     N = int(argv[0]) if argv else 512
@@ -78,6 +109,11 @@ def main(argv=None) -> None:
         print("|---|---|")
         for label, e in report(W, X, X_cal, family):
             print(f"| {label} | {e:.4f} |")
+    print(f"\nint family, inlier scale format and Q-Vector size, W {N}x{K}, X 64x{K}\n")
+    print("| SDQ | scale format | Q-Vector | bits / weight | relative output error |")
+    print("|---|---|---|---|---|")
+    for n_i, sfmt, qv, bits, e in scale_report(W, X, X_cal):
+        print(f"| 1:8 int8/e4m3 + {n_i}:8 int4 | {sfmt} | {qv} | {bits:.3f} | {e:.4f} |")
 
 
 if __name__ == "__main__":

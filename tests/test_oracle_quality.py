@@ -22,3 +22,17 @@ def test_report_rows_and_identities():
     L = S.pack_logical(W, Q.dense_baseline("int"))
     assert L["mask_i"].all() and not L["mask_o"].any()
     assert rows[next(k for k in rows if k.startswith("dense"))] == Q.rel_error(X, W, Q.dense_baseline("int"))
+
+
+def test_scale_report_bits_and_identities():
+    W = synth.make_w(2, 0, 16, 512)
+    X = synth.make_x(2, 4, 512)
+    X_cal = synth.make_x(2, 20, 512)[4:]
+    rows = Q.scale_report(W, X, X_cal, n_is=(3,))
+    assert len(rows) == 9
+    bits = {(r[1], r[2]): r[3] for r in rows}
+    # 1:8 8-bit outliers (1.375) + 3:8 int4 (2.625) + fp32 row scale (32/K) + scales
+    assert bits[("f16", 16)] == 1.375 + 2.625 + 32 / 512 + 1.0
+    assert bits[("e4m3", 16)] == 1.375 + 2.625 + 32 / 512 + 0.5 + 32 / 512
+    assert bits[("ue6m2", 64)] == 1.375 + 2.625 + 32 / 512 + 0.125
+    assert all(np.isfinite(r[4]) and r[4] > 0 for r in rows)
