@@ -23,6 +23,9 @@ Paper passages followed (Jeong et al., SDQ):
 * Stage 3 quantizes each branch with per-vector (VS-Quant) scale factors,
   outliers at a higher precision than inliers; activations are quantized too
   (Section 3.3 and Section 5, "Stage 3").
+* The dual family follows Section 5.1's worked configuration: int8
+  outliers with int8 activations A_o and fp4 inliers with fp4 activations
+  A_i, O = SpMM(A_o, W_o) + SpMM(A_i, W_i).
 * Inference is O = SpMM(A, W_o) + SpMM(A, W_i) (Section 5.1); since both
   branches skip only zeros, it equals the dense product of the activations
   with the dequantized W_o + W_i, which is what ``gemm_fp64`` computes.
@@ -51,7 +54,7 @@ from . import formats as F
 
 @dataclasses.dataclass(frozen=True)
 class Config:
-    family: str        # "int" | "mx"
+    family: str        # "int" | "mx" | "dual"
     n_o: int
     m_o: int
     fmt_o: str         # "e4m3" | "int8"
@@ -85,15 +88,22 @@ class Config:
     @property
     def qv_o(self) -> int:
         """Dense-K positions that share one outlier scale (0 = whole row)."""
-        return 0 if self.family == "int" else 32
+        return 32 if self.family == "mx" else 0
+
+    @property
+    def row_outliers(self) -> bool:
+        """Outliers with one fp32 scale per row (int and dual families)."""
+        return self.family in ("int", "dual")
 
     def check(self, K: int) -> None:
-        assert self.family in ("int", "mx")
+        assert self.family in ("int", "mx", "dual")
         assert self.m_i in (4, 8, 16) and 1 <= self.n_i <= self.m_i
         assert self.n_o == 0 or (self.m_o in (4, 8, 16) and 1 <= self.n_o <= self.m_o)
         if self.family == "int":
             assert self.fmt_o in ("e4m3", "int8") and self.fmt_i == "int4"
             assert self.fmt_a == "int8"
+        elif self.family == "dual":
+            assert self.fmt_o == "int8" and self.fmt_i == "e2m1" and self.fmt_a == "int8+e2m1"
         else:
             assert self.fmt_o == "e4m3" and self.fmt_i == "e2m1" and self.fmt_a == "e4m3"
         # every m_i-group must still hold n_i candidates after outlier extraction
@@ -105,7 +115,7 @@ class Config:
             most = self.n_o * (self.m_i // self.m_o)
         assert self.n_i + most <= self.m_i, "infeasible n_i"
         m_o = self.m_o if self.n_o else self.m_i
-        for d in (self.m_i, self.qv_i, m_o, 32 if self.family == "mx" else 1):
+        for d in (self.m_i, self.qv_i, m_o, 1 if self.family == "int" else 32):
             assert K % d == 0, f"K={K} not divisible by {d}"
         assert self.decomp in ("same", "magnitude", "product", "error", "output_error")
         if self.family == "int":
@@ -255,13 +265,13 @@ def _block_amax(absW: np.ndarray, mask: np.ndarray, qv: int) -> np.ndarray:
 def quantize_outliers(W: np.ndarray, mask_o: np.ndarray, cfg: Config):
     """Outlier codes (dense [N, K], zero off-support) and scales.
 
-    int family: one fp32 scale per row, s_o = amax/qmax, q = enc(W / s_o).
-    mx family:  one e8m0 exponent per 32 K, E = floor(log2 amax) - 8.
+    int, dual: one fp32 scale per row, s_o = amax/qmax, q = enc(W / s_o).
+    mx family: one e8m0 exponent per 32 K, E = floor(log2 amax) - 8.
     """
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
     absW = np.abs(W)
-    if cfg.family == "int":
+    if cfg.row_outliers:
         qmax = np.float32(127.0 if cfg.fmt_o == "int8" else F.E4M3_MAX)
         a = np.where(mask_o, absW, np.float32(0)).max(axis=1) if K else np.zeros(N, np.float32)
         s = (a / qmax).astype(np.float32)                          # fp32 divide
@@ -379,7 +389,7 @@ def dequant_outliers(L: Dict) -> np.ndarray:
     c = L["code_o_dense"]
     if not cfg.n_o:
         return np.zeros((N, K))
-    if cfg.family == "int":
+    if cfg.row_outliers:
         v = c.view(np.int8).astype(np.float64) if cfg.fmt_o == "int8" else F.e4m3_decode(c)
         return v * L["scale_o"].astype(np.float64)[:, None]
     return F.e4m3_decode(c) * np.repeat(F.e8m0_value(L["scale_o"]), 32, axis=1)
@@ -455,13 +465,14 @@ def int_partials(Xq: np.ndarray, L: Dict):
     P_o[m, n] = sum_k Xq[m,k] * q_o[n,k] when outliers are int8 (else None).
     """
     cfg: Config = L["cfg"]
-    assert cfg.family == "int"
+    assert cfg.family in ("int", "dual")
     X = Xq.view(np.int8).astype(np.int64)
     Qi = L["code_i_dense"].astype(np.int64)
     M, K = X.shape
     N = Qi.shape[0]
     qv = cfg.qv_i
-    P_i = np.einsum("mbk,nbk->mnb", X.reshape(M, K // qv, qv), Qi.reshape(N, K // qv, qv))
+    P_i = None if cfg.family == "dual" else \
+        np.einsum("mbk,nbk->mnb", X.reshape(M, K // qv, qv), Qi.reshape(N, K // qv, qv))
     P_o = None
     if cfg.n_o and cfg.fmt_o == "int8":
         P_o = X @ L["code_o_dense"].view(np.int8).astype(np.int64).T
@@ -488,7 +499,7 @@ def sparse_gemm_loops(Xq: np.ndarray, s_a: np.ndarray, L: Dict) -> np.ndarray:
                     for j in range(cfg.n_o):
                         k = g * cfg.m_o + int(L["pos_o"][n, g, j])
                         c = int(L["code_o"][n, g, j])
-                        if cfg.family == "int":
+                        if cfg.row_outliers:
                             w = (c - 256 if c > 127 else c) if cfg.fmt_o == "int8" else F.e4m3_value(c)
                             w *= float(L["scale_o"][n])
                         else:
@@ -507,9 +518,76 @@ def sparse_gemm_loops(Xq: np.ndarray, s_a: np.ndarray, L: Dict) -> np.ndarray:
     return Y
 
 
+# ---------------------------------------------------------------------------
+# the dual family (Section 5.1's worked configuration): int8 A_o, fp4 A_i
+# ---------------------------------------------------------------------------
+def quantize_act_dual(X: np.ndarray):
+    """A_o: int8 per token, as ``quantize_act`` for an int8 configuration.
+    A_i: MXFP4 per token, one e8m0 exponent per 32 K, E = floor(log2 amax) - 2
+    (clamped to [-127, 127]; an all-zero block gets E = -127 and zero codes),
+    codes e2m1(X / 2^E) nearest-even, saturating.
+    Returns (Ao int8 codes as uint8 [M, K], s_ao fp32 [M],
+             Ai e2m1 codes [M, K] (one nibble per byte), Ea e8m0 codes [M, K/32])."""
+    X = np.asarray(X, dtype=np.float32)
+    M, K = X.shape
+    Ao, s_ao = quantize_act(X, Config("int", 0, 8, "e4m3", 1, 8, "int4", "int8"))
+    a = np.abs(X).reshape(M, K // 32, 32).max(axis=-1)
+    E = np.clip(F.floor_log2(np.where(a > 0, a, 1.0)) - 2, -127, 127)
+    E = np.where(a > 0, E, -127)
+    Ai = F.e2m1_encode(X.astype(np.float64) / np.ldexp(1.0, np.repeat(E, 32, axis=1)))
+    Ai = np.where(np.repeat(a > 0, 32, axis=1), Ai, 0).astype(np.uint8)
+    return Ao, s_ao, Ai, (E + 127).astype(np.uint8)
+
+
+def dequant_act_dual(Ao, s_ao, Ai, Ea):
+    """(A_o, A_i) dequantized, fp64."""
+    A_o = Ao.view(np.int8).astype(np.float64) * s_ao.astype(np.float64)[:, None]
+    A_i = F.e2m1_decode(Ai) * np.repeat(F.e8m0_value(Ea), 32, axis=1)
+    return A_o, A_i
+
+
+def gemm_fp64_dual(Ao, s_ao, Ai, Ea, L: Dict):
+    """O = A_o W_o^T + A_i W_i^T in fp64; also O_o and O_i."""
+    A_o, A_i = dequant_act_dual(Ao, s_ao, Ai, Ea)
+    Y_o = A_o @ dequant_outliers(L).T
+    Y_i = A_i @ dequant_inliers(L).T
+    return Y_o + Y_i, Y_o, Y_i
+
+
+def sparse_gemm_loops_dual(Ao, s_ao, Ai, Ea, L: Dict) -> np.ndarray:
+    """The two SpMMs of the dual family as loops over the stored slots (tiny
+    shapes only): outliers against A_o, inliers against A_i."""
+    cfg: Config = L["cfg"]
+    A_o, A_i = dequant_act_dual(Ao, s_ao, Ai, Ea)
+    M = A_o.shape[0]
+    N, K = L["N"], L["K"]
+    Y = np.zeros((M, N))
+    for n in range(N):
+        for m in range(M):
+            acc = 0.0
+            for g in range(K // cfg.m_o if cfg.n_o else 0):
+                for j in range(cfg.n_o):
+                    k = g * cfg.m_o + int(L["pos_o"][n, g, j])
+                    c = int(L["code_o"][n, g, j])
+                    acc += A_o[m, k] * (c - 256 if c > 127 else c) * float(L["scale_o"][n])
+            for g in range(K // cfg.m_i):
+                for j in range(cfg.n_i):
+                    k = g * cfg.m_i + int(L["pos_i"][n, g, j])
+                    w = F.e2m1_value(int(L["code_i"][n, g, j])) * 2.0 ** (int(L["scale_i"][n, k // 32]) - 127)
+                    acc += A_i[m, k] * w
+            Y[m, n] = acc
+    return Y
+
+
 def reference(X: np.ndarray, W: np.ndarray, cfg: Config, act_norm=None):
-    """Convenience: quantize activations, pack, and multiply."""
-    Xq, s_a = quantize_act(X, cfg)
+    """Convenience: quantize activations, pack, and multiply.  For the dual
+    family the activations come back as (Ao, Ai) and their scales as
+    (s_ao, Ea)."""
     L = pack_logical(W, cfg, act_norm)
+    if cfg.family == "dual":
+        Ao, s_ao, Ai, Ea = quantize_act_dual(X)
+        Y, _, _ = gemm_fp64_dual(Ao, s_ao, Ai, Ea, L)
+        return Y, (Ao, Ai), (s_ao, Ea), L
+    Xq, s_a = quantize_act(X, cfg)
     Y, _, _ = gemm_fp64(Xq, s_a, L)
     return Y, Xq, s_a, L
