@@ -60,8 +60,15 @@ typedef enum {
  *  SDQ_FAMILY_MX: activations fp8-e4m3 per token (fp32 scale); outliers
  *    fp8-e4m3 and inliers fp4-e2m1, each branch with one e8m0 (power of two)
  *    scale per 32 consecutive K positions of a row (OCP MX shared exponents).
+ *  SDQ_FAMILY_DUAL (Section 5.1's worked configuration, e.g. 1:8 int8 +
+ *    6:8 fp4): outliers int8 with one fp32 scale per row against int8
+ *    activations A_o (fp32 scale per token); inliers fp4-e2m1 with an e8m0
+ *    scale per 32 K against fp4-e2m1 activations A_i (MXFP4: an e8m0 scale
+ *    per 32 K per token).  fmt_o INT8, fmt_i E2M1, fmt_a INT8 (A_o; A_i is
+ *    implied); n_o in {0, 1} with m_o = 8, any n_i with n_o + n_i <= 8.
+ *    Quantize with sdq_quantize_act_dual and multiply with sdq_gemm_dual.
  */
-enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1 };
+enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1, SDQ_FAMILY_DUAL = 2 };
 enum { SDQ_FMT_INT8 = 1, SDQ_FMT_INT4 = 2, SDQ_FMT_E4M3 = 3, SDQ_FMT_E2M1 = 4 };
 enum { SDQ_METRIC_MAGNITUDE = 0, SDQ_METRIC_PRODUCT = 1 };
 /* Decomposition metric (which kept weights become the outliers) and the
@@ -277,6 +284,35 @@ sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, 
 sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, float* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);
+
+/* Dual family (SDQ_FAMILY_DUAL; Section 5.1's int8 A_o / fp4 A_i): the two
+ * activation tensors of every token, from one read of X.
+ *   X      device, [M, K] row-major, x_dtype SDQ_DTYPE_F32 or SDQ_DTYPE_BF16
+ *   Xq_o   device, [M, K] int8 codes of A_o (as sdq_quantize_act for int8)
+ *   s_a_o  device, [M] fp32 scales of A_o
+ *   Xq_i   device, [M, K/2] bytes: e2m1 codes of A_i, k even in the low nibble
+ *   e_a_i  device, [M, K/32] e8m0 codes: per 32-K block a = max|X|,
+ *          E = floor(log2 a) - 2 clamped to [-127, 127] (a == 0: E = -127 and
+ *          zero codes); code = e2m1(X * 2^-E), nearest even, saturating at 6
+ * X, Xq_o and Xq_i must be 16-byte aligned.  M = 0 is a no-op.  Returns
+ * SDQ_ERR_CONFIG for a configuration of another family. */
+sdq_status sdq_quantize_act_dual(const sdq_config* cfg, const void* X, int32_t x_dtype, int64_t M,
+                                 int64_t K, void* Xq_o, float* s_a_o, void* Xq_i, void* e_a_i,
+                                 void* stream);
+
+/* The dual-family decomposed GEMM (Section 5.1):
+ *   Y[m,n] = s_a_o[m] * s_o[n] * sum_k Xq_o[m,k] * q_o[n,k]
+ *          + sum_k e2m1(Xq_i[m,k]) 2^(e_a_i[m,k/32]-127) * e2m1(q_i[n,k]) 2^(E_i[n,k/32])
+ * with the outlier branch exact in int32 and the inlier branch in fp32.
+ *   Xq_o, s_a_o, Xq_i, e_a_i  device, as written by sdq_quantize_act_dual
+ *   packed   device, the blob written by sdq_pack for the same cfg, N, K
+ *   Y        device, [M, N] fp32 row-major (overwritten)
+ * M = 0 is a no-op.  Deterministic.  sdq_gemm, sdq_gemm_ex, sdq_gemm_ws,
+ * sdq_linear and sdq_quantize_act return SDQ_ERR_UNSUPPORTED for this
+ * family. */
+sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, const float* s_a_o,
+                         const void* Xq_i, const void* e_a_i, int64_t M, const void* packed,
+                         int64_t N, int64_t K, float* Y, void* stream);
 
 #ifdef __cplusplus
 }

@@ -21,21 +21,21 @@ from typing import Dict, Optional
 import numpy as np
 
 from . import _lib
-from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_INT, FAMILY_MX, FMT_E2M1, FMT_E4M3, FMT_INT4,
+from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_DUAL, FAMILY_INT, FAMILY_MX, FMT_E2M1, FMT_E4M3, FMT_INT4,
                    FMT_INT8, METRIC_MAGNITUDE, METRIC_PRODUCT, PATH_AUTO, PATH_DECODE, PATH_MFMA,
                    PATH_DENSE,
                    SDQError)
 
 __all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
            "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
-           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check"]
+           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual"]
 
 _FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
 
 
 @dataclasses.dataclass(frozen=True)
 class Config:
-    family: str = "int"      # "int" | "mx"
+    family: str = "int"      # "int" | "mx" | "dual"
     n_o: int = 1
     m_o: int = 8
     fmt_o: str = "e4m3"      # "e4m3" | "int8"
@@ -62,12 +62,24 @@ class Config:
         return Config(fmt.family, fmt.n_o, fmt.m_o, fmt.fmt_o, fmt.n_i, fmt.m_i, fmt.fmt_i,
                       fmt.fmt_a, metric)
 
+    @staticmethod
+    def dual_family(n_o=1, n_i=6, metric="magnitude") -> "Config":
+        """Section 5.1's worked configuration: n_o:8 int8 outliers against int8
+        activations, n_i:8 fp4 inliers against fp4 (MXFP4) activations."""
+        return Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8", metric)
+
     @property
     def mx(self) -> bool:
         return self.family == "mx"
 
+    @property
+    def e8m0_inliers(self) -> bool:
+        """Inlier scales are e8m0 per 32 K (mx and dual families)."""
+        return self.family in ("mx", "dual")
+
     def c(self) -> _lib.sdq_config:
-        return _lib.sdq_config(FAMILY_MX if self.mx else FAMILY_INT, self.n_o, self.m_o,
+        fam = {"int": FAMILY_INT, "mx": FAMILY_MX, "dual": FAMILY_DUAL}[self.family]
+        return _lib.sdq_config(fam, self.n_o, self.m_o,
                                _FMT[self.fmt_o], self.n_i, self.m_i, _FMT[self.fmt_i],
                                _FMT[self.fmt_a],
                                METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE,
@@ -121,6 +133,9 @@ def pack_logical(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = No
     if cfg.mx:
         scale_o = np.zeros((N, K // 32), np.uint8)
         scale_i = np.zeros((N, K // 32), np.uint8)
+    elif cfg.family == "dual":
+        scale_o = np.zeros(N, np.float32)
+        scale_i = np.zeros((N, K // 32), np.uint8)
     else:
         scale_o = np.zeros(N, np.float32)
         scale_i = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
@@ -138,6 +153,8 @@ def unpack_dense(blob: np.ndarray, cfg: Config, N: int, K: int) -> Dict[str, np.
     ci = np.zeros((N, K), np.uint8)
     if cfg.mx:
         so, si = np.zeros((N, K // 32), np.uint8), np.zeros((N, K // 32), np.uint8)
+    elif cfg.family == "dual":
+        so, si = np.zeros(N, np.float32), np.zeros((N, K // 32), np.uint8)
     else:
         so = np.zeros(N, np.float32)
         si = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
@@ -176,6 +193,43 @@ def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
                                            _dev(Xq, "Xq"), _dev(s_a, "s_a"), _stream(stream)),
                "sdq_quantize_act")
     return Xq, s_a
+
+
+def quantize_act_dual(X, cfg: Config, stream=None):
+    """The dual family's activations on the GPU: returns (Xq_o uint8 [M, K],
+    s_a_o f32 [M], Xq_i uint8 [M, K/2] fp4 nibbles, e_a_i uint8 [M, K/32] e8m0)."""
+    import torch
+    M, K = X.shape
+    if X.dtype == torch.float32:
+        dt = DTYPE_F32
+    elif X.dtype == torch.bfloat16:
+        dt = DTYPE_BF16
+    else:
+        raise ValueError("X must be float32 or bfloat16")
+    dev = X.device
+    Xo = torch.empty((M, K), dtype=torch.uint8, device=dev)
+    s_a = torch.empty((M,), dtype=torch.float32, device=dev)
+    Xi = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+    Ea = torch.empty((M, K // 32), dtype=torch.uint8, device=dev)
+    _lib.check(_lib.lib().sdq_quantize_act_dual(C.byref(cfg.c()), _dev(X, "X"), dt, M, K, _dev(Xo, "Xq_o"),
+                                                _dev(s_a, "s_a_o"), _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"),
+                                                _stream(stream)), "sdq_quantize_act_dual")
+    return Xo, s_a, Xi, Ea
+
+
+def gemm_dual(Xo, s_a, Xi, Ea, packed, N: int, K: int, cfg: Config, out=None, stream=None):
+    """The dual family's GEMM on the GPU (fp32 output [M, N])."""
+    import torch
+    M = Xo.shape[0]
+    if Xo.shape[1] != K or Xi.shape[1] * 2 != K or Ea.shape[1] * 32 != K:
+        raise ValueError("activations have the wrong K")
+    if packed.numel() < pack_size(cfg, N, K):
+        raise ValueError("packed buffer too small")
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=Xo.device)
+    _lib.check(_lib.lib().sdq_gemm_dual(C.byref(cfg.c()), _dev(Xo, "Xq_o"), _dev(s_a, "s_a_o"),
+                                        _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"), M, _dev(packed, "packed"),
+                                        N, K, _dev(Y, "Y"), _stream(stream)), "sdq_gemm_dual")
+    return Y
 
 
 def gemm_workspace_size(cfg: Config, M: int, N: int, K: int, path: int = PATH_AUTO) -> int:

@@ -13,7 +13,7 @@ STATUS = {
     -4: "SDQ_ERR_BUFFER_TOO_SMALL", -5: "SDQ_ERR_HIP", -6: "SDQ_ERR_UNSUPPORTED",
     -7: "SDQ_ERR_VALUE",
 }
-FAMILY_INT, FAMILY_MX = 0, 1
+FAMILY_INT, FAMILY_MX, FAMILY_DUAL = 0, 1, 2
 FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
 METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
 DECOMP = {"same": 0, "magnitude": 1, "product": 2, "error": 3, "output_error": 4}
@@ -27,6 +27,7 @@ EXPORTS = (
     "sdq_status_string", "sdq_check", "sdq_pack_size", "sdq_logical_bytes", "sdq_pack",
     "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
     "sdq_gemm_path", "sdq_linear", "sdq_gemm_workspace_size", "sdq_gemm_ws",
+    "sdq_quantize_act_dual", "sdq_gemm_dual",
 )
 
 
@@ -73,6 +74,8 @@ def lib() -> C.CDLL:
             "sdq_gemm_ws": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_size_t, vp,
                                       C.c_int32]),
             "sdq_linear": (C.c_int, [cfgp, vp, C.c_int32, i64, vp, vp, vp, i64, i64, vp, vp]),
+            "sdq_quantize_act_dual": (C.c_int, [cfgp, vp, C.c_int32, i64, i64, vp, vp, vp, vp, vp]),
+            "sdq_gemm_dual": (C.c_int, [cfgp, vp, vp, vp, vp, i64, vp, i64, i64, vp, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)

@@ -28,6 +28,7 @@ SOURCES = [
     "gemm_int_mfma.hip",
     "gemm_mx_mfma.hip",
     "gemm_mx_dense.hip",
+    "gemm_dual.hip",
 ]
 
 COMMON = [

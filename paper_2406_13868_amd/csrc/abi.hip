@@ -55,6 +55,7 @@ extern "C" sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int
   Cfg c;
   const sdq_status s = check_config(cfg, 1, K, &c);
   if (s != SDQ_OK) return s;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;  // two activation tensors: sdq_quantize_act_dual
   if (M < 0 || M > (int64_t(1) << 31)) return SDQ_ERR_SHAPE;
   if (x_dtype != SDQ_DTYPE_F32 && x_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
   if (M == 0) return SDQ_OK;
@@ -72,6 +73,7 @@ extern "C" sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N,
   if (s != SDQ_OK) return s;
   if (!path) return SDQ_ERR_NULL;
   if (M < 0) return SDQ_ERR_SHAPE;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;  // sdq_gemm_dual has one kernel
   *path = auto_path(c, M, K);
   return SDQ_OK;
 }
@@ -85,6 +87,7 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
   if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
   if (path == SDQ_PATH_DENSE) return SDQ_ERR_UNSUPPORTED;  // needs a workspace: sdq_gemm_ws
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;                  // two activation tensors: sdq_gemm_dual
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16)
@@ -120,6 +123,7 @@ extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, 
   if (!bytes) return SDQ_ERR_NULL;
   if (M < 0) return SDQ_ERR_SHAPE;
   if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, K);
   if (path == SDQ_PATH_DENSE && !(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
   *bytes = path == SDQ_PATH_DENSE ? mx_dense_workspace_bytes(N, K) : 0;
@@ -165,6 +169,7 @@ extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
   if (x_dtype != SDQ_DTYPE_F32 && x_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (M == 0) return SDQ_OK;
   if (!X || !Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq) % 16 ||
@@ -182,4 +187,47 @@ extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x
   const sdq_status q = sdq_quantize_act(cfg, X, x_dtype, M, K, Xq, s_a, stream);
   if (q != SDQ_OK) return q;
   return sdq_gemm(cfg, Xq, s_a, M, packed, N, K, Y, stream);
+}
+
+extern "C" sdq_status sdq_quantize_act_dual(const sdq_config* cfg, const void* X, int32_t x_dtype,
+                                            int64_t M, int64_t K, void* Xq_o, float* s_a_o,
+                                            void* Xq_i, void* e_a_i, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, 1, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!c.dual) return SDQ_ERR_CONFIG;
+  if (M < 0 || M > (int64_t(1) << 31)) return SDQ_ERR_SHAPE;
+  if (x_dtype != SDQ_DTYPE_F32 && x_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
+  if (M == 0) return SDQ_OK;
+  if (!X || !Xq_o || !s_a_o || !Xq_i || !e_a_i) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq_o) % 16 ||
+      reinterpret_cast<uintptr_t>(Xq_i) % 16)
+    return SDQ_ERR_SHAPE;
+  const hipError_t e = launch_act_quant_dual(X, x_dtype, M, K, static_cast<uint8_t*>(Xq_o), s_a_o,
+                                             static_cast<uint8_t*>(Xq_i), static_cast<uint8_t*>(e_a_i),
+                                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, const float* s_a_o,
+                                    const void* Xq_i, const void* e_a_i, int64_t M, const void* packed,
+                                    int64_t N, int64_t K, float* Y, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!c.dual) return SDQ_ERR_CONFIG;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (M == 0) return SDQ_OK;
+  if (!Xq_o || !s_a_o || !Xq_i || !e_a_i || !packed || !Y) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(Xq_o) % 16 || reinterpret_cast<uintptr_t>(Xq_i) % 16 ||
+      reinterpret_cast<uintptr_t>(packed) % 16)
+    return SDQ_ERR_SHAPE;
+  const hipError_t e = launch_dual_mfma(c, static_cast<const uint8_t*>(Xq_o), s_a_o,
+                                        static_cast<const uint8_t*>(Xq_i), static_cast<const uint8_t*>(e_a_i),
+                                        M, static_cast<const uint8_t*>(packed), N, K, Y,
+                                        static_cast<hipStream_t>(stream));
+  if (log_enabled())
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> dual_mfma\n", (long long)M, (long long)N,
+                 (long long)K);
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }

@@ -152,7 +152,76 @@ hipError_t launch_typed(const void* X, int64_t M, int64_t K, uint8_t* Xq, float*
   return hipGetLastError();
 }
 
+// ---- the dual family's two activation tensors (Section 5.1: int8 A_o for
+//      the outliers, fp4 A_i for the inliers).  A_o as above (int8, one fp32
+//      scale per token); A_i is MXFP4: per token and 32-K block, E =
+//      floor(log2 amax) - 2 clamped to [-127, 127] (an all-zero block: E =
+//      -127 and zero codes), codes e2m1(x * 2^-E) to nearest even, saturating
+//      at 6, with the sign of x; two codes per byte, the even k in the low
+//      nibble, and one e8m0 byte E + 127 per block.
+
+// e2m1 code (sign in bit 3) of t, nearest even: the tie points 0.25, 1.25, 2.5
+// and 5 stay on the lower (even) code, 0.75, 1.75 and 3.5 go to the upper one.
+__device__ __forceinline__ uint32_t e2m1_rne(float t) {
+  const float a = fabsf(t);
+  const uint32_t mag = uint32_t(a > 0.25f) + uint32_t(a >= 0.75f) + uint32_t(a > 1.25f) +
+                       uint32_t(a >= 1.75f) + uint32_t(a > 2.5f) + uint32_t(a >= 3.5f) + uint32_t(a > 5.f);
+  return mag | ((__float_as_uint(t) >> 28) & 8u);
+}
+
+// One workgroup per token, two passes over the row (the second from L2):
+// the row amax, then per 8-element piece the int8 codes, the block amax of
+// the four pieces of its 32-K block (lanes 4j..4j+3 of a wave), and the fp4
+// codes.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void act_quant_dual(const void* __restrict__ X, int64_t K,
+                                                           uint8_t* __restrict__ Xo, float* __restrict__ s_a,
+                                                           uint8_t* __restrict__ Xi, uint8_t* __restrict__ Ea) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  const int64_t P = K >> 3;  // pieces of 8 elements, a multiple of 16
+  float amax = 0.f;
+  for (int64_t p = threadIdx.x; p < P; p += kThreads) {
+    float v[8];
+    load8<BF16>(X, m * K + p * 8, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
+  }
+  amax = block_max(amax, red);
+  const float inv = amax > 0.f ? 127.f / amax : 0.f;
+  if (threadIdx.x == 0) s_a[m] = amax / 127.f;
+  for (int64_t base = 0; base < P; base += kThreads) {  // the same trip count for every lane
+    const int64_t p = base + threadIdx.x;
+    const bool ok = p < P;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (ok) load8<BF16>(X, m * K + p * 8, v);
+    float bm = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) bm = fmaxf(bm, fabsf(v[i]));
+    bm = fmaxf(bm, __shfl_xor(bm, 1, 64));
+    bm = fmaxf(bm, __shfl_xor(bm, 2, 64));
+    const int E = bm > 0.f ? min(max(__builtin_amdgcn_frexp_expf(bm) - 1 - 2, -127), 127) : -127;
+    if (!ok) continue;
+    quant_store8<false>(v, inv, Xo + m * K + p * 8);
+    uint32_t q = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) q |= (bm > 0.f ? e2m1_rne(ldexpf(v[i], -E)) : 0u) << (4 * i);
+    *reinterpret_cast<uint32_t*>(Xi + m * (K / 2) + p * 4) = q;
+    if ((p & 3) == 0) Ea[m * (K / 32) + (p >> 2)] = uint8_t(E + 127);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_act_quant_dual(const void* X, int x_dtype, int64_t M, int64_t K, uint8_t* Xo,
+                                 float* s_a, uint8_t* Xi, uint8_t* Ea, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(M)), block(kThreads);
+  if (x_dtype == SDQ_DTYPE_BF16)
+    hipLaunchKernelGGL((act_quant_dual<true>), grid, block, 0, st, X, K, Xo, s_a, Xi, Ea);
+  else
+    hipLaunchKernelGGL((act_quant_dual<false>), grid, block, 0, st, X, K, Xo, s_a, Xi, Ea);
+  return hipGetLastError();
+}
 
 hipError_t launch_act_quant(const Cfg& c, const void* X, int x_dtype, int64_t M, int64_t K,
                             uint8_t* Xq, float* s_a, hipStream_t st) {

@@ -48,6 +48,20 @@
 //        with br = 0 for the outlier branch and 1 for the inlier branch
 //
 // Rows beyond N in the last tile are all-zero (codes and scales).
+//
+// Dual family (int8 outliers against int8 activations, fp4 inliers against
+// fp4 activations), per (tile t, chunk c), in this order:
+//   section A  inlier e2m1 codes, dense   2048 B  [t][c]
+//              piece ((s*2 + h)*32 + r) of 16 bytes holds K 64s + 32h .. +32
+//              of row r (64-K step s), byte j = K 2j (low nibble), 2j + 1
+//              (high nibble): the fp4 operand of lane h*32 + r as loaded
+//   section B  outlier half-words         1024 B  [t][c]
+//              group g = 4u + 2h + i (32-K step u, half h, i in {0,1}) of
+//              row r at half-word ((u*2 + h)*32 + r)*2 + i: bits 0-2 the
+//              position, bits 8-15 the int8 code (0: no outlier)
+//   section C  inlier e8m0 scales          128 B  [t][c]
+//              32-K block b = 2s + h of row r at byte b*32 + r
+//   section D  outlier row scales, fp32 [t][32]
 #pragma once
 #include <cstddef>
 #include <cstdint>
@@ -82,6 +96,37 @@ inline Layout make_layout(bool mx, int64_t N, int64_t K, bool sc8 = false) {
   L.total = L.irow_off + (sc8 ? L.n_tiles * kTileN * 4 : 0);
   return L;
 }
+
+constexpr int kDualNibBytesPerTC = kTileN * kChunkK / 2;     // 2048
+constexpr int kDualOutBytesPerTC = kTileN * (kChunkK / 8) * 2;  // 1024
+constexpr int kDualScaleBytesPerTC = kTileN * (kChunkK / 32);   // 128
+
+struct DualLayout {
+  int64_t n_tiles = 0, n_chunks = 0;
+  int64_t nib_off = 0, out_off = 0, scale_off = 0, rows_off = 0, total = 0;
+};
+
+inline DualLayout make_dual_layout(int64_t N, int64_t K) {
+  DualLayout L;
+  L.n_tiles = (N + kTileN - 1) / kTileN;
+  L.n_chunks = K / kChunkK;
+  const int64_t tc = L.n_tiles * L.n_chunks;
+  L.nib_off = 0;
+  L.out_off = tc * kDualNibBytesPerTC;
+  L.scale_off = L.out_off + tc * kDualOutBytesPerTC;
+  L.rows_off = L.scale_off + tc * kDualScaleBytesPerTC;
+  L.total = L.rows_off + L.n_tiles * kTileN * 4;
+  return L;
+}
+inline int dual_nib_byte(int k, int r) {  // k in 0..127 within the chunk
+  const int s = k >> 6, h = (k >> 5) & 1;
+  return ((s * 2 + h) * 32 + r) * 16 + ((k & 31) >> 1);
+}
+inline int dual_out_halfword(int g, int r) {
+  const int u = g >> 2, h = (g >> 1) & 1, i = g & 1;
+  return ((u * 2 + h) * 32 + r) * 2 + i;
+}
+inline int dual_scale_byte(int b, int r) { return b * 32 + r; }
 
 // Word index of group g (0..15 within the chunk) of tile row r.
 inline int int_word_index(int g, int r) {

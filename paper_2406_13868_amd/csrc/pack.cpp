@@ -208,8 +208,9 @@ sdq_status int_inlier_scales(const Cfg& c, const float* w, int64_t K, const uint
 // kept positions.  Same scale rules as the final inlier quantization.
 sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* keep8, float* D,
                         float* V, uint16_t* SC) {
-  const int qv = c.mx ? 32 : 16;
-  if (!c.mx) {
+  const bool mx_in = c.mx || c.dual;  // fp4 inliers with e8m0 scales per 32 K
+  const int qv = mx_in ? 32 : 16;
+  if (!mx_in) {
     float row;
     const sdq_status st = int_inlier_scales(c, w, K, keep8, V, SC, &row);
     if (st != SDQ_OK) return st;
@@ -223,7 +224,7 @@ sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* 
     for (int kk = 0; kk < qv; ++kk) {
       const int64_t k = k0 + kk;
       float deq = 0.f;
-      if (c.mx) {
+      if (mx_in) {
         if (a > 0.f) {
           const int E = clamp_int(floor_log2f(a) - 2, -127, 127);
           const uint8_t q = enc_e2m1(std::ldexp(double(w[k]), -E));
@@ -313,7 +314,8 @@ struct RowSink {
   uint8_t* pos_i; uint8_t* code_i; void* scale_i; float* scale_i_row;
   // kernel layout output (may be null)
   uint8_t* blob;
-  const Layout* lay;
+  const Layout* lay;        // int and mx families
+  const DualLayout* dlay;   // dual family
 };
 
 // Packs row n with the per-thread scratch sc.
@@ -339,7 +341,7 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
 
   // ---- inlier block scales of the row (INT family)
   float s_irow = 0.f;
-  if (!c.mx) {
+  if (!c.mx && !c.dual) {
     const sdq_status st = int_inlier_scales(c, w, K, im8, sc.V.data(), sc.SC.data(), &s_irow);
     if (st != SDQ_OK) return st;
     if (out.scale_i_row) out.scale_i_row[n] = s_irow;
@@ -383,6 +385,30 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
         sb[mx_scale_byte(bb, int(r), 0)] = c.n_o ? uint8_t(Eo + 127) : 0;
         sb[mx_scale_byte(bb, int(r), 1)] = uint8_t(Ei + 127);
       }
+    } else if (c.dual) {
+      // fp4 inliers with an e8m0 scale per 32 K (the MX rule)
+      float ai = 0.f;
+      for (int gg = 0; gg < 4; ++gg)
+        for (int p = 0; p < 8; ++p)
+          if ((im[gg] >> p) & 1u) ai = std::fmax(ai, std::fabs(w[k0 + 8 * gg + p]));
+      const int Ei = ai > 0.f ? clamp_int(floor_log2f(ai) - 2, -127, 127) : -127;
+      for (int gg = 0; gg < 4; ++gg)
+        for (int p = 0; p < 8; ++p)
+          if (((im[gg] >> p) & 1u) && ai > 0.f)
+            icode[8 * gg + p] = enc_e2m1(std::ldexp(double(w[k0 + 8 * gg + p]), -Ei));
+      const int64_t b = k0 / 32;
+      if (out.scale_i) static_cast<uint8_t*>(out.scale_i)[n * (K / 32) + b] = uint8_t(Ei + 127);
+      if (out.blob) {
+        const int64_t ch = k0 / kChunkK;
+        out.blob[out.dlay->scale_off + (t * out.dlay->n_chunks + ch) * kDualScaleBytesPerTC +
+                 dual_scale_byte(int((k0 % kChunkK) / 32), int(r))] = uint8_t(Ei + 127);
+      }
+      // int8 outliers with the row scale
+      if (c.n_o && s_o != 0.f)
+        for (int gg = 0; gg < 4; ++gg)
+          for (int p = 0; p < 8; ++p)
+            if ((om[gg] >> p) & 1u)
+              ocode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(w[k0 + 8 * gg + p] / s_o)), -127, 127)));
     } else {
       for (int hb = 0; hb < 2; ++hb) {  // two 16-K blocks
         const int64_t kb = k0 / 16 + hb;
@@ -446,7 +472,22 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
     }
 
     // ---- kernel layout
-    if (out.blob) {
+    if (out.blob && c.dual) {
+      const int64_t ch = k0 / kChunkK;
+      const int64_t tc = t * out.dlay->n_chunks + ch;
+      uint8_t* nib = out.blob + out.dlay->nib_off + tc * kDualNibBytesPerTC;
+      uint16_t* hw = reinterpret_cast<uint16_t*>(out.blob + out.dlay->out_off + tc * kDualOutBytesPerTC);
+      for (int kk = 0; kk < 32; ++kk) {
+        const int k = int(k0 % kChunkK) + kk;
+        nib[dual_nib_byte(k, int(r))] |= uint8_t((icode[kk] & 0xFu) << ((k & 1) * 4));
+      }
+      for (int gg = 0; gg < 4; ++gg) {
+        uint16_t v = 0;
+        for (int p = 0; p < 8; ++p)
+          if ((om[gg] >> p) & 1u) v = uint16_t(p | (ocode[8 * gg + p] << 8));
+        hw[dual_out_halfword(int((k0 % kChunkK) / 8) + gg, int(r))] = v;
+      }
+    } else if (out.blob) {
       const int64_t ch = k0 / kChunkK;
       uint32_t* words = reinterpret_cast<uint32_t*>(out.blob + out.lay->words_off) +
                         (t * out.lay->n_chunks + ch) * kWordsPerTC;
@@ -476,7 +517,9 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
       }
     }
   }
-  if (out.blob && !c.mx) {
+  if (out.blob && c.dual) {
+    reinterpret_cast<float*>(out.blob + out.dlay->rows_off)[n] = s_o;
+  } else if (out.blob && !c.mx) {
     float* rows = reinterpret_cast<float*>(out.blob + out.lay->rows_off);
     rows[n] = s_o;
     if (c.sc8) reinterpret_cast<float*>(out.blob + out.lay->irow_off)[n] = s_irow;
@@ -535,7 +578,7 @@ extern "C" sdq_status sdq_pack_size(const sdq_config* cfg, int64_t N, int64_t K,
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (!bytes) return SDQ_ERR_NULL;
-  *bytes = size_t(layout_for(c, N, K).total);
+  *bytes = size_t(c.dual ? make_dual_layout(N, K).total : layout_for(c, N, K).total);
   return SDQ_OK;
 }
 
@@ -552,6 +595,9 @@ extern "C" sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_
   if (c.mx) {
     bits += (K / 32) * 8;               // inlier e8m0
     if (c.n_o) bits += (K / 32) * 8;    // outlier e8m0
+  } else if (c.dual) {
+    bits += (K / 32) * 8;               // inlier e8m0
+    if (c.n_o) bits += 32;              // outlier fp32 per row
   } else {
     bits += (K / 16) * (c.sc8 ? 8 : 16);  // inlier fp16, or e4m3 ...
     if (c.sc8) bits += 32;                // ... with an fp32 (power of two) per row
@@ -568,11 +614,13 @@ extern "C" sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N,
   if (s != SDQ_OK) return s;
   if (!W || !packed) return SDQ_ERR_NULL;
   const Layout lay = layout_for(c, N, K);
-  if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  const DualLayout dlay = make_dual_layout(N, K);
+  const size_t total = size_t(c.dual ? dlay.total : lay.total);
+  if (bytes < total) return SDQ_ERR_BUFFER_TOO_SMALL;
   if ((s = check_act_norm(c, act_norm, K)) != SDQ_OK) return s;
-  std::memset(packed, 0, size_t(lay.total));
+  std::memset(packed, 0, total);
   RowSink sink{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-               static_cast<uint8_t*>(packed), &lay};
+               static_cast<uint8_t*>(packed), &lay, &dlay};
   return run_rows(c, W, N, K, act_norm, sink, n_threads);
 }
 
@@ -592,7 +640,7 @@ extern "C" sdq_status sdq_pack_logical(const sdq_config* cfg, const float* W, in
   }
   if (scale_i_row && !c.sc8) std::memset(scale_i_row, 0, size_t(N) * 4);
   RowSink sink{pos_o, code_o, scale_o, pos_i, code_i, scale_i, c.sc8 ? scale_i_row : nullptr,
-               nullptr, nullptr};
+               nullptr, nullptr, nullptr};
   return run_rows(c, W, N, K, act_norm, sink, n_threads);
 }
 
@@ -605,8 +653,36 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
   if (s != SDQ_OK) return s;
   if (!packed || !code_o_dense || !code_i_dense || !scale_o || !scale_i) return SDQ_ERR_NULL;
   const Layout lay = layout_for(c, N, K);
-  if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
   const uint8_t* blob = static_cast<const uint8_t*>(packed);
+  if (c.dual) {
+    const DualLayout dl = make_dual_layout(N, K);
+    if (bytes < size_t(dl.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
+    for (int64_t n = 0; n < N; ++n) {
+      const int64_t t = n / kTileN;
+      const int r = int(n % kTileN);
+      for (int64_t ch = 0; ch < dl.n_chunks; ++ch) {
+        const int64_t tc = t * dl.n_chunks + ch;
+        const uint8_t* nib = blob + dl.nib_off + tc * kDualNibBytesPerTC;
+        const uint16_t* hw = reinterpret_cast<const uint16_t*>(blob + dl.out_off + tc * kDualOutBytesPerTC);
+        for (int k = 0; k < kChunkK; ++k) {
+          const int64_t kk = n * K + ch * kChunkK + k;
+          code_i_dense[kk] = uint8_t((nib[dual_nib_byte(k, r)] >> ((k & 1) * 4)) & 0xFu);
+          code_o_dense[kk] = 0;
+        }
+        for (int g = 0; g < 16; ++g) {
+          const uint16_t v = hw[dual_out_halfword(g, r)];
+          if (v >> 8) code_o_dense[n * K + ch * kChunkK + g * 8 + (v & 7)] = uint8_t(v >> 8);
+        }
+        for (int b = 0; b < 4; ++b)
+          static_cast<uint8_t*>(scale_i)[n * (K / 32) + ch * 4 + b] =
+              blob[dl.scale_off + tc * kDualScaleBytesPerTC + dual_scale_byte(b, r)];
+      }
+      static_cast<float*>(scale_o)[n] = reinterpret_cast<const float*>(blob + dl.rows_off)[n];
+      if (scale_i_row) scale_i_row[n] = 0.f;
+    }
+    return SDQ_OK;
+  }
+  if (bytes < size_t(lay.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
   std::memset(code_o_dense, 0, size_t(N * K));
   std::memset(code_i_dense, 0, size_t(N * K));
   for (int64_t n = 0; n < N; ++n) {

@@ -8,7 +8,8 @@
 namespace sdq {
 
 struct Cfg {
-  bool mx;
+  bool mx;    // MX family (fp8 outliers and fp4 inliers, e8m0 scales, fp8 activations)
+  bool dual;  // dual family (int8 outliers, fp4 inliers, int8 + fp4 activations)
   int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric, decomp, order;
   bool sc8;  // INT family with two-level e4m3 inlier scales
 };
@@ -24,8 +25,9 @@ inline bool needs_act_norm(const Cfg& c) {
 // Validates a configuration and shape; fills `out` on success.
 inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* out) {
   if (!c) return SDQ_ERR_NULL;
-  if (c->family != SDQ_FAMILY_INT && c->family != SDQ_FAMILY_MX) return SDQ_ERR_CONFIG;
-  const bool mx = c->family == SDQ_FAMILY_MX;
+  if (c->family != SDQ_FAMILY_INT && c->family != SDQ_FAMILY_MX && c->family != SDQ_FAMILY_DUAL)
+    return SDQ_ERR_CONFIG;
+  const bool mx = c->family == SDQ_FAMILY_MX, dual = c->family == SDQ_FAMILY_DUAL;
   if (c->n_o < 0 || c->n_i < 0 || c->m_o <= 0 || c->m_i <= 0) return SDQ_ERR_CONFIG;
   if (c->n_o > c->m_o || c->n_i > c->m_i || c->n_i == 0) return SDQ_ERR_CONFIG;
   if (c->metric != SDQ_METRIC_MAGNITUDE && c->metric != SDQ_METRIC_PRODUCT) return SDQ_ERR_CONFIG;
@@ -38,20 +40,30 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   if (mx) {
     if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
       return SDQ_ERR_CONFIG;
+  } else if (dual) {
+    if (c->fmt_o != SDQ_FMT_INT8 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_INT8)
+      return SDQ_ERR_CONFIG;
   } else {
     if ((c->fmt_o != SDQ_FMT_E4M3 && c->fmt_o != SDQ_FMT_INT8) || c->fmt_i != SDQ_FMT_INT4 ||
         c->fmt_a != SDQ_FMT_INT8)
       return SDQ_ERR_CONFIG;
   }
   // What the kernels implement.
-  if (c->m_i != 8 || c->n_i > 3) return SDQ_ERR_UNSUPPORTED;
-  if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
+  if (c->m_i != 8) return SDQ_ERR_UNSUPPORTED;
+  if (dual) {
+    // dense fp4 inliers: any n_i with n_o + n_i <= 8; 1:8 outliers
+    if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8) || c->n_o + c->n_i > 8) return SDQ_ERR_UNSUPPORTED;
+  } else {
+    if (c->n_i > 3) return SDQ_ERR_UNSUPPORTED;
+    if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
+  }
   // upper bounds keep every per-block offset of the kernels in 32 bits
   if (N <= 0 || K <= 0 || K % 128 != 0 || N > (int64_t(1) << 21) || K > (int64_t(1) << 22))
     return SDQ_ERR_SHAPE;
   if (N > (int64_t(1) << 31) || K > (int64_t(1) << 24)) return SDQ_ERR_SHAPE;
   if (out) {
     out->mx = mx;
+    out->dual = dual;
     out->n_o = c->n_o;
     out->m_o = c->n_o ? c->m_o : 8;
     out->fmt_o = c->fmt_o;

@@ -348,3 +348,53 @@ def test_e4m3_scales_sizes_and_validation():
     assert ps16.value - ps8.value == N * (K // 16) - N * 4
     mx = sdq.Config("mx", 1, 8, "e4m3", 2, 8, "e2m1", "e4m3", sfmt_i="e4m3").c()
     assert L.sdq_pack_size(C.byref(mx), 32, 128, C.byref(ps8)) == -3   # INT family only
+
+
+# ---- the dual family (Section 5.1's int8 A_o / fp4 A_i configuration)
+@pytest.mark.parametrize("n_o,n_i,metric,decomp", [(1, 6, "magnitude", "same"), (1, 6, "product", "error"),
+                                                   (1, 7, "magnitude", "same"), (1, 3, "product", "same"),
+                                                   (0, 8, "magnitude", "same"), (0, 5, "magnitude", "same")])
+def test_dual_pack_matches_oracle(n_o, n_i, metric, decomp):
+    N, K = 40, 384
+    W = synth.make_w(2, 0, N, K)
+    W[4, :] = 0.0
+    W[6, :40] *= np.float32(1e-6)
+    an = np.exp(np.random.default_rng(1).standard_normal(K)).astype(np.float32)
+    c = sdq.Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8", metric, decomp)
+    co = S.Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8+e2m1", metric, decomp)
+    Lg, Lo = sdq.pack_logical(W, c, act_norm=an), S.pack_logical(W, co, act_norm=an)
+    assert np.array_equal(Lg["pos_i"], Lo["pos_i"].astype(np.uint8))
+    assert np.array_equal(Lg["code_i"], Lo["code_i"])
+    assert np.array_equal(Lg["scale_i"], Lo["scale_i"])
+    if n_o:
+        assert np.array_equal(Lg["pos_o"], Lo["pos_o"].astype(np.uint8))
+        assert np.array_equal(Lg["code_o"], Lo["code_o"])
+        assert np.array_equal(Lg["scale_o"].view(np.uint32), Lo["scale_o"].view(np.uint32))
+    U = sdq.unpack_dense(sdq.pack(W, c, act_norm=an), c, N, K)
+    assert np.array_equal(U["code_i_dense"], Lo["code_i_dense"])
+    assert np.array_equal(U["code_o_dense"], Lo["code_o_dense"])
+    assert np.array_equal(U["scale_i"], Lo["scale_i"])
+
+
+def test_dual_sizes_and_validation():
+    L = _lib.lib()
+    n = C.c_size_t()
+    dual = sdq.Config.dual_family()
+    N, K = 4096, 4096
+    assert L.sdq_pack_size(C.byref(dual.c()), N, K, C.byref(n)) == 0
+    # dense fp4 nibbles (4 b/w), outlier half-words (2 b/w), e8m0 per 32 (0.25 b/w), fp32 per row
+    assert n.value == N * K // 2 + N * K // 4 + N * K // 32 + N * 4
+    assert L.sdq_logical_bytes(C.byref(dual.c()), N, K, C.byref(n)) == 0
+    # 1:8 int8 (8+3 bits per 8) + 6:8 fp4 (6 x (4+3) per 8) + e8m0 per 32 + fp32 per row
+    assert n.value == (N * (K // 8 * 11 + K // 8 * 42 + K // 32 * 8 + 32) + 7) // 8
+    assert L.sdq_pack_size(C.byref(sdq.Config("dual", 1, 16, "int8", 6, 8, "e2m1", "int8").c()), 32, 128,
+                           C.byref(n)) == -6      # 1:16 outliers not built for this family
+    assert L.sdq_pack_size(C.byref(sdq.Config("dual", 1, 8, "e4m3", 6, 8, "e2m1", "int8").c()), 32, 128,
+                           C.byref(n)) == -3
+    cfg = dual.c()
+    assert L.sdq_gemm(C.byref(cfg), C.c_void_p(16), C.c_void_p(16), 1, C.c_void_p(16), 32, 128,
+                      C.c_void_p(16), None) == -6
+    assert L.sdq_gemm_dual(C.byref(sdq.Config.int_family().c()), None, None, None, None, 1, None, 32, 128,
+                           None, None) == -3
+    assert L.sdq_gemm_dual(C.byref(cfg), None, None, None, None, 1, None, 32, 128, None, None) == -1
+    assert L.sdq_gemm_dual(C.byref(cfg), None, None, None, None, 0, None, 32, 128, None, None) == 0
