@@ -41,7 +41,21 @@ WORKLOADS = {
     "llama7b-mlp-prefill": (3, [0, 1, 2], 2048),
     "opt6.7b-ffn-decode": (4, [0, 1], 64),
     "tiny": (1, [0], 16),
+    # the paper's SDQ-W7:8-1:8int8-6:8fp4 (dual activations) on the LLaMA-7B block
+    "llama7b-block-dual": (6, [0, 1, 2, 3, 4, 5, 6], 4096),
 }
+
+# Dense MFMA peaks by operand type (MI355X, TFLOP/s or TOP/s).
+MFMA_PEAK = {"fp8": 5033.0, "f16": 2516.6, "fp4": 10066.0, "int8": 5033.0}
+
+
+def dual_mfma_peak() -> float:
+    """Dense-equivalent peak of the dual GEMM's instruction mix: per 64 K of a
+    32x32 tile one fp4 x fp4 instruction (32*32*64 products at the fp4 rate)
+    and two int8 ones (32*32*32 each at the int8 rate); the dense-equivalent
+    work is 2*32*32*64."""
+    t = 2 * 32 * 32 * 64 / MFMA_PEAK["fp4"] + 2 * (2 * 32 * 32 * 32) / MFMA_PEAK["int8"]
+    return 2 * 32 * 32 * 64 / t
 
 
 def parse():
@@ -52,7 +66,8 @@ def parse():
     p.add_argument("--workload", default="llama7b-attn-decode",
                    help="|".join(WORKLOADS) + "|sweep (with --layer/--M/--fmt)")
     p.add_argument("--layer", type=int, default=0, help="block-sweep layer index (0..6)")
-    p.add_argument("--M", type=int, default=1, help="block-sweep token count")
+    p.add_argument("--M", type=int, default=0,
+                   help="token count: block sweep (default 1) or the dual block workload (default 4096)")
     p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
     p.add_argument("--inlier-scale", default="", choices=["", "e4m3"],
                    help="INT family: two-level e4m3 inlier scales instead of the workload's fp16 "
@@ -124,12 +139,16 @@ def main():
         wid = 5
         fmt = synth.WORKLOADS[5].formats[a.fmt]
         layers = [a.layer]
-        M = a.M
+        M = a.M or 1
         wl_name = f"llama7b block sweep {synth.WORKLOADS[5].layers[a.layer].name} M={M} {fmt.label}"
     else:
         wid, layers, M = WORKLOADS[a.workload]
+        if a.M and wid == 6:
+            M = a.M
         fmt = synth.WORKLOADS[wid].formats[0]
         wl_name = synth.WORKLOADS[wid].name
+        if wid == 6:
+            wl_name += f" M={M}"
     W_def = synth.WORKLOADS[wid]
     cfg = sdq.Config.of(fmt)
     if a.inlier_scale:
@@ -164,31 +183,51 @@ def main():
     Xd = [[torch.from_numpy(X).to(dev).to(x_dtype) for X in Xs] for _ in range(R)]
     Xq = [[torch.empty((M, L.K), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)]
     sa = [[torch.empty((M,), dtype=torch.float32, device=dev) for _ in Ls] for _ in range(R)]
+    dual = cfg.family == "dual"
+    # the dual family's fp4 activations and their e8m0 scales
+    Xi = [[torch.empty((M, L.K // 2), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)] if dual else None
+    Ea = [[torch.empty((M, L.K // 32), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)] if dual else None
     Y = [[torch.empty((M, L.N), dtype=torch.float32, device=dev) for L in Ls] for _ in range(R)]
     # GEMM workspace (the two-pass path for many MX tokens), one for all layers:
     # the calls are ordered on one stream
-    ws_bytes = max(sdq.gemm_workspace_size(cfg, M, L.N, L.K) for L in Ls)
+    ws_bytes = 0 if dual else max(sdq.gemm_workspace_size(cfg, M, L.N, L.K) for L in Ls)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
     stream = torch.cuda.current_stream()
+    def quant(r, j):
+        if dual:
+            sdq.quantize_act_dual(Xd[r][j], cfg, out=(Xq[r][j], sa[r][j], Xi[r][j], Ea[r][j]))
+        else:
+            sdq.quantize_act(Xd[r][j], cfg, out=Xq[r][j], scales=sa[r][j])
+
     for r in range(R):  # every rotated copy's Xq/s_a holds real codes before any GEMM-only launch
         for j in range(len(Ls)):
-            sdq.quantize_act(Xd[r][j], cfg, out=Xq[r][j], scales=sa[r][j])
+            quant(r, j)
     torch.cuda.synchronize()
+
+    def gemm_one(r, j, L):
+        if dual:
+            sdq.gemm_dual(Xq[r][j], sa[r][j], Xi[r][j], Ea[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j])
+        else:
+            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], workspace=ws)
 
     def step(i):
         r = i % R
         for j, L in enumerate(Ls):
-            sdq.linear(Xd[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], xq=Xq[r][j],
-                       scales=sa[r][j], workspace=ws)
+            if dual:  # quantize into this copy's buffers, then multiply
+                quant(r, j)
+                gemm_one(r, j, L)
+            else:
+                sdq.linear(Xd[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], xq=Xq[r][j],
+                           scales=sa[r][j], workspace=ws)
 
     def gemms(i):
         r = i % R
         for j, L in enumerate(Ls):
-            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], workspace=ws)
+            gemm_one(r, j, L)
 
     def gemms_hot(i):
         for j, L in enumerate(Ls):
-            sdq.gemm(Xq[0][j], sa[0][j], blobs[0][j], L.N, L.K, cfg, out=Y[0][j], workspace=ws)
+            gemm_one(0, j, L)
 
     def capture(fn, n, start):
         """HIP graph of n calls of fn (launch-bound loops replay without host gaps)."""
@@ -254,15 +293,15 @@ def main():
 
     flops = sum(2.0 * M * L.N * L.K for L in Ls)
     alg_bytes = logical + sum(M * L.K + 4 * M + 4 * M * L.N for L in Ls)
-    paths = sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
-    hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family == "mx" and M < 256)
+    paths = [] if dual else sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
+    hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family != "int" and M < 256)
     if hbm_bound:
         achieved = alg_bytes / (gemm_us * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
         achieved = flops / (gemm_us * 1e-6) / 1e12
-        peak = MFMA_PEAK_TFLOPS["fp8" if cfg.family == "mx" else "f16"]
+        peak = round(dual_mfma_peak(), 1) if dual else MFMA_PEAK_TFLOPS["fp8" if cfg.family == "mx" else "f16"]
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
     tkey = a.workload if a.workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
@@ -292,10 +331,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8" if cfg.family == "int" else "fp8",
+        "dtype": {"int": "int8", "mx": "fp8", "dual": "int8+fp4"}[cfg.family],
         "data": "synthetic (seeded generators shaped like the named layers; no weights or datasets)",
         "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
-                   "formats": fmt.label, "gemm_path": ["decode", "mfma", "dense (two passes)"][paths[-1] - 1] if paths else None,
+                   "formats": fmt.label,
+                   "gemm_path": "dual mfma" if dual else ["decode", "mfma", "dense (two passes)"][paths[-1] - 1],
                    "parallelism": "none (one GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,
@@ -392,8 +432,11 @@ def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
     while t < seconds or reps == 0:
         t0 = time.perf_counter()
         for X, Lg in zip(Xs, packs):
-            Xq, s_a = S.quantize_act(X[:ms], cfg_o)
-            S.gemm_fp64(Xq, s_a, Lg)
+            if cfg_o.family == "dual":
+                S.gemm_fp64_dual(*S.quantize_act_dual(X[:ms]), Lg)
+            else:
+                Xq, s_a = S.quantize_act(X[:ms], cfg_o)
+                S.gemm_fp64(Xq, s_a, Lg)
             flops += 2.0 * ms * Lg["N"] * Lg["K"]
         t += time.perf_counter() - t0
         reps += 1

@@ -195,9 +195,10 @@ def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
     return Xq, s_a
 
 
-def quantize_act_dual(X, cfg: Config, stream=None):
+def quantize_act_dual(X, cfg: Config, out=None, stream=None):
     """The dual family's activations on the GPU: returns (Xq_o uint8 [M, K],
-    s_a_o f32 [M], Xq_i uint8 [M, K/2] fp4 nibbles, e_a_i uint8 [M, K/32] e8m0)."""
+    s_a_o f32 [M], Xq_i uint8 [M, K/2] fp4 nibbles, e_a_i uint8 [M, K/32] e8m0),
+    written into `out` (a tuple of those four tensors) when given."""
     import torch
     M, K = X.shape
     if X.dtype == torch.float32:
@@ -207,10 +208,13 @@ def quantize_act_dual(X, cfg: Config, stream=None):
     else:
         raise ValueError("X must be float32 or bfloat16")
     dev = X.device
-    Xo = torch.empty((M, K), dtype=torch.uint8, device=dev)
-    s_a = torch.empty((M,), dtype=torch.float32, device=dev)
-    Xi = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
-    Ea = torch.empty((M, K // 32), dtype=torch.uint8, device=dev)
+    if out is not None:
+        Xo, s_a, Xi, Ea = out
+    else:
+        Xo = torch.empty((M, K), dtype=torch.uint8, device=dev)
+        s_a = torch.empty((M,), dtype=torch.float32, device=dev)
+        Xi = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        Ea = torch.empty((M, K // 32), dtype=torch.uint8, device=dev)
     _lib.check(_lib.lib().sdq_quantize_act_dual(C.byref(cfg.c()), _dev(X, "X"), dt, M, K, _dev(Xo, "Xq_o"),
                                                 _dev(s_a, "s_a_o"), _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"),
                                                 _stream(stream)), "sdq_quantize_act_dual")

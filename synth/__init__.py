@@ -29,6 +29,7 @@ __all__ = [
     "Workload",
     "WORKLOADS",
     "INT_1x8_E4M3_3x8",
+    "dual_formats",
     "rng_for",
     "bf16_round",
     "make_x",
@@ -48,9 +49,11 @@ class Formats:
     per-row fp32 scale, inliers int4 with one fp16 scale per 16 dense K.
     family "mx": fp8-e4m3 per-token activations, outliers fp8-e4m3 and inliers
     fp4-e2m1, each branch with one e8m0 scale per 32 dense K.
+    family "dual": int8 outliers (per-row fp32 scale) against int8 per-token
+    activations, fp4-e2m1 inliers (e8m0 per 32) against MXFP4 activations.
     """
 
-    family: str  # "int" | "mx"
+    family: str  # "int" | "mx" | "dual"
     n_o: int
     m_o: int
     fmt_o: str  # "e4m3" | "int8"
@@ -71,6 +74,10 @@ def int_formats(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, m_i=8) -> Formats:
 
 def mx_formats(n_o=1, m_o=8, n_i=2, m_i=8) -> Formats:
     return Formats("mx", n_o, m_o, "e4m3", n_i, m_i, "e2m1", "e4m3")
+
+
+def dual_formats(n_o=1, n_i=6) -> Formats:
+    return Formats("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8")
 
 
 INT_1x8_E4M3_3x8 = int_formats()
@@ -128,6 +135,9 @@ WORKLOADS: Dict[int, Workload] = {
                 tuple(int_formats(1, mo, "e4m3", ni, 8) for mo in (8, 16) for ni in (2, 3))
                 + tuple(mx_formats(1, mo, ni, 8) for mo in (8, 16) for ni in (2, 3)),
                 "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
+    # The paper's headline SDQ-W7:8-1:8int8-6:8fp4 on the LLaMA-7B block shapes.
+    6: Workload(6, "llama7b block, dual 1:8 int8 + 6:8 fp4", LLAMA7B_LAYERS, (1, 16, 256, 4096),
+                (dual_formats(1, 6),), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
 }
 
 
