@@ -18,10 +18,10 @@
 // The branches accumulate apart (fp32 and int32) and meet in the epilogue.
 //
 // A workgroup of four waves covers four 32-row tiles of W and 32*MS tokens;
-// each wave owns one tile and all MS token sub-tiles.  Activations are read
-// straight from L2 into registers (the four waves of a workgroup read the
-// same lines, so the L1 cache serves most of them); each wave keeps two
-// 128-K chunks of loads in flight.
+// each wave owns one tile and all MS token sub-tiles.  The workgroup stages
+// each 128-K chunk of both activation tensors in LDS once (double-buffered,
+// one barrier per chunk) for its four waves; each wave streams its tile's
+// weights into registers one chunk ahead.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -66,11 +66,21 @@ __device__ __forceinline__ v4i outlier_bytes(uint32_t hw2) {
   return r;
 }
 
+// LDS rows of one 128-K chunk of activations, padded so that the 16-byte
+// fragment reads of 8 consecutive rows fall on distinct banks.
+constexpr int kRowO = kChunkK + 16;      // int8 codes of A_o: 144 bytes
+constexpr int kRowI = kChunkK / 2 + 16;  // fp4 codes of A_i: 80 bytes
+
 template <int MS>
-__global__ __launch_bounds__(kDThreads, 1) void dual_mfma_kernel(DualArgs a) {
+__global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(DualArgs a) {
   constexpr int BM = 32 * MS;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // one chunk of the workgroup's activations, two buffers
+  __shared__ __align__(16) uint8_t xo_s[2][BM * kRowO];
+  __shared__ __align__(16) uint8_t xi_s[2][BM * kRowI];
+  __shared__ __align__(16) uint32_t ea_s[2][BM];  // the four e8m0 bytes of a row's chunk
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, h = lane >> 5;
   const int m0 = blockIdx.y * BM;
   const int t_raw = blockIdx.x * kDWaves + wave;
@@ -92,15 +102,49 @@ __global__ __launch_bounds__(kDThreads, 1) void dual_mfma_kernel(DualArgs a) {
   const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.blob + a.scale_off + size_t(tile) * KC * kDualScaleBytesPerTC,
                                                 uint32_t(KC) * kDualScaleBytesPerTC);
 
-  struct Stage {
-    v4i bi[2];        // fp4 inlier fragments of the two 64-K steps
-    int sb[2];        // their e8m0 scales (block 2s + h of row col)
-    uint32_t hw[4];   // outlier half-word pairs of the four 32-K steps
-    v4i ai[MS][2];    // fp4 activations
-    int sa[MS][2];    // their e8m0 scales
-    v4i ao[MS][4];    // int8 activations
+  // ---- activation staging: thread tid moves 16-byte pieces tid + 256 i of
+  //      the chunk (8 per row of A_o, 4 per row of A_i) and, below BM, the
+  //      four scale bytes of row tid
+  constexpr int kPo = BM * 8 / kDThreads;                       // BM * 8 >= 256
+  constexpr int kPi = (BM * 4 + kDThreads - 1) / kDThreads;      // 128 pieces at BM = 32
+  struct XRegs { v4i o[kPo]; v4i i[kPi]; uint32_t e; };
+  auto load_x = [&](int c, XRegs& x) __attribute__((always_inline)) {
+    const uint32_t cs = uint32_t(c);
+#pragma unroll
+    for (int j = 0; j < kPo; ++j) {
+      const int p = tid + j * kDThreads;
+      x.o[j] = ld16(xo, uint32_t(p >> 3) * K + uint32_t(p & 7) * 16, cs * kChunkK);
+    }
+#pragma unroll
+    for (int j = 0; j < kPi; ++j) {
+      const int p = tid + j * kDThreads;
+      if (BM * 4 % kDThreads == 0 || p < BM * 4)
+        x.i[j] = ld16(xi, uint32_t(p >> 2) * (K / 2) + uint32_t(p & 3) * 16, cs * (kChunkK / 2));
+    }
+    if (tid < BM) x.e = __builtin_amdgcn_raw_buffer_load_b32(ea, uint32_t(tid) * (K / 32), cs * 4, 0);
   };
-  auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
+  auto store_x = [&](int buf, const XRegs& x) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < kPo; ++j) {
+      const int p = tid + j * kDThreads;
+      *reinterpret_cast<v4i*>(&xo_s[buf][(p >> 3) * kRowO + (p & 7) * 16]) = x.o[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kPi; ++j) {
+      const int p = tid + j * kDThreads;
+      if (BM * 4 % kDThreads == 0 || p < BM * 4)
+        *reinterpret_cast<v4i*>(&xi_s[buf][(p >> 2) * kRowI + (p & 3) * 16]) = x.i[j];
+    }
+    if (tid < BM) ea_s[buf][tid] = x.e;
+  };
+
+  // ---- the wave's weight stream, one chunk per stage
+  struct BRegs {
+    v4i bi[2];       // fp4 inlier fragments of the two 64-K steps
+    int sb[2];       // their e8m0 scales (block 2s + h of row col)
+    uint32_t hw[4];  // outlier half-word pairs of the four 32-K steps
+  };
+  auto load_b = [&](int c, BRegs& st) __attribute__((always_inline)) {
     const uint32_t cs = uint32_t(c);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -110,17 +154,6 @@ __global__ __launch_bounds__(kDThreads, 1) void dual_mfma_kernel(DualArgs a) {
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       st.hw[u] = __builtin_amdgcn_raw_buffer_load_b32(wo, uint32_t(u * 64 + lane) * 4u, cs * kDualOutBytesPerTC, 0);
-#pragma unroll
-    for (int ms = 0; ms < MS; ++ms) {
-      const uint32_t row = uint32_t(ms * 32 + col);
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        st.ai[ms][s] = ld16(xi, row * (K / 2) + uint32_t(s * 32 + h * 16), cs * (kChunkK / 2));
-        st.sa[ms][s] = ld8(ea, row * (K / 32) + uint32_t(2 * s + h), cs * (kChunkK / 32));
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) st.ao[ms][u] = ld16(xo, row * K + uint32_t(u * 32 + h * 16), cs * kChunkK);
-    }
   };
 
   v16f acc[MS];
@@ -130,39 +163,56 @@ __global__ __launch_bounds__(kDThreads, 1) void dual_mfma_kernel(DualArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { acc[ms][e] = 0.f; acco[ms][e] = 0; }
 
-  auto compute = [&](const Stage& st) __attribute__((always_inline)) {
+  auto compute = [&](int buf, const BRegs& st) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const v8i b = {st.bi[s][0], st.bi[s][1], st.bi[s][2], st.bi[s][3], 0, 0, 0, 0};
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
-        const v8i av = {st.ai[ms][s][0], st.ai[ms][s][1], st.ai[ms][s][2], st.ai[ms][s][3], 0, 0, 0, 0};
+        const int r = ms * 32 + col;
+        const v4i a4 = *reinterpret_cast<const v4i*>(&xi_s[buf][r * kRowI + s * 32 + h * 16]);
+        const int sa = int((ea_s[buf][r] >> (8 * (2 * s + h))) & 0xFFu);
+        const v8i av = {a4[0], a4[1], a4[2], a4[3], 0, 0, 0, 0};
         // fp4 (format 4) on both sides, each lane half with its block's scale
-        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, b, acc[ms], 4, 4, 0, st.sa[ms][s], 0,
-                                                                   st.sb[s]);
+        acc[ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, b, acc[ms], 4, 4, 0, sa, 0, st.sb[s]);
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const v4i bo = outlier_bytes(st.hw[u]);
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms)
-        acco[ms] = __builtin_amdgcn_mfma_i32_32x32x32_i8(st.ao[ms][u], bo, acco[ms], 0, 0, 0);
+      for (int ms = 0; ms < MS; ++ms) {
+        const v4i ao = *reinterpret_cast<const v4i*>(&xo_s[buf][(ms * 32 + col) * kRowO + u * 32 + h * 16]);
+        acco[ms] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ao, bo, acco[ms], 0, 0, 0);
+      }
     }
   };
 
-  // two chunks in flight; loads past the last chunk re-read it (never used)
-  Stage s0, s1;
-  load(0, s0);
-  load(min(1, last), s1);
+  // ---- pipeline: chunk c in LDS buffer c & 1 and weight stage c & 1; the
+  //      activations of chunk c + 1 wait in registers and are stored after
+  //      the products of chunk c.  Loads past the last chunk re-read it.
+  XRegs X;
+  BRegs B0, B1;
+  load_x(0, X);
+  load_b(0, B0);
+  store_x(0, X);
+  load_x(min(1, last), X);
+  load_b(min(1, last), B1);
+  __syncthreads();
   int c = 0;
   for (; c + 1 < KC; c += 2) {  // one exit, so the accumulators stay in place
-    compute(s0);
-    load(min(c + 2, last), s0);
-    compute(s1);
-    load(min(c + 3, last), s1);
+    compute(0, B0);
+    load_b(min(c + 2, last), B0);
+    store_x(1, X);  // chunk c + 1 (buffer 1 was last read before the previous barrier)
+    load_x(min(c + 2, last), X);
+    __syncthreads();
+    compute(1, B1);
+    load_b(min(c + 3, last), B1);
+    store_x(0, X);  // chunk c + 2
+    load_x(min(c + 3, last), X);
+    __syncthreads();
   }
-  if (c < KC) compute(s0);  // a last chunk of even rank
+  if (c < KC) compute(0, B0);  // a last chunk of even rank
 
   if (!tile_ok) return;
   const int n = tile * kTileN + col;
@@ -175,6 +225,123 @@ __global__ __launch_bounds__(kDThreads, 1) void dual_mfma_kernel(DualArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e)
       store_out(yr, a.N, n, ms, e, h, fmaf(rs.v[ms][e], so * float(acco[ms][e]), acc[ms][e]));
+}
+
+// Split-K form for few tokens (M <= 32): one 32-row tile per workgroup, its
+// NW waves take interleaved 128-K chunks (two in flight per wave) and read
+// their activations straight into registers; the wave partials of both
+// accumulators are summed through LDS in a fixed-order tree.  This keeps
+// n_tiles * NW waves streaming weights where the tiled form above would run
+// only n_tiles / 4 workgroups.
+template <int NW>
+__global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
+  __shared__ float red[NW / 2][2][16][64];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, h = lane >> 5;
+  const int m0 = blockIdx.y * 32;
+  const int tile = blockIdx.x;
+  const int KC = a.n_chunks, last = KC - 1;
+  const uint32_t K = uint32_t(a.K);
+
+  const uint32_t rows = uint32_t(min(a.M - m0, 32));
+  const __amdgpu_buffer_rsrc_t xo = buffer_rsrc(a.Xo + size_t(m0) * K, rows * K);
+  const __amdgpu_buffer_rsrc_t xi = buffer_rsrc(a.Xi + size_t(m0) * (K / 2), rows * (K / 2));
+  const __amdgpu_buffer_rsrc_t ea = buffer_rsrc(a.Ea + size_t(m0) * (K / 32), rows * (K / 32));
+  const __amdgpu_buffer_rsrc_t wn =
+      buffer_rsrc(a.blob + size_t(tile) * KC * kDualNibBytesPerTC, uint32_t(KC) * kDualNibBytesPerTC);
+  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(tile) * KC * kDualOutBytesPerTC,
+                                                uint32_t(KC) * kDualOutBytesPerTC);
+  const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.blob + a.scale_off + size_t(tile) * KC * kDualScaleBytesPerTC,
+                                                uint32_t(KC) * kDualScaleBytesPerTC);
+
+  struct Stage {
+    v4i bi[2];
+    int sb[2];
+    uint32_t hw[4];
+    v4i ai[2];
+    uint32_t sa;  // the chunk's four e8m0 bytes of token row col
+    v4i ao[4];
+  };
+  auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
+    const uint32_t cs = uint32_t(c);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      st.bi[s] = ld16(wn, uint32_t(s * 64 + lane) * 16u, cs * kDualNibBytesPerTC);
+      st.sb[s] = ld8(ws, uint32_t(s * 64 + lane), cs * kDualScaleBytesPerTC);
+      st.ai[s] = ld16(xi, uint32_t(col) * (K / 2) + uint32_t(s * 32 + h * 16), cs * (kChunkK / 2));
+    }
+    st.sa = __builtin_amdgcn_raw_buffer_load_b32(ea, uint32_t(col) * (K / 32), cs * 4, 0);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      st.hw[u] = __builtin_amdgcn_raw_buffer_load_b32(wo, uint32_t(u * 64 + lane) * 4u, cs * kDualOutBytesPerTC, 0);
+      st.ao[u] = ld16(xo, uint32_t(col) * K + uint32_t(u * 32 + h * 16), cs * kChunkK);
+    }
+  };
+
+  v16f acc;
+  v16i acco;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) { acc[e] = 0.f; acco[e] = 0; }
+
+  auto compute = [&](const Stage& st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const v8i b = {st.bi[s][0], st.bi[s][1], st.bi[s][2], st.bi[s][3], 0, 0, 0, 0};
+      const v8i av = {st.ai[s][0], st.ai[s][1], st.ai[s][2], st.ai[s][3], 0, 0, 0, 0};
+      const int sa = int((st.sa >> (8 * (2 * s + h))) & 0xFFu);
+      acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, b, acc, 4, 4, 0, sa, 0, st.sb[s]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acco = __builtin_amdgcn_mfma_i32_32x32x32_i8(st.ao[u], outlier_bytes(st.hw[u]), acco, 0, 0, 0);
+  };
+
+  // wave w takes chunks w, w + NW, ...; stage s0 its even-numbered ones and s1
+  // the odd ones, each refilled right after its products; loads past the last
+  // chunk re-read it (never used)
+  Stage s0, s1;
+  load(min(wave, last), s0);
+  load(min(wave + NW, last), s1);
+  int c = wave;
+  for (; c + NW < KC; c += 2 * NW) {  // one exit, so the accumulators stay in place
+    compute(s0);
+    load(min(c + 2 * NW, last), s0);
+    compute(s1);
+    load(min(c + 3 * NW, last), s1);
+  }
+  if (c < KC) compute(s0);
+
+  // ---- tree over the waves: in round r, wave w + 2^r hands its partials to w
+#pragma unroll
+  for (int stride = NW / 2; stride >= 1; stride >>= 1) {
+    if (wave >= stride && wave < 2 * stride) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float x = acc[e];
+        const int y = acco[e];
+        red[wave - stride][0][e][lane] = x;
+        red[wave - stride][1][e][lane] = __int_as_float(y);
+      }
+    }
+    __syncthreads();
+    if (wave < stride) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        acc[e] += red[wave][0][e][lane];
+        acco[e] += __float_as_int(red[wave][1][e][lane]);
+      }
+    }
+    __syncthreads();
+  }
+  if (wave > 0) return;
+  const int n = tile * kTileN + col;
+  if (n >= a.N) return;
+  const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
+  const RowScales<1> rs = load_row_scales<1>(a.s_a, a.M, m0, h);
+  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32);
+#pragma unroll
+  for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, 0, e, h, fmaf(rs.v[0][e], so * float(acco[e]), acc[e]));
 }
 
 template <int MS>
@@ -193,7 +360,11 @@ hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, c
   const DualLayout L = make_dual_layout(N, K);
   const DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
                    L.out_off, L.scale_off, L.rows_off};
-  if (M <= 32) return launch_ms<1>(a, st);
+  if (M <= 32) {
+    const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 31) / 32));
+    hipLaunchKernelGGL((dual_splitk_kernel<4>), grid, dim3(4 * 64), 0, st, a);
+    return hipGetLastError();
+  }
   if (M <= 64) return launch_ms<2>(a, st);
   return launch_ms<4>(a, st);
 }
