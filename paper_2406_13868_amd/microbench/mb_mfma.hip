@@ -36,6 +36,45 @@ __global__ __launch_bounds__(256) void k_f16(float* out, int iters, int seed) {
   for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) s += acc[j][e];
   if (s == 1234.5f) out[threadIdx.x] = s;
 }
+typedef int i4v __attribute__((ext_vector_type(4)));
+typedef int i16v __attribute__((ext_vector_type(16)));
+template <int NACC>
+__global__ __launch_bounds__(256) void k_i8(float* out, int iters, int seed) {
+  i4v a, b;
+  for (int i = 0; i < 4; ++i) { a[i] = seed * (threadIdx.x + i); b[i] = seed ^ (threadIdx.x * 7 + i); }
+  i16v acc[NACC];
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) acc[j][e] = 0;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) acc[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[j], 0, 0, 0);
+  }
+  int s = 0;
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) s += acc[j][e];
+  if (s == 12345) out[threadIdx.x] = float(s);
+}
+// the dual GEMM's mix per 64 K: one scaled fp4 x fp4 and two int8 32x32x32, on NACC
+// accumulator pairs (counted as 3 instructions per pair and iteration)
+template <int NACC>
+__global__ __launch_bounds__(256) void k_dual(float* out, int iters, int seed) {
+  i8v a, b;
+  i4v c, d;
+  for (int i = 0; i < 8; ++i) { a[i] = seed * (threadIdx.x + i); b[i] = seed ^ (threadIdx.x * 7 + i); }
+  for (int i = 0; i < 4; ++i) { c[i] = a[i] + 1; d[i] = b[i] + 3; }
+  f16v acc[NACC];
+  i16v acco[NACC];
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) { acc[j][e] = 0.f; acco[j][e] = 0; }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) {
+      acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc[j], 4, 4, 0, 127, 0, 127);
+      acco[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(c, d, acco[j], 0, 0, 0);
+      acco[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(d, c, acco[j], 0, 0, 0);
+    }
+  }
+  float s = 0.f;
+  for (int j = 0; j < NACC; ++j) for (int e = 0; e < 16; ++e) s += acc[j][e] + float(acco[j][e]);
+  if (s == 1234.5f) out[threadIdx.x] = s;
+}
 int main() {
   float* out; CK(hipMalloc(&out, 1024 * 4));
   hipEvent_t e0, e1; CK(hipEventCreate(&e0)); CK(hipEventCreate(&e1));
@@ -56,6 +95,9 @@ int main() {
     run("scale fp8 x fp8, 8 acc", k_scale<0, 0, 8>, blocks, 8);
     run("f16 32x32x16, 4 acc", k_f16<4>, blocks, 4);
     run("f16 32x32x16, 8 acc", k_f16<8>, blocks, 8);
+    run("i8 32x32x32, 4 acc", k_i8<4>, blocks, 4);
+    run("i8 32x32x32, 8 acc", k_i8<8>, blocks, 8);
+    run("dual mix (fp4 + 2 i8), 4 pairs", k_dual<4>, blocks, 12);
   }
   printf("mb done\n");
   return 0;
