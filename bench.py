@@ -38,6 +38,8 @@ MFMA_PEAK_TFLOPS = {"fp8": 5033.0, "f16": 2516.6}
 WORKLOADS = {
     # name: (workload id, layer indices, M)
     "llama7b-attn-decode": (2, [0], 1),
+    # q, k and v stacked along N, one launch (N = 12288)
+    "llama7b-qkv-decode": (7, [0], 1),
     "llama7b-mlp-prefill": (3, [0, 1, 2], 2048),
     "opt6.7b-ffn-decode": (4, [0, 1], 64),
     "tiny": (1, [0], 16),
@@ -72,6 +74,8 @@ def parse():
     p.add_argument("--inlier-scale", default="", choices=["", "e4m3"],
                    help="INT family: two-level e4m3 inlier scales instead of the workload's fp16 "
                         "(the quantized scale format of the paper's Section 7 study)")
+    p.add_argument("--y-dtype", default="f32", choices=["f32", "bf16"],
+                   help="GEMM output type (bf16: the fp32 result rounded to nearest even)")
     p.add_argument("--rotate-mb", type=float, default=512.0)
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -157,6 +161,10 @@ def main():
             raise SystemExit("--inlier-scale applies to the INT family only")
         cfg = dataclasses.replace(cfg, sfmt_i=a.inlier_scale)
         wl_name += f", {a.inlier_scale} inlier scales (two-level)"
+    if a.y_dtype != "f32":
+        import dataclasses
+        cfg = dataclasses.replace(cfg, y_dtype=a.y_dtype)
+        wl_name += f", {a.y_dtype} output"
 
     # ---------------------------------------------------------------- inputs
     Ls = [W_def.layers[i] for i in layers]
@@ -187,7 +195,7 @@ def main():
     # the dual family's fp4 activations and their e8m0 scales
     Xi = [[torch.empty((M, L.K // 2), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)] if dual else None
     Ea = [[torch.empty((M, L.K // 32), dtype=torch.uint8, device=dev) for L in Ls] for _ in range(R)] if dual else None
-    Y = [[torch.empty((M, L.N), dtype=torch.float32, device=dev) for L in Ls] for _ in range(R)]
+    Y = [[torch.empty((M, L.N), dtype=cfg.y_torch_dtype(), device=dev) for L in Ls] for _ in range(R)]
     # GEMM workspace (the two-pass path for many MX tokens), one for all layers:
     # the calls are ordered on one stream
     ws_bytes = 0 if dual else max(sdq.gemm_workspace_size(cfg, M, L.N, L.K) for L in Ls)
@@ -292,7 +300,8 @@ def main():
         gemm_hot_us = round(gemm_hot_us, 3)
 
     flops = sum(2.0 * M * L.N * L.K for L in Ls)
-    alg_bytes = logical + sum(M * L.K + 4 * M + 4 * M * L.N for L in Ls)
+    y_bytes = 2 if cfg.y_dtype == "bf16" else 4
+    alg_bytes = logical + sum(M * L.K + 4 * M + y_bytes * M * L.N for L in Ls)
     paths = [] if dual else sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
     hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family != "int" and M < 256)
     if hbm_bound:

@@ -13,7 +13,8 @@
  *
  * Conventions shared by every entry point
  *   - W is [N, K] row-major (row n = output feature, K = reduction), X and Xq
- *     are [M, K] row-major, Y is [M, N] row-major fp32.
+ *     are [M, K] row-major, Y is [M, N] row-major, fp32 or (sdq_config.y_dtype)
+ *     bf16.
  *   - N:M groups and scale blocks run along K inside one row of W.
  *   - Every function returns an sdq_status (0 = SDQ_OK, negative = error).
  *     Nothing throws, aborts or prints (unless SDQ_LOG=1 is set, which prints
@@ -112,7 +113,14 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  *           fp16 per 16 K, MX e8m0 per 32 K) or, INT family only,
  *           SDQ_SCALE_E4M3: VS-Quant's two levels, an fp8-e4m3 scale per 16
  *           K times one power-of-two scale 2^E per row, E the smallest with
- *           every vector scale amax/7 of the row <= 448 * 2^E. */
+ *           every vector scale amax/7 of the row <= 448 * 2^E.
+ *   y_dtype element type of the GEMM output Y: SDQ_DTYPE_F32 (0, the
+ *           default) or SDQ_DTYPE_BF16 (half the output bytes).  A bf16
+ *           output is the fp32 output rounded to nearest even, bit for bit,
+ *           with one exception: on SDQ_PATH_DENSE, a wave of outputs whose
+ *           blocks include one that did not merge its inliers rounds its one
+ *           fp32 sum (main products plus those inliers) instead of the fp32
+ *           path's two-step sum.  The packer ignores it. */
 typedef struct {
   int32_t family;
   int32_t n_o, m_o, fmt_o;
@@ -121,6 +129,7 @@ typedef struct {
   int32_t metric;
   int32_t decomp, order;
   int32_t sfmt_i;
+  int32_t y_dtype;
 } sdq_config;
 
 /* Static description of an error code (never NULL). */
@@ -224,10 +233,14 @@ sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int32_t x_dtyp
  * with both branches accumulated in one fp32 accumulator per output.
  *   Xq, s_a  device, as written by sdq_quantize_act for the same cfg
  *   packed   device, the blob written by sdq_pack for the same cfg, N, K
- *   Y        device, [M, N] fp32 row-major (overwritten)
- * M = 0 is a no-op.  The result is deterministic (no atomics). */
+ *   Y        device, [M, N] row-major, fp32 or bf16 by cfg->y_dtype
+ *            (overwritten; 4-byte aligned)
+ * M = 0 is a no-op.  The result is deterministic (no atomics).  The
+ * arithmetic of one output does not depend on N: on the decode path, rows
+ * of W stacked along N into one blob (e.g. the q, k and v projections, which
+ * read the same X) give the separate launches' outputs bit for bit. */
 sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
-                    const void* packed, int64_t N, int64_t K, float* Y, void* stream);
+                    const void* packed, int64_t N, int64_t K, void* Y, void* stream);
 
 /* sdq_gemm with an explicit kernel choice: SDQ_PATH_DECODE (weight-streaming
  * vector kernel, INT family, any M up to 8), SDQ_PATH_MFMA (matrix-core
@@ -235,7 +248,7 @@ sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int
  * SDQ_ERR_UNSUPPORTED for a path that does not serve the configuration and
  * for SDQ_PATH_DENSE, which takes a workspace (sdq_gemm_ws). */
 sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
-                       const void* packed, int64_t N, int64_t K, float* Y, void* stream,
+                       const void* packed, int64_t N, int64_t K, void* Y, void* stream,
                        int32_t path);
 
 /* Activation quantization and the decomposed GEMM in one call: the same
@@ -245,9 +258,9 @@ sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a, 
  * the activations into LDS itself; otherwise it enqueues the two kernels.
  *   X       device, [M, K] fp32 or bf16 (x_dtype)
  *   Xq, s_a device, outputs as in sdq_quantize_act (always written)
- *   packed  device, as in sdq_gemm;  Y device, [M, N] fp32 (overwritten) */
+ *   packed  device, as in sdq_gemm;  Y device, [M, N] as in sdq_gemm */
 sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int64_t M,
-                      void* Xq, float* s_a, const void* packed, int64_t N, int64_t K, float* Y,
+                      void* Xq, float* s_a, const void* packed, int64_t N, int64_t K, void* Y,
                       void* stream);
 
 /* The path sdq_gemm takes for this configuration and M (SDQ_PATH_DECODE or
@@ -282,7 +295,7 @@ sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, 
  * merge are added after the last chunk instead of within their chunk, a
  * different fp32 rounding order. */
 sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
-                       const void* packed, int64_t N, int64_t K, float* Y, void* workspace,
+                       const void* packed, int64_t N, int64_t K, void* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);
 
 /* Dual family (SDQ_FAMILY_DUAL; Section 5.1's int8 A_o / fp4 A_i): the two
@@ -306,13 +319,14 @@ sdq_status sdq_quantize_act_dual(const sdq_config* cfg, const void* X, int32_t x
  * with the outlier branch exact in int32 and the inlier branch in fp32.
  *   Xq_o, s_a_o, Xq_i, e_a_i  device, as written by sdq_quantize_act_dual
  *   packed   device, the blob written by sdq_pack for the same cfg, N, K
- *   Y        device, [M, N] fp32 row-major (overwritten)
+ *   Y        device, [M, N] row-major, fp32 or bf16 by cfg->y_dtype
+ *            (overwritten; 4-byte aligned)
  * M = 0 is a no-op.  Deterministic.  sdq_gemm, sdq_gemm_ex, sdq_gemm_ws,
  * sdq_linear and sdq_quantize_act return SDQ_ERR_UNSUPPORTED for this
  * family. */
 sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, const float* s_a_o,
                          const void* Xq_i, const void* e_a_i, int64_t M, const void* packed,
-                         int64_t N, int64_t K, float* Y, void* stream);
+                         int64_t N, int64_t K, void* Y, void* stream);
 
 #ifdef __cplusplus
 }

@@ -47,6 +47,7 @@ class Config:
     decomp: str = "same"       # outlier metric: "same" | "magnitude" | "product" | "error" | "output_error"
     order: str = "large"       # outliers by the largest ("large") or smallest ("small") decomp metric
     sfmt_i: str = ""           # inlier scales: "" (int fp16 / mx e8m0) | "e4m3" (int, two-level)
+    y_dtype: str = "f32"       # GEMM output: "f32" | "bf16" (the fp32 result rounded to nearest even)
 
     @staticmethod
     def int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, metric="magnitude") -> "Config":
@@ -84,7 +85,12 @@ class Config:
                                _FMT[self.fmt_a],
                                METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE,
                                _lib.DECOMP[self.decomp], _lib.ORDER[self.order],
-                               _lib.SCALE[self.sfmt_i])
+                               _lib.SCALE[self.sfmt_i],
+                               {"f32": DTYPE_F32, "bf16": DTYPE_BF16}[self.y_dtype])
+
+    def y_torch_dtype(self):
+        import torch
+        return torch.bfloat16 if self.y_dtype == "bf16" else torch.float32
 
 
 def _p(a) -> C.c_void_p:
@@ -177,6 +183,17 @@ def _dev(t, what: str):
     return C.c_void_p(t.data_ptr())
 
 
+def _out(out, M: int, N: int, cfg: Config, device):
+    """The GEMM output: `out` checked against [M, N] of cfg's output dtype, or a new tensor."""
+    import torch
+    dt = cfg.y_torch_dtype()
+    if out is None:
+        return torch.empty((M, N), dtype=dt, device=device)
+    if tuple(out.shape) != (M, N) or out.dtype != dt:
+        raise ValueError(f"out must be [{M}, {N}] {dt}, got {list(out.shape)} {out.dtype}")
+    return out
+
+
 def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
     """Per-token activation quantization on the GPU: returns (Xq uint8, s_a f32)."""
     import torch
@@ -222,14 +239,14 @@ def quantize_act_dual(X, cfg: Config, out=None, stream=None):
 
 
 def gemm_dual(Xo, s_a, Xi, Ea, packed, N: int, K: int, cfg: Config, out=None, stream=None):
-    """The dual family's GEMM on the GPU (fp32 output [M, N])."""
+    """The dual family's GEMM on the GPU (output [M, N], fp32 or bf16 by cfg.y_dtype)."""
     import torch
     M = Xo.shape[0]
     if Xo.shape[1] != K or Xi.shape[1] * 2 != K or Ea.shape[1] * 32 != K:
         raise ValueError("activations have the wrong K")
     if packed.numel() < pack_size(cfg, N, K):
         raise ValueError("packed buffer too small")
-    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=Xo.device)
+    Y = _out(out, M, N, cfg, Xo.device)
     _lib.check(_lib.lib().sdq_gemm_dual(C.byref(cfg.c()), _dev(Xo, "Xq_o"), _dev(s_a, "s_a_o"),
                                         _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"), M, _dev(packed, "packed"),
                                         N, K, _dev(Y, "Y"), _stream(stream)), "sdq_gemm_dual")
@@ -246,7 +263,7 @@ def gemm_workspace_size(cfg: Config, M: int, N: int, K: int, path: int = PATH_AU
 
 def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PATH_AUTO,
          stream=None, workspace=None):
-    """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 output).
+    """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 or bf16 output by cfg.y_dtype).
 
     Paths that take a workspace (the two-pass MX path for many tokens) use
     `workspace` (a uint8 CUDA tensor of at least gemm_workspace_size bytes)
@@ -257,7 +274,7 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
         raise ValueError("Xq has the wrong K")
     if packed.numel() < pack_size(cfg, N, K):
         raise ValueError("packed buffer too small")
-    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=Xq.device)
+    Y = _out(out, M, N, cfg, Xq.device)
     ws_bytes = gemm_workspace_size(cfg, M, N, K, path)
     if ws_bytes == 0:
         _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
@@ -291,7 +308,7 @@ def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=Non
         raise ValueError("X must be float32 or bfloat16")
     Xq = xq if xq is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
     s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
-    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=X.device)
+    Y = _out(out, M, N, cfg, X.device)
     if gemm_workspace_size(cfg, M, N, K) > 0:
         quantize_act(X, cfg, out=Xq, scales=s_a, stream=stream)
         gemm(Xq, s_a, packed, N, K, cfg, out=Y, stream=stream, workspace=workspace)

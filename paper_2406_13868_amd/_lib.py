@@ -35,7 +35,8 @@ class sdq_config(C.Structure):
     _fields_ = [("family", C.c_int32), ("n_o", C.c_int32), ("m_o", C.c_int32),
                 ("fmt_o", C.c_int32), ("n_i", C.c_int32), ("m_i", C.c_int32),
                 ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32),
-                ("decomp", C.c_int32), ("order", C.c_int32), ("sfmt_i", C.c_int32)]
+                ("decomp", C.c_int32), ("order", C.c_int32), ("sfmt_i", C.c_int32),
+                ("y_dtype", C.c_int32)]
 
 
 class SDQError(RuntimeError):

@@ -79,7 +79,7 @@ extern "C" sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N,
 }
 
 extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a,
-                                  int64_t M, const void* packed, int64_t N, int64_t K, float* Y,
+                                  int64_t M, const void* packed, int64_t N, int64_t K, void* Y,
                                   void* stream, int32_t path) {
   Cfg c;
   const sdq_status s = check_config(cfg, N, K, &c);
@@ -90,7 +90,8 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   if (c.dual) return SDQ_ERR_UNSUPPORTED;                  // two activation tensors: sdq_gemm_dual
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
-  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16)
+  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
+      reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
   if (path == SDQ_PATH_AUTO) path = auto_path(c, M, K);
   if (path == SDQ_PATH_DECODE && (c.mx || !decode_fits(M, K))) return SDQ_ERR_UNSUPPORTED;
@@ -131,7 +132,7 @@ extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, 
 }
 
 extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a,
-                                  int64_t M, const void* packed, int64_t N, int64_t K, float* Y,
+                                  int64_t M, const void* packed, int64_t N, int64_t K, void* Y,
                                   void* workspace, size_t ws_bytes, void* stream, int32_t path) {
   Cfg c;
   const sdq_status s = check_config(cfg, N, K, &c);
@@ -144,7 +145,7 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y || !workspace) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
-      reinterpret_cast<uintptr_t>(workspace) % 16)
+      reinterpret_cast<uintptr_t>(workspace) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
   if (ws_bytes < mx_dense_workspace_bytes(N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
   const hipError_t e = launch_mx_dense(c, static_cast<const uint8_t*>(Xq), s_a, M,
@@ -157,13 +158,13 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
 }
 
 extern "C" sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
-                               const void* packed, int64_t N, int64_t K, float* Y, void* stream) {
+                               const void* packed, int64_t N, int64_t K, void* Y, void* stream) {
   return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, SDQ_PATH_AUTO);
 }
 
 extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int64_t M,
                                  void* Xq, float* s_a, const void* packed, int64_t N, int64_t K,
-                                 float* Y, void* stream) {
+                                 void* Y, void* stream) {
   Cfg c;
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
@@ -173,7 +174,7 @@ extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x
   if (M == 0) return SDQ_OK;
   if (!X || !Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq) % 16 ||
-      reinterpret_cast<uintptr_t>(packed) % 16)
+      reinterpret_cast<uintptr_t>(packed) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (auto_path(c, M, K) == SDQ_PATH_DECODE && decode_fused_fits(M, K)) {
@@ -211,7 +212,7 @@ extern "C" sdq_status sdq_quantize_act_dual(const sdq_config* cfg, const void* X
 
 extern "C" sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, const float* s_a_o,
                                     const void* Xq_i, const void* e_a_i, int64_t M, const void* packed,
-                                    int64_t N, int64_t K, float* Y, void* stream) {
+                                    int64_t N, int64_t K, void* Y, void* stream) {
   Cfg c;
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
@@ -220,7 +221,7 @@ extern "C" sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, con
   if (M == 0) return SDQ_OK;
   if (!Xq_o || !s_a_o || !Xq_i || !e_a_i || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq_o) % 16 || reinterpret_cast<uintptr_t>(Xq_i) % 16 ||
-      reinterpret_cast<uintptr_t>(packed) % 16)
+      reinterpret_cast<uintptr_t>(packed) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
   const hipError_t e = launch_dual_mfma(c, static_cast<const uint8_t*>(Xq_o), s_a_o,
                                         static_cast<const uint8_t*>(Xq_i), static_cast<const uint8_t*>(e_a_i),

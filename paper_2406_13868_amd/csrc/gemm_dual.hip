@@ -44,9 +44,10 @@ struct DualArgs {
   const uint8_t* Xi;  // [M][K/2] e2m1 codes of A_i, the even k in the low nibble
   const uint8_t* Ea;  // [M][K/32] e8m0 scales of A_i
   const uint8_t* blob;
-  float* Y;
+  void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t out_off, scale_off, rows_off;
+  bool y_bf16 = false;  // Y as bf16
 };
 
 __device__ __forceinline__ v4i ld16(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, BM);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, BM);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
   if (n >= a.N) return;
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
   const RowScales<1> rs = load_row_scales<1>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, 32);
 #pragma unroll
   for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, 0, e, h, fmaf(rs.v[0][e], so * float(acco[e]), acc[e]));
 }
@@ -355,11 +356,11 @@ hipError_t launch_ms(const DualArgs& a, hipStream_t st) {
 
 hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
                             const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
-                            float* Y, hipStream_t st) {
-  (void)c;
+                            void* Y, hipStream_t st) {
   const DualLayout L = make_dual_layout(N, K);
-  const DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
-                   L.out_off, L.scale_off, L.rows_off};
+  DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
+             L.out_off, L.scale_off, L.rows_off};
+  a.y_bf16 = c.y_bf16;
   if (M <= 32) {
     const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 31) / 32));
     hipLaunchKernelGGL((dual_splitk_kernel<4>), grid, dim3(4 * 64), 0, st, a);

@@ -34,6 +34,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
+#include "tile_out.h"
 
 namespace sdq {
 namespace {
@@ -59,9 +60,10 @@ struct DecodeArgs {
   float* s_a_out;      // fused form: written by workgroup 0
   uint8_t* Xq_out;     // fused form: written by workgroup 0
   const uint8_t* blob;
-  float* Y;
+  void* Y;
   int M, N, K, n_chunks;
   int64_t scales_off, rows_off, irow_off;
+  bool y_bf16 = false;  // Y as bf16
 };
 
 // LDS bytes of one wave's activation region: MT tokens x (8S chunks + the zero chunk).
@@ -355,7 +357,7 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
       float v = part[ws][0][m][r];
 #pragma unroll
       for (int p = 1; p < KS; ++p) v += part[ws][p][m][r];
-      if (m < M) a.Y[size_t(m) * a.N + n] = s_scale[m] * (v * 0.0625f);
+      if (m < M) store_y(a.Y, a.y_bf16, size_t(m) * a.N + n, s_scale[m] * (v * 0.0625f));
     }
   }
 }
@@ -453,19 +455,21 @@ bool decode_fits(int64_t M, int64_t K) {
 }
 
 hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                             const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
+                             const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {
   const Layout L = layout_for(c, N, K);
   DecodeArgs a{Xq, s_a, nullptr, nullptr, nullptr, blob, Y, int(M), int(N), int(K),
                int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
+  a.y_bf16 = c.y_bf16;
   return launch_fuse<0>(c, a, st);
 }
 
 hipError_t launch_int_decode_fused(const Cfg& c, const void* X, int x_dtype, int64_t M,
                                    uint8_t* Xq_out, float* s_a_out, const uint8_t* blob, int64_t N,
-                                   int64_t K, float* Y, hipStream_t st) {
+                                   int64_t K, void* Y, hipStream_t st) {
   const Layout L = layout_for(c, N, K);
   DecodeArgs a{nullptr, nullptr, X, s_a_out, Xq_out, blob, Y, int(M), int(N), int(K),
                int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
+  a.y_bf16 = c.y_bf16;
   if (x_dtype == SDQ_DTYPE_BF16) return launch_fuse<2>(c, a, st);
   return launch_fuse<1>(c, a, st);
 }

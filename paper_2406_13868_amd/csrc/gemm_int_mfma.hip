@@ -44,9 +44,10 @@ struct MfmaArgs {
   const uint8_t* Xq;
   const float* s_a;
   const uint8_t* blob;
-  float* Y;
+  void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off, rows_off, irow_off;
+  bool y_bf16 = false;  // Y as bf16
 };
 
 // The fp16 inlier scale of block kb from a row's scale registers sv: fp16
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   // the inlier row scale of two-level e4m3 scales (a power of two: exact)
   const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[n] : 1.f;
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -453,7 +454,7 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
   const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[n] : 1.f;  // a power of two
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, 32 * MS);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, 32 * MS);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -504,10 +505,11 @@ hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                           const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {
   const Layout L = layout_for(c, N, K);
   MfmaArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
              L.scales_off, L.rows_off, L.irow_off};
+  a.y_bf16 = c.y_bf16;
   if (M <= 32) return launch_ms<1>(c, a, st);
   // 33..64 tokens: one 64-token block expands every weight once; when that
   // leaves fewer workgroups than compute units, two 32-token blocks fill the

@@ -80,10 +80,11 @@ struct DenseArgs {
   const float* s_a;
   const uint8_t* blob;
   const uint4* frag;
-  float* Y;
+  void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
   int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
+  bool y_bf16 = false;  // Y as bf16
 };
 
 typedef int i4v __attribute__((ext_vector_type(4)));
@@ -305,9 +306,15 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
     }
   }
 
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, kDBM);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, kDBM);
+  // fp32 output: every wave stores here, and a wave with a block that did
+  // not merge its inliers adds them to the stored values below.  bf16 output
+  // cannot be read back exactly, so such a wave keeps its accumulators,
+  // adds the inliers into them and stores once at the end.
+  const bool fixup = __any(bad);
+  const bool keep = fixup && a.y_bf16;
   // ---- outputs
-  {
+  if (!keep) {
     const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -325,13 +332,15 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
   //      their fp8 x fp4 products accumulate from zero, A read from global
   //      memory, and are added to the stored outputs.  (Kept apart from the
   //      main accumulators, which would otherwise need a second copy.)
-  if (__any(bad)) {
+  if (fixup) {
+    if (!keep) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int ms = 0; ms < kDMS; ++ms)
+        for (int ms = 0; ms < kDMS; ++ms)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
+          for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const __amdgpu_buffer_rsrc_t wr =
@@ -370,9 +379,12 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
       for (int ms = 0; ms < kDMS; ++ms)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const uint32_t off = (uint32_t(ms * 32 + tile_row(e, h)) * uint32_t(a.N) + uint32_t(n)) * 4u;
-          const float y = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(yr, off, 0, 1));  // glc: from L2
-          store_out(yr, a.N, n, ms, e, h, y + rs.v[ms][e] * acc[j][ms][e]);
+          float y = 0.f;
+          if (!keep) {
+            const uint32_t off = (uint32_t(ms * 32 + tile_row(e, h)) * uint32_t(a.N) + uint32_t(n)) * 4u;
+            y = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(yr.r, off, 0, 1));  // glc: from L2
+          }
+          store_out(yr, a.N, n, ms, e, h, keep ? rs.v[ms][e] * acc[j][ms][e] : y + rs.v[ms][e] * acc[j][ms][e]);
         }
     }
   }
@@ -380,12 +392,14 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
 
 template <int NI>
 hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8_t* blob,
-                     const Layout& L, int64_t N, int64_t K, float* Y, uint4* frag, hipStream_t st) {
+                     const Layout& L, int64_t N, int64_t K, void* Y, bool y_bf16, uint4* frag,
+                     hipStream_t st) {
   const int n_units = int(L.n_tiles * L.n_chunks);
   hipLaunchKernelGGL((mx_densify_kernel<NI>), dim3(unsigned((n_units + 3) / 4)), dim3(256), 0, st,
                      blob, L.scales_off, n_units, frag);
   DenseArgs a{Xq, s_a, blob, frag, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
               L.scales_off, int((M + kDBM - 1) / kDBM)};
+  a.y_bf16 = y_bf16;
   const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
   const unsigned wgs = unsigned(groups * a.m_blocks);
   if (wgs < 2 * kCUs)
@@ -403,13 +417,13 @@ size_t mx_dense_workspace_bytes(int64_t N, int64_t K) {
 }
 
 hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                           const uint8_t* blob, int64_t N, int64_t K, float* Y, void* workspace,
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                            hipStream_t st) {
   const Layout L = make_layout(true, N, K);
   uint4* frag = static_cast<uint4*>(workspace);
-  if (c.n_i == 1) return launch_ni<1>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
-  if (c.n_i == 2) return launch_ni<2>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
-  return launch_ni<3>(Xq, s_a, M, blob, L, N, K, Y, frag, st);
+  if (c.n_i == 1) return launch_ni<1>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+  if (c.n_i == 2) return launch_ni<2>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+  return launch_ni<3>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
 }
 
 }  // namespace sdq

@@ -35,10 +35,11 @@ struct MxArgs {
   const uint8_t* Xq;
   const float* s_a;
   const uint8_t* blob;
-  float* Y;
+  void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
   int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
+  bool y_bf16 = false;  // Y as bf16
 };
 
 template <int MS, int NI, bool HAS_O>
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
-  const __amdgpu_buffer_rsrc_t yr = out_rows(a.Y, a.M, a.N, m0, BM);
+  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, BM);
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -265,9 +266,10 @@ hipError_t launch_ms(const Cfg& c, const MxArgs& a, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                          const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st) {
+                          const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {
   const Layout L = make_layout(true, N, K);
   MxArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles), L.scales_off};
+  a.y_bf16 = c.y_bf16;
   if (M <= 32) return launch_ms<1>(c, a, st);
   if (M <= 64) return launch_ms<2>(c, a, st);
   return launch_ms<4>(c, a, st);

@@ -47,17 +47,17 @@ hipError_t launch_act_quant_dual(const void* X, int x_dtype, int64_t M, int64_t 
 // Dual family, matrix-core kernel (any M): fp4 x fp4 inliers and int8 x int8 outliers.
 hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
                             const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
-                            float* Y, hipStream_t st);
+                            void* Y, hipStream_t st);
 
 // INT family, weight-streaming vector kernel (small M).
 constexpr int kDecodeMaxM = 8;
 hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                             const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+                             const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 // Same kernel with the per-token activation quantization fused in front: every
 // workgroup quantizes X into LDS; workgroup 0 also writes Xq and s_a.
 hipError_t launch_int_decode_fused(const Cfg& c, const void* X, int x_dtype, int64_t M,
                                    uint8_t* Xq_out, float* s_a_out, const uint8_t* blob, int64_t N,
-                                   int64_t K, float* Y, hipStream_t st);
+                                   int64_t K, void* Y, hipStream_t st);
 // Whether the decode kernel takes M tokens of width K (it keeps them in LDS),
 // and whether its fused form does.
 bool decode_fits(int64_t M, int64_t K);
@@ -65,11 +65,11 @@ bool decode_fused_fits(int64_t M, int64_t K);
 
 // INT family, matrix-core kernel (any M).
 hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                           const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 
 // MX family, scaled matrix-core kernel (any M).
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                          const uint8_t* blob, int64_t N, int64_t K, float* Y, hipStream_t st);
+                          const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 
 // MX family with outliers, two passes for many tokens: the blob is expanded
 // once into dense merged fp8 fragments in `workspace` (at least
@@ -77,7 +77,7 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
 constexpr int64_t kDenseMinM = 512;
 size_t mx_dense_workspace_bytes(int64_t N, int64_t K);
 hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                           const uint8_t* blob, int64_t N, int64_t K, float* Y, void* workspace,
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                            hipStream_t st);
 
 }  // namespace sdq

@@ -11,7 +11,8 @@ struct Cfg {
   bool mx;    // MX family (fp8 outliers and fp4 inliers, e8m0 scales, fp8 activations)
   bool dual;  // dual family (int8 outliers, fp4 inliers, int8 + fp4 activations)
   int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric, decomp, order;
-  bool sc8;  // INT family with two-level e4m3 inlier scales
+  bool sc8;     // INT family with two-level e4m3 inlier scales
+  bool y_bf16;  // the GEMM writes Y as bf16 (nearest even of the fp32 result)
 };
 
 inline Layout layout_for(const Cfg& c, int64_t N, int64_t K) { return make_layout(c.mx, N, K, c.sc8); }
@@ -37,6 +38,7 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   if ((c->decomp != SDQ_DECOMP_SAME || c->order != SDQ_ORDER_LARGE) && c->n_o == 0) return SDQ_ERR_CONFIG;
   if (c->sfmt_i != SDQ_SCALE_DEFAULT && c->sfmt_i != SDQ_SCALE_E4M3) return SDQ_ERR_CONFIG;
   if (c->sfmt_i == SDQ_SCALE_E4M3 && c->family != SDQ_FAMILY_INT) return SDQ_ERR_CONFIG;
+  if (c->y_dtype != SDQ_DTYPE_F32 && c->y_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
   if (mx) {
     if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
       return SDQ_ERR_CONFIG;
@@ -75,6 +77,7 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
     out->decomp = c->decomp;
     out->order = c->order;
     out->sc8 = c->sfmt_i == SDQ_SCALE_E4M3;
+    out->y_bf16 = c->y_dtype == SDQ_DTYPE_BF16;
   }
   return SDQ_OK;
 }

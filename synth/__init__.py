@@ -138,6 +138,10 @@ WORKLOADS: Dict[int, Workload] = {
     # The paper's headline SDQ-W7:8-1:8int8-6:8fp4 on the LLaMA-7B block shapes.
     6: Workload(6, "llama7b block, dual 1:8 int8 + 6:8 fp4", LLAMA7B_LAYERS, (1, 16, 256, 4096),
                 (dual_formats(1, 6),), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
+    # LLaMA-7B q, k and v projections stacked along N (one weight of 12288 rows,
+    # the attention recipe), single-token decode: one launch for three layers.
+    7: Workload(7, "llama7b qkv-concatenated decode M=1 12288x4096", (Layer("qkv_proj", 12288, 4096),),
+                (1,), (INT_1x8_E4M3_3x8,), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
 }
 
 

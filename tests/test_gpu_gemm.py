@@ -235,6 +235,28 @@ def test_quantized_activations_feed_gemm_like_oracle():
     assert np.array_equal(Y.cpu().numpy(), Y2)
 
 
+@pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], MX_CFGS[0]], ids=_ids)
+@pytest.mark.parametrize("M", [1, 4, 64])
+def test_concatenated_projections_equal_separate(c, M):
+    """q, k and v stacked along N in one launch give the three separate
+    launches' outputs: bit for bit on the decode path (whose per-output
+    arithmetic does not depend on N), to the oracle's tolerance otherwise."""
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(*c)
+    N, K = 160, 1024
+    X = synth.make_x(2, M, K)
+    Ws = [synth.make_w(2, j, N, K) for j in range(3)]
+    say("qkv concat", _ids(c), M)
+    Yc, Xq, s_a, _ = run_gpu(X, np.concatenate(Ws), cfg)
+    for j, W in enumerate(Ws):
+        blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+        Yj = sdq.gemm(Xq, s_a, blob, N, K, cfg).cpu().numpy()
+        if c[0] == "int" and M <= 8:
+            assert np.array_equal(Yc[:, j * N:(j + 1) * N].view(np.uint32), Yj.view(np.uint32))
+        Yref, _, _, _ = S.reference(X, W, cfg_o)
+        check(Yc[:, j * N:(j + 1) * N], Yref, X, W, cfg_o, f"projection {j}")
+
+
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[4], MX_CFGS[0]], ids=_ids)
 @pytest.mark.parametrize("M,dt", [(1, "bf16"), (2, "f32"), (3, "bf16"), (16, "bf16")])
 def test_linear_equals_quantize_then_gemm(c, M, dt):

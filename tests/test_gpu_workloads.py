@@ -60,9 +60,9 @@ def _check_sampled(W, X, Y, Xq, s_a, fmt, seed, what):
         assert mr <= REL_TOL and nr <= REL_TOL, f"{what}: max_rel={mr:.2e} norm={nr:.2e}"
 
 
-@pytest.mark.parametrize("wid,li", [(2, 0), (3, 0), (3, 2), (4, 0), (4, 1), (1, 0)],
+@pytest.mark.parametrize("wid,li", [(2, 0), (3, 0), (3, 2), (4, 0), (4, 1), (1, 0), (7, 0)],
                          ids=["llama-attn-decode", "llama-mlp-gate-prefill", "llama-mlp-down-prefill",
-                              "opt-fc1-decode", "opt-fc2-decode", "tiny"])
+                              "opt-fc1-decode", "opt-fc2-decode", "tiny", "llama-qkv-decode"])
 def test_workload_layer(wid, li):
     w = synth.WORKLOADS[wid]
     M, fmt = w.M[0], w.formats[0]

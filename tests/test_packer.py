@@ -103,6 +103,19 @@ def test_product_metric_matches_oracle():
     _compare_logical(sdq.pack_logical(W, cfg, act_norm=c), S.pack_logical(W, cfg_o, act_norm=c), cfg_o)
 
 
+def test_concatenated_rows_pack_like_separate_matrices():
+    """Packing is row by row, so W_q, W_k and W_v stacked along N pack to
+    the stacked logical arrays of the three (one launch then serves all three)."""
+    cfg = sdq.Config("int", 1, 8, "e4m3", 3, 8, "int4", "int8")
+    Ws = [synth.make_w(2, j, 64, 512) for j in range(3)]
+    cat = sdq.pack_logical(np.concatenate(Ws), cfg)
+    parts = [sdq.pack_logical(W, cfg) for W in Ws]
+    for key, v in cat.items():
+        if v is None:
+            continue
+        assert np.array_equal(v, np.concatenate([p[key] for p in parts])), key
+
+
 @pytest.mark.parametrize("wid", [1, 2, 4])
 def test_workload_first_layer_matches_oracle(wid):
     """A row slice of each workload's first layer at its real K."""
@@ -188,6 +201,14 @@ def test_error_paths():
     mxc = sdq.Config.mx_family().c()
     assert L.sdq_gemm_ex(C.byref(mxc), C.c_void_p(16), C.c_void_p(16), 1, C.c_void_p(16),
                          32, 128, C.c_void_p(16), None, 1) == -6   # no decode path for MX
+    # the output type: fp32 or bf16 only; a misaligned Y is refused before any launch
+    bad_y = sdq.Config.int_family().c()
+    bad_y.y_dtype = 7
+    assert L.sdq_check(C.byref(bad_y), 32, 128) == -3
+    bf = sdq.Config("int", 1, 8, "e4m3", 3, 8, "int4", "int8", y_dtype="bf16").c()
+    assert L.sdq_check(C.byref(bf), 32, 128) == 0
+    assert L.sdq_gemm(C.byref(bf), C.c_void_p(16), C.c_void_p(16), 1, C.c_void_p(16), 32, 128,
+                      C.c_void_p(18), None) == -2
     for s in list(_lib.STATUS) + [123]:
         assert L.sdq_status_string(s)
 
