@@ -117,10 +117,10 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  *   y_dtype element type of the GEMM output Y: SDQ_DTYPE_F32 (0, the
  *           default) or SDQ_DTYPE_BF16 (half the output bytes).  A bf16
  *           output is the fp32 output rounded to nearest even, bit for bit,
- *           with one exception: on SDQ_PATH_DENSE, a wave of outputs whose
- *           blocks include one that did not merge its inliers rounds its one
- *           fp32 sum (main products plus those inliers) instead of the fp32
- *           path's two-step sum.  The packer ignores it. */
+ *           with one exception: on SDQ_PATH_DENSE, outputs whose wave met a
+ *           block that did not merge its inliers are rounded twice (the main
+ *           sum to bf16, then that value plus those inliers), an extra error
+ *           below 2^-9 of the main sum.  The packer ignores it. */
 typedef struct {
   int32_t family;
   int32_t n_o, m_o, fmt_o;

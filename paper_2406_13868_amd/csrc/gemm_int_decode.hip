@@ -131,7 +131,8 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
   __shared__ float s_scale[kDecodeMaxM];
   __shared__ float part[SPW][KS][kDecodeMaxM][kSliceRows];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: chunk offsets stay scalar
   const int ws = wave / KS, kq = wave % KS;  // slice in the workgroup, part of K
   const int K = a.K, M = a.M, KC = a.n_chunks;
   const int r = lane & 3, j = (lane >> 2) & 1, cc = lane >> 3;

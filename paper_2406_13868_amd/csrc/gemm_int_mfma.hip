@@ -141,7 +141,8 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   constexpr int BM = 32 * MS;
   __shared__ __align__(16) _Float16 xs[2][BM * kLdsRow];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: chunk offsets stay scalar
   const int col = lane & 31, h = lane >> 5;
   const int m0 = blockIdx.y * BM;
   const int tile = blockIdx.x * kWaves + wave;
@@ -281,7 +282,8 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   constexpr int BM = 32 * MS;
   __shared__ float red[NW / 2][16][64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = tid >> 6;  // (a wave-uniform copy makes the compiler spill at two sub-tiles)
   const int col = lane & 31, h = lane >> 5;
   const int m0 = blockIdx.y * BM;
   const int tile = blockIdx.x;

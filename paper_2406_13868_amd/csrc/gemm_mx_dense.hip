@@ -84,7 +84,6 @@ struct DenseArgs {
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
   int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
-  bool y_bf16 = false;  // Y as bf16
 };
 
 typedef int i4v __attribute__((ext_vector_type(4)));
@@ -104,7 +103,9 @@ __device__ __forceinline__ bool unmerged(uint32_t sc) {
 
 // DEEP: one workgroup per CU (a grid that cannot fill two per CU), loads four
 // chunks ahead; otherwise two workgroups per CU with a one-chunk pipeline.
-template <int NI, bool DEEP>
+// YB: Y as bf16 (a template parameter, so that each form has one store and
+// one read-back width).
+template <int NI, bool DEEP, bool YB>
 __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(DenseArgs a) {
   // fp8 activations of one 128-K chunk: 128 rows of 128 bytes, 16-byte piece
   // p of row r at piece p ^ lds_swizzle(r)
@@ -306,15 +307,10 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
     }
   }
 
-  const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, kDBM);
-  // fp32 output: every wave stores here, and a wave with a block that did
-  // not merge its inliers adds them to the stored values below.  bf16 output
-  // cannot be read back exactly, so such a wave keeps its accumulators,
-  // adds the inliers into them and stores once at the end.
-  const bool fixup = __any(bad);
-  const bool keep = fixup && a.y_bf16;
-  // ---- outputs
-  if (!keep) {
+  const OutRows yr = out_rows(a.Y, YB, a.M, a.N, m0, kDBM);
+  // ---- outputs (a wave with a block that did not merge its inliers adds
+  //      them to its stored values below)
+  {
     const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -332,15 +328,13 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
   //      their fp8 x fp4 products accumulate from zero, A read from global
   //      memory, and are added to the stored outputs.  (Kept apart from the
   //      main accumulators, which would otherwise need a second copy.)
-  if (fixup) {
-    if (!keep) {
+  if (__any(bad)) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int ms = 0; ms < kDMS; ++ms)
+      for (int ms = 0; ms < kDMS; ++ms)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
-    }
+        for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const __amdgpu_buffer_rsrc_t wr =
@@ -379,12 +373,14 @@ __global__ __launch_bounds__(kDThreads, DEEP ? 1 : 2) void mx_dense_kernel(Dense
       for (int ms = 0; ms < kDMS; ++ms)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          float y = 0.f;
-          if (!keep) {
-            const uint32_t off = (uint32_t(ms * 32 + tile_row(e, h)) * uint32_t(a.N) + uint32_t(n)) * 4u;
-            y = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(yr.r, off, 0, 1));  // glc: from L2
-          }
-          store_out(yr, a.N, n, ms, e, h, keep ? rs.v[ms][e] * acc[j][ms][e] : y + rs.v[ms][e] * acc[j][ms][e]);
+          // the stored value, from L2 (glc); a bf16 one was rounded once already
+          const uint32_t idx = uint32_t(ms * 32 + tile_row(e, h)) * uint32_t(a.N) + uint32_t(n);
+          float y;
+          if constexpr (YB)
+            y = __uint_as_float(uint32_t(__builtin_amdgcn_raw_buffer_load_b16(yr.r, idx * 2u, 0, 1)) << 16);
+          else
+            y = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(yr.r, idx * 4u, 0, 1));
+          store_out(yr, a.N, n, ms, e, h, y + rs.v[ms][e] * acc[j][ms][e]);
         }
     }
   }
@@ -399,13 +395,19 @@ hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8
                      blob, L.scales_off, n_units, frag);
   DenseArgs a{Xq, s_a, blob, frag, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
               L.scales_off, int((M + kDBM - 1) / kDBM)};
-  a.y_bf16 = y_bf16;
   const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
   const unsigned wgs = unsigned(groups * a.m_blocks);
-  if (wgs < 2 * kCUs)
-    hipLaunchKernelGGL((mx_dense_kernel<NI, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((mx_dense_kernel<NI, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
+  if (wgs < 2 * kCUs) {
+    if (y_bf16)
+      hipLaunchKernelGGL((mx_dense_kernel<NI, true, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL((mx_dense_kernel<NI, true, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
+  } else {
+    if (y_bf16)
+      hipLaunchKernelGGL((mx_dense_kernel<NI, false, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL((mx_dense_kernel<NI, false, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
+  }
   return hipGetLastError();
 }
 

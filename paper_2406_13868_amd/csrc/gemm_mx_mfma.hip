@@ -49,7 +49,8 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   // piece p of row r at piece p ^ lds_swizzle(r)
   __shared__ __align__(16) uint8_t xs[2][BM * kChunkK];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: chunk offsets stay scalar
   const int col = lane & 31, h = lane >> 5;
   int group, mblock;
   tile_work(blockIdx.x, gridDim.x / a.m_blocks, a.m_blocks, group, mblock);
