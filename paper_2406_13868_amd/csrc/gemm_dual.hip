@@ -366,7 +366,15 @@ hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, c
     hipLaunchKernelGGL((dual_splitk_kernel<4>), grid, dim3(4 * 64), 0, st, a);
     return hipGetLastError();
   }
-  if (M <= 64) return launch_ms<2>(a, st);
+  // Tokens per workgroup: 32, 64 or 128 (one, two or four sub-tiles per
+  // wave).  Larger blocks reuse every weight fragment for more tokens but
+  // give fewer workgroups; the smallest block that leaves the GPU full wins.
+  // Measured on the LLaMA-7B shapes: 4096x4096 at M = 128/256 takes 19/21 us
+  // with 32-token blocks against 31/32 us with 128; 11008x4096 at M = 512
+  // takes 60 us with 64-token blocks against 73 us with 128.
+  const int64_t groups = (a.n_tiles + kDWaves - 1) / kDWaves;
+  if (groups * ((M + 31) / 32) <= 256) return launch_ms<1>(a, st);
+  if (groups * ((M + 63) / 64) <= 1024 && groups * ((M + 127) / 128) < 512) return launch_ms<2>(a, st);
   return launch_ms<4>(a, st);
 }
 

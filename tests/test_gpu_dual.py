@@ -98,6 +98,31 @@ def test_gemm_dual_matches_oracle(n_o, n_i, M, N, K):
     _check(Y, X, W, cfg_o, f"dual {n_o}:8+{n_i}:8 M={M} N={N} K={K}")
 
 
+def _tokens_per_block(M, N):
+    """The tiled kernel's token block for this shape (32, 64 or 128): the
+    smallest that keeps the GPU full, by workgroup count."""
+    groups = -(-(-(-N // 32)) // 4)
+    if groups * -(-M // 32) <= 256:
+        return 32
+    if groups * -(-M // 64) <= 1024 and groups * -(-M // 128) < 512:
+        return 64
+    return 128
+
+
+@pytest.mark.parametrize("M,N,K,block", [(100, 256, 512, 32), (300, 16384, 256, 64),
+                                         (1100, 4096, 128, 64), (300, 32768, 128, 128),
+                                         (2100, 4096, 128, 128)])
+def test_gemm_dual_every_token_block(M, N, K, block):
+    """Shapes that take each token block of the tiled kernel, with ragged M."""
+    assert _tokens_per_block(M, N) == block
+    cfg, cfg_o = _cfgs(1, 6)
+    X = synth.make_x(2, M, K)
+    W = synth.make_w(2, 0, N, K)
+    say("gemm dual block", block, M, N, K)
+    Y, _ = _run(X, W, cfg)
+    _check(Y, X, W, cfg_o, f"dual block={block} M={M} N={N} K={K}")
+
+
 @pytest.mark.parametrize("M", [1, 256])
 def test_gemm_dual_llama_layer(M):
     """A LLaMA-7B 4096x4096 projection with the paper's 1:8 int8 + 6:8 fp4, bf16 input."""
