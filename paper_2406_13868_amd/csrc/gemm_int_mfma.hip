@@ -517,6 +517,15 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   // leaves fewer workgroups than compute units, two 32-token blocks fill the
   // GPU instead (each weight is then expanded twice)
   if (M <= 64) return L.n_tiles < kCUs ? launch_ms<1>(c, a, st) : launch_ms<2>(c, a, st);
+  // More tokens: the tiled kernel (four tiles x 128 tokens per workgroup,
+  // one workgroup per compute unit) does about 1.3x the work per unit of time
+  // of the split-K kernel over 64-token blocks, but only on a full grid: it
+  // runs when its last round of workgroups is at least 3/4 full.  Measured
+  // on 4096x4096: M = 128/256/512 take 24/37/70 us split-K against 104/106/111
+  // tiled (32 to 128 workgroups); 11008x4096 at M = 512 takes 179 against 216.
+  const int64_t w4 = int64_t((L.n_tiles + kWaves - 1) / kWaves) * ((M + 127) / 128);
+  const int64_t rounds = (w4 + kCUs - 1) / kCUs;
+  if (4 * w4 < 3 * kCUs * rounds) return launch_ms<2>(c, a, st);
   return launch_ms<4>(c, a, st);
 }
 

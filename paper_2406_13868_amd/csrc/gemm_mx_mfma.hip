@@ -31,6 +31,7 @@ using namespace mx;
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
+constexpr int64_t kCUs = 256;  // compute units of an MI355X
 struct MxArgs {
   const uint8_t* Xq;
   const float* s_a;
@@ -273,6 +274,13 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
   a.y_bf16 = c.y_bf16;
   if (M <= 32) return launch_ms<1>(c, a, st);
   if (M <= 64) return launch_ms<2>(c, a, st);
+  // More tokens: the largest token block that still gives a full round of
+  // workgroups wins (each block re-expands every weight it reads).  Measured
+  // at M = 128/256: 4096x4096 takes 26/27 us with 32-token blocks against
+  // 36/37 us with 128; 11008x4096 at M = 128 takes 31 us with 64 against 38.
+  const int64_t groups = (a.n_tiles + kWaves - 1) / kWaves;
+  if (groups * ((M + 31) / 32) <= kCUs) return launch_ms<1>(c, a, st);
+  if (groups * ((M + 63) / 64) <= kCUs) return launch_ms<2>(c, a, st);
   return launch_ms<4>(c, a, st);
 }
 

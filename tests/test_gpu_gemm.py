@@ -235,6 +235,40 @@ def test_quantized_activations_feed_gemm_like_oracle():
     assert np.array_equal(Y.cpu().numpy(), Y2)
 
 
+def _kernel_for(fam, M, N):
+    """Which matrix-core kernel the launcher picks above 64 tokens (the rule
+    the kernels' launchers state): INT "tiled" when its grid of
+    ceil(N/128) x ceil(M/128) workgroups fills its last round of 256 to at
+    least 3/4, else "split-K"; MX token blocks of 32, 64 or 128 (the largest
+    whose grid stays within one round of 256 workgroups)."""
+    groups = -(-N // 128)
+    if fam == "int":
+        w4 = groups * -(-M // 128)
+        rounds = -(-w4 // 256)
+        return "split-K" if 4 * w4 < 3 * 256 * rounds else "tiled"
+    if groups * -(-M // 32) <= 256:
+        return "block32"
+    if groups * -(-M // 64) <= 256:
+        return "block64"
+    return "block128"
+
+
+@pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 100, 70, 256, "split-K"), ("int", 384, 8192, 256, "tiled"),
+                                              ("int", 400, 8192, 128, "tiled"), ("int", 700, 2048, 128, "split-K"),
+                                              ("mx", 100, 70, 256, "block32"), ("mx", 200, 8192, 256, "block64"),
+                                              ("mx", 300, 8192, 128, "block128")])
+def test_every_matrix_kernel_above_64_tokens(fam, M, N, K, kernel):
+    """Shapes that take each matrix-core kernel and token block past 64 tokens, ragged M."""
+    assert _kernel_for(fam, M, N) == kernel
+    cfg, cfg_o = _cfgs(fam, 1, 8, "e4m3", 3 if fam == "int" else 2)
+    X = synth.make_x(1, M, K)
+    W = synth.make_w(1, 0, N, K)
+    say("kernel", fam, kernel, M, N, K)
+    Y, _, _, _ = run_gpu(X, W, cfg, path=sdq.PATH_MFMA)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    check(Y, Yref, X, W, cfg_o, f"{fam} {kernel} M={M} N={N} K={K}")
+
+
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], MX_CFGS[0]], ids=_ids)
 @pytest.mark.parametrize("M", [1, 4, 64])
 def test_concatenated_projections_equal_separate(c, M):
