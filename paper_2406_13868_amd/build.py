@@ -29,6 +29,7 @@ SOURCES = [
     "gemm_mx_mfma.hip",
     "gemm_mx_dense.hip",
     "gemm_dual.hip",
+    "gemm_dual_decode.hip",
 ]
 
 COMMON = [

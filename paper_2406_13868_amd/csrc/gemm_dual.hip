@@ -361,6 +361,7 @@ hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, c
   DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
              L.out_off, L.scale_off, L.rows_off};
   a.y_bf16 = c.y_bf16;
+  if (dual_decode_fits(M, N, K)) return launch_dual_decode(c, Xo, s_a, Xi, Ea, M, blob, N, K, Y, st);
   if (M <= 32) {
     const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 31) / 32));
     hipLaunchKernelGGL((dual_splitk_kernel<4>), grid, dim3(4 * 64), 0, st, a);

@@ -44,6 +44,12 @@ hipError_t launch_act_quant(const Cfg& c, const void* X, int x_dtype, int64_t M,
 // Dual family: int8 A_o (Xo, s_a) and MXFP4 A_i (Xi: [M][K/2] nibbles, Ea: [M][K/32] e8m0).
 hipError_t launch_act_quant_dual(const void* X, int x_dtype, int64_t M, int64_t K, uint8_t* Xo,
                                  float* s_a, uint8_t* Xi, uint8_t* Ea, hipStream_t st);
+// Dual family, one or two tokens: weight-streaming vector kernel (when
+// dual_decode_fits; launch_dual_mfma dispatches to it).
+bool dual_decode_fits(int64_t M, int64_t N, int64_t K);
+hipError_t launch_dual_decode(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
+                              const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
+                              void* Y, hipStream_t st);
 // Dual family, matrix-core kernel (any M): fp4 x fp4 inliers and int8 x int8 outliers.
 hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
                             const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,

@@ -98,6 +98,39 @@ def test_gemm_dual_matches_oracle(n_o, n_i, M, N, K):
     _check(Y, X, W, cfg_o, f"dual {n_o}:8+{n_i}:8 M={M} N={N} K={K}")
 
 
+@pytest.mark.parametrize("M", [1, 2])
+@pytest.mark.parametrize("N,K", [(256, 128), (70, 256), (544, 1152), (96, 4096), (40, 11008)])
+def test_gemm_dual_decode_matches_oracle(M, N, K):
+    """One and two tokens (the vector decode kernel; two tokens at K = 11008
+    exceed its register budget and take the matrix kernel): one chunk of K
+    (half the lanes idle), ragged N, parts of K from one to eight."""
+    cfg, cfg_o = _cfgs(1, 6)
+    X = synth.make_x(2, M, K)
+    W = synth.make_w(2, 0, N, K)
+    say("gemm dual decode", M, N, K)
+    Y, _ = _run(X, W, cfg)
+    _check(Y, X, W, cfg_o, f"dual decode M={M} N={N} K={K}")
+
+
+def test_gemm_dual_decode_grid_is_exact():
+    """The integer grid of test_gemm_dual_integer_grid_is_exact at one and two tokens."""
+    rng = np.random.default_rng(9)
+    N, K = 64, 512
+    for M in (1, 2):
+        X = rng.choice([-6.0, -4.0, -2.0, -1.0, 0.0, 1.0, 2.0, 3.0, 4.0, 6.0], (M, K)).astype(np.float32)
+        X[:, 0] = 127.0
+        X[:, 1:32] = rng.choice([-64.0, -32.0, 0.0, 32.0, 64.0, 96.0], (M, 31))
+        W = rng.choice([-6.0, -3.0, -1.0, 1.0, 2.0, 4.0, 6.0], (N, K)).astype(np.float32)
+        W[:, ::8] = 127.0 * rng.choice([-1.0, 1.0], (N, K // 8))
+        W[:, 1::32] = 6.0
+        cfg, cfg_o = _cfgs(1, 6)
+        Yref, _, (s_ao, Ea), L = S.reference(X, W, cfg_o)
+        assert (s_ao == 1).all() and (L["scale_o"] == 1).all()
+        say("gemm dual decode grid", M)
+        Y, _ = _run(X, W, cfg)
+        assert np.array_equal(Y.astype(np.float64), Yref)
+
+
 def _tokens_per_block(M, N):
     """The tiled kernel's token block for this shape (32, 64 or 128): the
     smallest that keeps the GPU full, by workgroup count."""
@@ -123,7 +156,7 @@ def test_gemm_dual_every_token_block(M, N, K, block):
     _check(Y, X, W, cfg_o, f"dual block={block} M={M} N={N} K={K}")
 
 
-@pytest.mark.parametrize("M", [1, 256])
+@pytest.mark.parametrize("M", [1, 2, 256])
 def test_gemm_dual_llama_layer(M):
     """A LLaMA-7B 4096x4096 projection with the paper's 1:8 int8 + 6:8 fp4, bf16 input."""
     cfg, cfg_o = _cfgs(1, 6, "magnitude")
