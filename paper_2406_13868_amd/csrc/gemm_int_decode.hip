@@ -95,6 +95,20 @@ __device__ __forceinline__ float sum_lanes_mod4(float v) {
   return __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
 }
 
+// Maximum over the 64 lanes of the wave: DPP row rotations by 1, 2, 4 and 8
+// inside each row of 16 lanes, then the permlane swaps across rows (no LDS
+// round trips).  A maximum is exact in any order.
+__device__ __forceinline__ float max_lanes(float v) {
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x121, 0xF, 0xF, false)));  // row_ror:1
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x122, 0xF, 0xF, false)));  // row_ror:2
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false)));  // row_ror:4
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false)));  // row_ror:8
+  const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(p16[0]), __uint_as_float(p16[1]));
+  const auto p32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p32[0]), __uint_as_float(p32[1]));
+}
+
 __device__ __forceinline__ _Float16 f16lo(uint32_t v) {
   return __builtin_bit_cast(_Float16, (unsigned short)(v & 0xFFFFu));
 }
@@ -251,8 +265,7 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
     }
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) amax[m] = fmaxf(amax[m], __shfl_xor(amax[m], o, 64));
+      amax[m] = max_lanes(amax[m]);
       if (lane == 0) red[wave][m] = amax[m];
     }
     __syncthreads();
