@@ -292,7 +292,11 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
       if (blockIdx.x == 0 && m < M && k < K)
         *reinterpret_cast<uint4*>(a.Xq_out + size_t(m) * K + k) = q;
     }
-    __syncthreads();
+    // the products read only this wave's region; s_scale, written by thread
+    // 0 above, is read after the workgroup barrier of the K-part sum
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
   // ---- 4. the products, one step at a time as the stream lands
