@@ -7,9 +7,11 @@
 //                                 or saturated to +-448 (fp8 e4m3)
 // A zero row gives s_a = 0 and zero codes.
 //
-// One workgroup of 256 threads per row.  Rows up to 16384 wide are read once
-// into registers (16-byte loads), reduced through a wave butterfly and LDS,
-// then quantized and written back with 8-byte stores; wider rows take a
+// One workgroup per row: 256 threads, or 1024 when there are few rows and
+// they are wide (so that the few compute units busy keep four times the loads
+// in flight).  Rows up to 8 pieces of 8 elements per thread are read once
+// into registers (16-byte loads), reduced by a DPP/permlane wave maximum and
+// LDS, then quantized and written back with 8-byte stores; wider rows take a
 // second pass over the (L2-resident) row.  The pass is HBM-bound: K*(in+1)
 // bytes per row.
 #include <hip/hip_runtime.h>
@@ -21,18 +23,30 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// Maximum over the 64 lanes of a wave: DPP row rotations by 1, 2, 4 and 8
+// inside each row of 16 lanes, then the permlane swaps across rows.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x121, 0xF, 0xF, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x122, 0xF, 0xF, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false)));
+  const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(p16[0]), __uint_as_float(p16[1]));
+  const auto p32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p32[0]), __uint_as_float(p32[1]));
 }
 
+// Maximum over a workgroup of NT threads (red: NT / 64 floats of LDS).
+template <int NT>
 __device__ __forceinline__ float block_max(float v, float* red) {
   v = wave_max(v);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) red[w] = v;
   __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) r = fmaxf(r, red[i]);
+  return r;
 }
 
 // Eight consecutive elements, widened to fp32.
@@ -80,31 +94,31 @@ __device__ __forceinline__ void quant_store8(const float (&v)[8], float inv, uin
   *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
 }
 
-template <bool BF16, bool E4M3, int CH>
-__global__ __launch_bounds__(kThreads) void act_quant_regs(const void* __restrict__ X, int64_t K,
-                                                           uint8_t* __restrict__ Xq,
-                                                           float* __restrict__ s_a) {
-  __shared__ float red[4];
+template <bool BF16, bool E4M3, int CH, int NT>
+__global__ __launch_bounds__(NT) void act_quant_regs(const void* __restrict__ X, int64_t K,
+                                                     uint8_t* __restrict__ Xq,
+                                                     float* __restrict__ s_a) {
+  __shared__ float red[NT / 64];
   const int64_t m = blockIdx.x;
   const int64_t P = K >> 3;  // pieces of 8 elements
   float v[CH][8];
   float amax = 0.f;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
-    const int64_t p = threadIdx.x + c * kThreads;
+    const int64_t p = threadIdx.x + c * NT;
     if (p < P) {
       load8<BF16>(X, m * K + p * 8, v[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[c][i]));
     }
   }
-  amax = block_max(amax, red);
+  amax = block_max<NT>(amax, red);
   const float qmax = E4M3 ? 448.f : 127.f;
   const float inv = amax > 0.f ? qmax / amax : 0.f;
   if (threadIdx.x == 0) s_a[m] = amax / qmax;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
-    const int64_t p = threadIdx.x + c * kThreads;
+    const int64_t p = threadIdx.x + c * NT;
     if (p < P) quant_store8<E4M3>(v[c], inv, Xq + m * K + p * 8);
   }
 }
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void act_quant_2pass(const void* __restri
 #pragma unroll
     for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
   }
-  amax = block_max(amax, red);
+  amax = block_max<kThreads>(amax, red);
   const float qmax = E4M3 ? 448.f : 127.f;
   const float inv = amax > 0.f ? qmax / amax : 0.f;
   if (threadIdx.x == 0) s_a[m] = amax / qmax;
@@ -139,14 +153,25 @@ hipError_t launch_typed(const void* X, int64_t M, int64_t K, uint8_t* Xq, float*
                         hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(M)), block(kThreads);
   const int64_t pieces = K / 8;
+  // few wide rows: 1024 threads per row
+  if (M < 256 && pieces > kThreads * 4 && pieces <= 4096 * 2) {
+    const dim3 big(1024);
+    if (pieces <= 1024 * 2)
+      hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 2, 1024>), grid, big, 0, st, X, K, Xq, s_a);
+    else if (pieces <= 1024 * 4)
+      hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 4, 1024>), grid, big, 0, st, X, K, Xq, s_a);
+    else
+      hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 8, 1024>), grid, big, 0, st, X, K, Xq, s_a);
+    return hipGetLastError();
+  }
   if (pieces <= 1 * kThreads)
-    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 1>), grid, block, 0, st, X, K, Xq, s_a);
+    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 1, kThreads>), grid, block, 0, st, X, K, Xq, s_a);
   else if (pieces <= 2 * kThreads)
-    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 2>), grid, block, 0, st, X, K, Xq, s_a);
+    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 2, kThreads>), grid, block, 0, st, X, K, Xq, s_a);
   else if (pieces <= 4 * kThreads)
-    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 4>), grid, block, 0, st, X, K, Xq, s_a);
+    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 4, kThreads>), grid, block, 0, st, X, K, Xq, s_a);
   else if (pieces <= 8 * kThreads)
-    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 8>), grid, block, 0, st, X, K, Xq, s_a);
+    hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 8, kThreads>), grid, block, 0, st, X, K, Xq, s_a);
   else
     hipLaunchKernelGGL((act_quant_2pass<BF16, E4M3>), grid, block, 0, st, X, K, Xq, s_a);
   return hipGetLastError();
@@ -187,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void act_quant_dual(const void* __restric
 #pragma unroll
     for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
   }
-  amax = block_max(amax, red);
+  amax = block_max<kThreads>(amax, red);
   const float inv = amax > 0.f ? 127.f / amax : 0.f;
   if (threadIdx.x == 0) s_a[m] = amax / 127.f;
   for (int64_t base = 0; base < P; base += kThreads) {  // the same trip count for every lane
