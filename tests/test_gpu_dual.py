@@ -197,3 +197,47 @@ def test_dual_entry_points_refuse_other_families():
         sdq.quantize_act(X, cfg)                       # two activation tensors: the dual call
     with pytest.raises(sdq.SDQError):
         sdq.quantize_act_dual(X, sdq.Config.int_family())
+
+
+@pytest.mark.parametrize("M", [1, 16, 130])
+@pytest.mark.parametrize("y_dtype", ["f32", "bf16"])
+def test_dual_hip_graph_replays_match_eager(M, y_dtype):
+    """Both dual calls captured in a HIP graph (the decode, split-K and tiled
+    forms by M) give the eager result on every replay, with eager work in
+    between."""
+    import dataclasses
+    torch = torch_cuda()
+    cfg = dataclasses.replace(_cfgs(1, 6)[0], y_dtype=y_dtype)
+    N, K = 512, 1024
+    X = torch.from_numpy(synth.make_x(2, M, K)).cuda().to(torch.bfloat16)
+    blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
+    Xo = torch.empty((M, K), dtype=torch.uint8, device="cuda")
+    s_a = torch.empty((M,), dtype=torch.float32, device="cuda")
+    Xi = torch.empty((M, K // 2), dtype=torch.uint8, device="cuda")
+    Ea = torch.empty((M, K // 32), dtype=torch.uint8, device="cuda")
+    Y = torch.empty((M, N), dtype=cfg.y_torch_dtype(), device="cuda")
+
+    def step():
+        sdq.quantize_act_dual(X, cfg, out=(Xo, s_a, Xi, Ea))
+        sdq.gemm_dual(Xo, s_a, Xi, Ea, blob, N, K, cfg, out=Y)
+
+    say("dual graph", M, y_dtype)
+    step()
+    torch.cuda.synchronize()
+    ref = Y.clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(4):
+        Y.fill_(float("nan"))
+        Xo.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
+        sdq.gemm_dual(Xo, s_a, Xi, Ea, blob, N, K, cfg, out=torch.empty_like(Y))
+        torch.cuda.synchronize()
