@@ -276,7 +276,8 @@ sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
  * the expansion runs once per weight instead of once per weight and block of
  * 128 tokens (at 512 tokens and more the two passes take less time).
  *   path   SDQ_PATH_AUTO (what sdq_gemm_ws takes: SDQ_PATH_DENSE for the MX
- *          family with outliers when M >= 512, else what sdq_gemm takes), or
+ *          family with outliers when M >= 512 and ceil(N/256) * ceil(M/128)
+ *          >= 160, else what sdq_gemm takes), or
  *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE
  *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE, 0 for the other paths
  * Returns SDQ_ERR_UNSUPPORTED for SDQ_PATH_DENSE outside the MX family with

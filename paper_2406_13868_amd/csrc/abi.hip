@@ -24,9 +24,13 @@ int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
 }
 
 // The path of sdq_gemm_ws: the two-pass form where its one expansion per
-// weight beats one per weight and 128 tokens.
-int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t K) {
-  if (c.mx && c.n_o > 0 && M >= kDenseMinM) return SDQ_PATH_DENSE;
+// weight beats the one-pass kernel's per token block, which needs many tokens
+// and a grid of at least 160 workgroups of 256 outputs x 128 tokens (measured:
+// 4096x4096 at M = 1024, 128 workgroups, takes 42 us in one pass against 48
+// in two; 11008x4096 at M = 512, 172 workgroups, 56 against 52).
+int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t N, int64_t K) {
+  const int64_t wgs = (N + 255) / 256 * ((M + 127) / 128);
+  if (c.mx && c.n_o > 0 && M >= kDenseMinM && wgs >= 160) return SDQ_PATH_DENSE;
   return auto_path(c, M, K);
 }
 
@@ -125,7 +129,7 @@ extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, 
   if (M < 0) return SDQ_ERR_SHAPE;
   if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
   if (c.dual) return SDQ_ERR_UNSUPPORTED;
-  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, K);
+  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
   if (path == SDQ_PATH_DENSE && !(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
   *bytes = path == SDQ_PATH_DENSE ? mx_dense_workspace_bytes(N, K) : 0;
   return SDQ_OK;
@@ -139,7 +143,7 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
   if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
-  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, K);
+  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
   if (path != SDQ_PATH_DENSE) return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
   if (!(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
   if (M == 0) return SDQ_OK;

@@ -358,28 +358,27 @@ def test_hip_graph_replays_match_eager_two_pass():
     X = torch.from_numpy(synth.make_x(2, M, K)).cuda()
     blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
     Xq, s_a = sdq.quantize_act(X, cfg)
-    assert sdq.gemm_workspace_size(cfg, M, N, K) > 0
-    ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_DENSE), dtype=torch.uint8, device="cuda")
     Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
     say("graph two-pass")
-    sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+    sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
     torch.cuda.synchronize()
     ref = Y.clone()
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
     torch.cuda.current_stream().wait_stream(side)
     with torch.cuda.graph(g):
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
     for rep in range(4):
         Y.fill_(float("nan"))
         ws.fill_(0x5A)
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y), workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y), path=sdq.PATH_DENSE, workspace=ws)
         torch.cuda.synchronize()
 
 

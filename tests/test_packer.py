@@ -245,8 +245,11 @@ def test_gemm_workspace_size_and_validation():
     mx, mx_no = sdq.Config.mx_family(), sdq.Config("mx", 0, 8, "e4m3", 2, 8, "e2m1", "e4m3")
     it = sdq.Config.int_family()
     assert sdq.gemm_workspace_size(mx, 2048, 11008, 4096) == 11008 * 4096
-    assert sdq.gemm_workspace_size(mx, 512, 100, 384) == 128 * 384      # N padded to 32
-    assert sdq.gemm_workspace_size(mx, 511, 100, 384) == 0               # one pass below 512 tokens
+    assert sdq.gemm_workspace_size(mx, 512, 11008, 4096) == 11008 * 4096  # 43 x 4 workgroups
+    assert sdq.gemm_workspace_size(mx, 512, 100, 384) == 0               # one pass on a small grid
+    assert sdq.gemm_workspace_size(mx, 1024, 4096, 4096) == 0            # 16 x 8 workgroups
+    assert sdq.gemm_workspace_size(mx, 511, 11008, 4096) == 0            # one pass below 512 tokens
+    assert sdq.gemm_workspace_size(mx, 512, 100, 384, sdq.PATH_DENSE) == 128 * 384  # N padded to 32
     assert sdq.gemm_workspace_size(mx, 1, 100, 384, sdq.PATH_DENSE) == 128 * 384
     assert sdq.gemm_workspace_size(mx, 4096, 100, 384, sdq.PATH_MFMA) == 0
     assert sdq.gemm_workspace_size(mx_no, 4096, 100, 384) == 0           # no outlier branch
