@@ -236,6 +236,17 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(cfg, 1, 4096, 4096) == sdq.PATH_DECODE
     assert sdq.gemm_path(cfg, 2048, 4096, 4096) == sdq.PATH_MFMA
     assert sdq.gemm_path(sdq.Config.mx_family(), 1, 4096, 4096) == sdq.PATH_MFMA
+    # the decode kernel up to 8 tokens where its registers fit the row
+    for M in range(1, 9):
+        assert sdq.gemm_path(cfg, M, 4096, 4096) == sdq.PATH_DECODE, M
+    assert sdq.gemm_path(cfg, 9, 4096, 4096) == sdq.PATH_MFMA
+    assert sdq.gemm_path(cfg, 2, 4096, 11008) == sdq.PATH_DECODE
+    assert sdq.gemm_path(cfg, 3, 4096, 11008) == sdq.PATH_MFMA
+    # the two-pass MX path only on a grid of at least 160 workgroups
+    mx = sdq.Config.mx_family()
+    assert sdq.gemm_path(mx, 512, 11008, 4096, workspace=True) == sdq.PATH_DENSE
+    assert sdq.gemm_path(mx, 1024, 4096, 4096, workspace=True) == sdq.PATH_MFMA
+    assert sdq.gemm_path(mx, 2048, 4096, 4096, workspace=True) == sdq.PATH_DENSE
 
 
 def test_gemm_workspace_size_and_validation():
