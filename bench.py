@@ -115,8 +115,8 @@ def measured_traffic(name: str):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {a.gpus}); "
-              "the path shards by output rows with no exchange, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py: runs on one GPU only (asked for --gpus {a.gpus}); across GPUs the "
+              "layer would shard by output rows of W, with no exchange between them", file=sys.stderr)
         sys.exit(2)
 
     import torch
