@@ -292,7 +292,7 @@ def test_concatenated_projections_equal_separate(c, M):
 
 
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[4], MX_CFGS[0]], ids=_ids)
-@pytest.mark.parametrize("M,dt", [(1, "bf16"), (2, "f32"), (3, "bf16"), (16, "bf16")])
+@pytest.mark.parametrize("M,dt", [(1, "bf16"), (2, "f32"), (3, "bf16"), (4, "f32"), (16, "bf16")])
 def test_linear_equals_quantize_then_gemm(c, M, dt):
     """sdq_linear (one fused kernel on the decode path) == the two-call path, bit for bit."""
     torch = torch_cuda()
