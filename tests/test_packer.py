@@ -209,6 +209,12 @@ def test_error_paths():
     assert L.sdq_check(C.byref(bf), 32, 128) == 0
     assert L.sdq_gemm(C.byref(bf), C.c_void_p(16), C.c_void_p(16), 1, C.c_void_p(16), 32, 128,
                       C.c_void_p(18), None) == -2
+    dual = sdq.Config.dual_family().c()
+    p16 = C.c_void_p(16)
+    assert L.sdq_gemm_dual(C.byref(dual), p16, p16, p16, p16, 1, p16, 32, 128, C.c_void_p(18), None) == -2
+    assert L.sdq_gemm_dual(C.byref(dual), p16, p16, p16, p16, 1, p16, 32, 120, p16, None) == -2  # K % 128
+    assert L.sdq_gemm_dual(C.byref(dual), None, p16, p16, p16, 1, p16, 32, 128, p16, None) == -1
+    assert L.sdq_gemm_dual(C.byref(cfg), p16, p16, p16, p16, 1, p16, 32, 128, p16, None) == -3  # INT config
     for s in list(_lib.STATUS) + [123]:
         assert L.sdq_status_string(s)
 
