@@ -194,28 +194,28 @@ __device__ __forceinline__ uint32_t e2m1_rne(float t) {
   return mag | ((__float_as_uint(t) >> 28) & 8u);
 }
 
-// One workgroup per token, two passes over the row (the second from L2):
-// the row amax, then per 8-element piece the int8 codes, the block amax of
-// the four pieces of its 32-K block (lanes 4j..4j+3 of a wave), and the fp4
-// codes.
-template <bool BF16>
-__global__ __launch_bounds__(kThreads) void act_quant_dual(const void* __restrict__ X, int64_t K,
-                                                           uint8_t* __restrict__ Xo, float* __restrict__ s_a,
-                                                           uint8_t* __restrict__ Xi, uint8_t* __restrict__ Ea) {
-  __shared__ float red[4];
+// One workgroup of NT threads per token, two passes over the row (the
+// second from L2): the row amax, then per 8-element piece the int8 codes, the
+// block amax of the four pieces of its 32-K block (lanes 4j..4j+3 of a wave),
+// and the fp4 codes.
+template <bool BF16, int NT>
+__global__ __launch_bounds__(NT) void act_quant_dual(const void* __restrict__ X, int64_t K,
+                                                     uint8_t* __restrict__ Xo, float* __restrict__ s_a,
+                                                     uint8_t* __restrict__ Xi, uint8_t* __restrict__ Ea) {
+  __shared__ float red[NT / 64];
   const int64_t m = blockIdx.x;
   const int64_t P = K >> 3;  // pieces of 8 elements, a multiple of 16
   float amax = 0.f;
-  for (int64_t p = threadIdx.x; p < P; p += kThreads) {
+  for (int64_t p = threadIdx.x; p < P; p += NT) {
     float v[8];
     load8<BF16>(X, m * K + p * 8, v);
 #pragma unroll
     for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
   }
-  amax = block_max<kThreads>(amax, red);
+  amax = block_max<NT>(amax, red);
   const float inv = amax > 0.f ? 127.f / amax : 0.f;
   if (threadIdx.x == 0) s_a[m] = amax / 127.f;
-  for (int64_t base = 0; base < P; base += kThreads) {  // the same trip count for every lane
+  for (int64_t base = 0; base < P; base += NT) {  // the same trip count for every lane
     const int64_t p = base + threadIdx.x;
     const bool ok = p < P;
     float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -240,11 +240,21 @@ __global__ __launch_bounds__(kThreads) void act_quant_dual(const void* __restric
 
 hipError_t launch_act_quant_dual(const void* X, int x_dtype, int64_t M, int64_t K, uint8_t* Xo,
                                  float* s_a, uint8_t* Xi, uint8_t* Ea, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(M)), block(kThreads);
-  if (x_dtype == SDQ_DTYPE_BF16)
-    hipLaunchKernelGGL((act_quant_dual<true>), grid, block, 0, st, X, K, Xo, s_a, Xi, Ea);
-  else
-    hipLaunchKernelGGL((act_quant_dual<false>), grid, block, 0, st, X, K, Xo, s_a, Xi, Ea);
+  // few tokens: more threads per token (measured at M = 1: one 256-thread
+  // workgroup takes about 5 us on a 4096..11008-wide row)
+  const dim3 grid(static_cast<unsigned>(M));
+  const int64_t P = K / 8;
+  const bool bf16 = x_dtype == SDQ_DTYPE_BF16;
+  if (M < 256 && P >= 1024) {
+    if (bf16) hipLaunchKernelGGL((act_quant_dual<true, 1024>), grid, dim3(1024), 0, st, X, K, Xo, s_a, Xi, Ea);
+    else hipLaunchKernelGGL((act_quant_dual<false, 1024>), grid, dim3(1024), 0, st, X, K, Xo, s_a, Xi, Ea);
+  } else if (M < 256 && P >= 512) {
+    if (bf16) hipLaunchKernelGGL((act_quant_dual<true, 512>), grid, dim3(512), 0, st, X, K, Xo, s_a, Xi, Ea);
+    else hipLaunchKernelGGL((act_quant_dual<false, 512>), grid, dim3(512), 0, st, X, K, Xo, s_a, Xi, Ea);
+  } else {
+    if (bf16) hipLaunchKernelGGL((act_quant_dual<true, kThreads>), grid, dim3(kThreads), 0, st, X, K, Xo, s_a, Xi, Ea);
+    else hipLaunchKernelGGL((act_quant_dual<false, kThreads>), grid, dim3(kThreads), 0, st, X, K, Xo, s_a, Xi, Ea);
+  }
   return hipGetLastError();
 }
 

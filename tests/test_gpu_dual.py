@@ -58,7 +58,7 @@ def _check(Y, X, W, cfg_o, what):
 
 
 @pytest.mark.parametrize("M,K", [(1, 128), (5, 256), (64, 4096), (33, 1024),
-                                 (300, 512)])
+                                 (300, 512), (1, 4096), (2, 11008), (1, 16384)])
 @pytest.mark.parametrize("bf16", [False, True])
 def test_act_quant_dual_bit_exact(M, K, bf16):
     rng = np.random.default_rng(M + K)
