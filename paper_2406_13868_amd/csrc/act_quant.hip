@@ -7,9 +7,9 @@
 //                                 or saturated to +-448 (fp8 e4m3)
 // A zero row gives s_a = 0 and zero codes.
 //
-// One workgroup per row: 256 threads, or 1024 when there are few rows and
-// they are wide (so that the few compute units busy keep four times the loads
-// in flight).  Rows up to 8 pieces of 8 elements per thread are read once
+// One workgroup per row: 256 threads, or 512 / 1024 when there are few rows
+// and they are 2K..8K / wider (so that the few compute units busy keep more
+// loads in flight).  Rows up to 8 pieces of 8 elements per thread are read once
 // into registers (16-byte loads), reduced by a DPP/permlane wave maximum and
 // LDS, then quantized and written back with 8-byte stores; wider rows take a
 // second pass over the (L2-resident) row.  The pass is HBM-bound: K*(in+1)
@@ -154,7 +154,7 @@ hipError_t launch_typed(const void* X, int64_t M, int64_t K, uint8_t* Xq, float*
   const dim3 grid(static_cast<unsigned>(M)), block(kThreads);
   const int64_t pieces = K / 8;
   // few wide rows: 1024 threads per row
-  if (M < 256 && pieces > kThreads * 4 && pieces <= 4096 * 2) {
+  if (M < 256 && pieces > 1024 && pieces <= 4096 * 2) {
     const dim3 big(1024);
     if (pieces <= 1024 * 2)
       hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 2, 1024>), grid, big, 0, st, X, K, Xq, s_a);
@@ -162,6 +162,14 @@ hipError_t launch_typed(const void* X, int64_t M, int64_t K, uint8_t* Xq, float*
       hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 4, 1024>), grid, big, 0, st, X, K, Xq, s_a);
     else
       hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 8, 1024>), grid, big, 0, st, X, K, Xq, s_a);
+    return hipGetLastError();
+  }
+  if (M < 256 && pieces > kThreads && pieces <= 1024) {  // few rows of 2K..8K elements: 512 threads per row
+    const dim3 mid(512);
+    if (pieces <= 512)
+      hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 1, 512>), grid, mid, 0, st, X, K, Xq, s_a);
+    else
+      hipLaunchKernelGGL((act_quant_regs<BF16, E4M3, 2, 512>), grid, mid, 0, st, X, K, Xq, s_a);
     return hipGetLastError();
   }
   if (pieces <= 1 * kThreads)
