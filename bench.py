@@ -73,7 +73,7 @@ def parse():
     p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
     p.add_argument("--inlier-scale", default="", choices=["", "e4m3"],
                    help="INT family: two-level e4m3 inlier scales instead of the workload's fp16 "
-                        "(the quantized scale format of the paper's Section 7 study)")
+                        "(the quantized scale format of the paper's Section 6.4 study)")
     p.add_argument("--y-dtype", default="f32", choices=["f32", "bf16"],
                    help="GEMM output type (bf16: the fp32 result rounded to nearest even)")
     p.add_argument("--rotate-mb", type=float, default=512.0)

@@ -100,7 +100,7 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  *           (SDQ_METRIC_MAGNITUDE) or |W| * act_norm[k] (SDQ_METRIC_PRODUCT,
  *           Wanda's weight-activation product)
  *   decomp  metric that picks the outliers among the kept weights (Section
- *           5, Stage 2; the variants of Section 7's decomposition study):
+ *           5, Stage 2; the variants of Section 6.4's decomposition study):
  *           SDQ_DECOMP_SAME (the significance metric), _MAGNITUDE, _PRODUCT,
  *           _ERROR (the error the inlier quantizer would make on the weight)
  *           or _OUTPUT_ERROR (that error times act_norm[k])
@@ -109,7 +109,7 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  * decomp = SAME with order = LARGE (both zero) is the default; any other
  * choice needs n_o = 1.
  *   sfmt_i  inlier scale format (Section 3.3: scales are quantized too;
- *           Section 7 compares 8-bit scale formats): SDQ_SCALE_DEFAULT (INT
+ *           Section 6.4 compares 8-bit scale formats): SDQ_SCALE_DEFAULT (INT
  *           fp16 per 16 K, MX e8m0 per 32 K) or, INT family only,
  *           SDQ_SCALE_E4M3: VS-Quant's two levels, an fp8-e4m3 scale per 16
  *           K times one power-of-two scale 2^E per row, E the smallest with

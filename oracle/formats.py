@@ -14,7 +14,7 @@ VS-Quant).  The exact encodings follow the public format definitions:
 * E8M0 (OCP MX shared scale): an unsigned biased exponent, value 2^(c-127);
   code 255 is NaN.
 * ufp8 E6M2 (the unsigned scale format of the paper's quantization study,
-  Section 7): 6 exponent bits with bias 31, 2 mantissa bits, no sign;
+  Section 6.4): 6 exponent bits with bias 31, 2 mantissa bits, no sign;
   exponent field 0 encodes subnormals m/4 * 2^-30; every code is finite
   (the largest is 1.75 * 2^32).
 * fp16: IEEE binary16 (numpy's float16 cast is round-to-nearest-even).

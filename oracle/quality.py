@@ -12,11 +12,11 @@ decomposed and quantized weights (Section 5.1), for
     sparsity (every position an inlier: int4 with fp16 scales per 16, or
     e2m1 with e8m0 per 32, activations int8 / e4m3 per token), and
   * SDQ with each decomposition metric (same, magnitude, product, error,
-    output error) in each order (Large, Small) of Section 7's study, with
+    output error) in each order (Large, Small) of Section 6.4's study, with
     the magnitude or the product significance metric for sparsification.
 
 It also reports, for the int family, the inlier scale format (fp16, the
-two-level e4m3 of VS-Quant, ufp8-e6m2; Section 7's quantization study) and
+two-level e4m3 of VS-Quant, ufp8-e6m2; Section 6.4's quantization study) and
 the Q-Vector size (16, 32, 64 dense positions per scale; Section 3.3) next to
 the resulting logical bits per weight.
 

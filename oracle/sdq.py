@@ -18,7 +18,7 @@ Paper passages followed (Jeong et al., SDQ):
 * The decomposition metric may differ from the significance metric and be
   taken in either order: magnitude, weight-activation product, or the error
   the inlier quantizer makes on the weight (alone or times the activation
-  norm), "Large" or "Small" (Section 5, "Stage 2", and Section 7's
+  norm), "Large" or "Small" (Section 5, "Stage 2", and Section 6.4's
   decomposition study).  These run the two stages in the paper's order.
 * Stage 3 quantizes each branch with per-vector (VS-Quant) scale factors,
   outliers at a higher precision than inliers; activations are quantized too
@@ -189,7 +189,7 @@ def top_n_by_key(key: np.ndarray, allowed: np.ndarray, m: int, n: int):
 def inlier_error(W: np.ndarray, keep: np.ndarray, cfg: Config) -> np.ndarray:
     """|W - deq Q_i(W)| on the kept positions (0 elsewhere), fp32: the error the
     inlier quantizer (scales over the kept positions of each block) makes on
-    every kept weight -- the quantization error of Section 7's error-based
+    every kept weight -- the quantization error of Section 6.4's error-based
     decomposition metric."""
     W = np.asarray(W, dtype=np.float32)
     q, scale, row = quantize_inliers(W, keep, cfg)

@@ -183,6 +183,46 @@ def _dev(t, what: str):
     return C.c_void_p(t.data_ptr())
 
 
+def _need(t, shape, dtype, what: str):
+    """Check a caller-supplied tensor before its pointer reaches the library,
+    which cannot see sizes: exact shape and dtype (placement and contiguity are
+    checked where the pointer is taken)."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what} must be a torch tensor")
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{what} must be {list(shape)} {dtype}, got {list(t.shape)} {t.dtype}")
+    return t
+
+
+def _need_bytes(t, nbytes: int, what: str):
+    """A raw byte buffer (packed weights, workspace): at least nbytes."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what} must be a torch tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what} holds {have} bytes, needs {nbytes}")
+    return t
+
+
+def _x_dtype(X):
+    import torch
+    if X.dtype == torch.float32:
+        return DTYPE_F32
+    if X.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    raise ValueError("X must be float32 or bfloat16")
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) > 1:
+        raise ValueError(f"tensors are on different devices: {sorted(map(str, devs))}")
+
+
 def _out(out, M: int, N: int, cfg: Config, device):
     """The GEMM output: `out` checked against [M, N] of cfg's output dtype, or a new tensor."""
     import torch
@@ -197,15 +237,15 @@ def _out(out, M: int, N: int, cfg: Config, device):
 def quantize_act(X, cfg: Config, out=None, scales=None, stream=None):
     """Per-token activation quantization on the GPU: returns (Xq uint8, s_a f32)."""
     import torch
+    if X.dim() != 2:
+        raise ValueError("X must be [M, K]")
     M, K = X.shape
-    if X.dtype == torch.float32:
-        dt = DTYPE_F32
-    elif X.dtype == torch.bfloat16:
-        dt = DTYPE_BF16
-    else:
-        raise ValueError("X must be float32 or bfloat16")
+    dt = _x_dtype(X)
     Xq = out if out is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
     s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
+    _need(Xq, (M, K), torch.uint8, "Xq")
+    _need(s_a, (M,), torch.float32, "s_a")
+    _same_device(X, Xq, s_a)
     _lib.check(_lib.lib().sdq_quantize_act(C.byref(cfg.c()), _dev(X, "X"), dt, M, K,
                                            _dev(Xq, "Xq"), _dev(s_a, "s_a"), _stream(stream)),
                "sdq_quantize_act")
@@ -217,13 +257,10 @@ def quantize_act_dual(X, cfg: Config, out=None, stream=None):
     s_a_o f32 [M], Xq_i uint8 [M, K/2] fp4 nibbles, e_a_i uint8 [M, K/32] e8m0),
     written into `out` (a tuple of those four tensors) when given."""
     import torch
+    if X.dim() != 2:
+        raise ValueError("X must be [M, K]")
     M, K = X.shape
-    if X.dtype == torch.float32:
-        dt = DTYPE_F32
-    elif X.dtype == torch.bfloat16:
-        dt = DTYPE_BF16
-    else:
-        raise ValueError("X must be float32 or bfloat16")
+    dt = _x_dtype(X)
     dev = X.device
     if out is not None:
         Xo, s_a, Xi, Ea = out
@@ -232,6 +269,11 @@ def quantize_act_dual(X, cfg: Config, out=None, stream=None):
         s_a = torch.empty((M,), dtype=torch.float32, device=dev)
         Xi = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
         Ea = torch.empty((M, K // 32), dtype=torch.uint8, device=dev)
+    _need(Xo, (M, K), torch.uint8, "Xq_o")
+    _need(s_a, (M,), torch.float32, "s_a_o")
+    _need(Xi, (M, K // 2), torch.uint8, "Xq_i")
+    _need(Ea, (M, K // 32), torch.uint8, "e_a_i")
+    _same_device(X, Xo, s_a, Xi, Ea)
     _lib.check(_lib.lib().sdq_quantize_act_dual(C.byref(cfg.c()), _dev(X, "X"), dt, M, K, _dev(Xo, "Xq_o"),
                                                 _dev(s_a, "s_a_o"), _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"),
                                                 _stream(stream)), "sdq_quantize_act_dual")
@@ -241,12 +283,16 @@ def quantize_act_dual(X, cfg: Config, out=None, stream=None):
 def gemm_dual(Xo, s_a, Xi, Ea, packed, N: int, K: int, cfg: Config, out=None, stream=None):
     """The dual family's GEMM on the GPU (output [M, N], fp32 or bf16 by cfg.y_dtype)."""
     import torch
+    if Xo.dim() != 2:
+        raise ValueError("Xq_o must be [M, K]")
     M = Xo.shape[0]
-    if Xo.shape[1] != K or Xi.shape[1] * 2 != K or Ea.shape[1] * 32 != K:
-        raise ValueError("activations have the wrong K")
-    if packed.numel() < pack_size(cfg, N, K):
-        raise ValueError("packed buffer too small")
+    _need(Xo, (M, K), torch.uint8, "Xq_o")
+    _need(s_a, (M,), torch.float32, "s_a_o")
+    _need(Xi, (M, K // 2), torch.uint8, "Xq_i")
+    _need(Ea, (M, K // 32), torch.uint8, "e_a_i")
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
     Y = _out(out, M, N, cfg, Xo.device)
+    _same_device(Xo, s_a, Xi, Ea, packed, Y)
     _lib.check(_lib.lib().sdq_gemm_dual(C.byref(cfg.c()), _dev(Xo, "Xq_o"), _dev(s_a, "s_a_o"),
                                         _dev(Xi, "Xq_i"), _dev(Ea, "e_a_i"), M, _dev(packed, "packed"),
                                         N, K, _dev(Y, "Y"), _stream(stream)), "sdq_gemm_dual")
@@ -269,12 +315,14 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
     `workspace` (a uint8 CUDA tensor of at least gemm_workspace_size bytes)
     or a fresh one."""
     import torch
+    if Xq.dim() != 2:
+        raise ValueError("Xq must be [M, K]")
     M = Xq.shape[0]
-    if Xq.shape[1] != K:
-        raise ValueError("Xq has the wrong K")
-    if packed.numel() < pack_size(cfg, N, K):
-        raise ValueError("packed buffer too small")
+    _need(Xq, (M, K), torch.uint8, "Xq")
+    _need(s_a, (M,), torch.float32, "s_a")
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
     Y = _out(out, M, N, cfg, Xq.device)
+    _same_device(Xq, s_a, packed, Y, workspace)
     ws_bytes = gemm_workspace_size(cfg, M, N, K, path)
     if ws_bytes == 0:
         _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
@@ -283,6 +331,7 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
         return Y
     ws = workspace if workspace is not None else torch.empty(ws_bytes, dtype=torch.uint8,
                                                              device=Xq.device)
+    _need_bytes(ws, ws_bytes, "workspace")
     _lib.check(_lib.lib().sdq_gemm_ws(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
                                       _dev(packed, "packed"), N, K, _dev(Y, "Y"),
                                       _dev(ws, "workspace"), ws.numel() * ws.element_size(),
@@ -297,18 +346,17 @@ def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=Non
     sdq_gemm_ws where the GEMM takes a workspace; otherwise sdq_linear's two
     kernels back to back."""
     import torch
+    if X.dim() != 2 or X.shape[1] != K:
+        raise ValueError(f"X must be [M, {K}], got {list(X.shape)}")
     M = X.shape[0]
-    if X.shape[1] != K:
-        raise ValueError("X has the wrong K")
-    if X.dtype == torch.float32:
-        dt = DTYPE_F32
-    elif X.dtype == torch.bfloat16:
-        dt = DTYPE_BF16
-    else:
-        raise ValueError("X must be float32 or bfloat16")
+    dt = _x_dtype(X)
     Xq = xq if xq is not None else torch.empty((M, K), dtype=torch.uint8, device=X.device)
     s_a = scales if scales is not None else torch.empty((M,), dtype=torch.float32, device=X.device)
+    _need(Xq, (M, K), torch.uint8, "Xq")
+    _need(s_a, (M,), torch.float32, "s_a")
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
     Y = _out(out, M, N, cfg, X.device)
+    _same_device(X, Xq, s_a, packed, Y, workspace)
     if gemm_workspace_size(cfg, M, N, K) > 0:
         quantize_act(X, cfg, out=Xq, scales=s_a, stream=stream)
         gemm(Xq, s_a, packed, N, K, cfg, out=Y, stream=stream, workspace=workspace)

@@ -14,7 +14,7 @@ namespace sdq {
 // XCD b % 8, each with its own L2).  This maps b to a work index so that every
 // XCD takes a contiguous range of the G indices: neighbouring work items,
 // which share cache lines, meet in one L2.  It is a bijection on [0, G).
-__device__ __forceinline__ int xcd_contiguous(int b, int G) {
+__host__ __device__ __forceinline__ int xcd_contiguous(int b, int G) {
   const int x = b & 7, i = b >> 3, q = G >> 3, rem = G & 7;
   return x * q + min(x, rem) + i;
 }
@@ -26,7 +26,7 @@ __device__ __forceinline__ int xcd_contiguous(int b, int G) {
 // activations of half the tokens while the weights of a group are read by
 // one XCD per half.  Below 8 token blocks it is plain (group, token block).
 // A bijection on [0, G * MB).
-__device__ __forceinline__ void tile_work(int b, int G, int MB, int& group, int& mblock) {
+__host__ __device__ __forceinline__ void tile_work(int b, int G, int MB, int& group, int& mblock) {
   const int L = xcd_contiguous(b, G * MB);
   const int h0 = MB >= 8 ? (MB + 1) / 2 : MB;  // token blocks of the first half
   if (L < G * h0) {

@@ -6,7 +6,7 @@
 //              become the inliers; everything else is pruned.  Significance
 //              is |w| or |w| * act_norm[k] (Wanda's product metric); ties go
 //              to the lower k.  With a separate decomposition metric (the
-//              variants of Section 7's decomposition study) the stages run in
+//              variants of Section 6.4's decomposition study) the stages run in
 //              the paper's order instead: sparsify every 8-group to
 //              n_o + n_i kept positions, then extract the outliers among the
 //              kept ones by that metric, largest or smallest first.

@@ -435,7 +435,7 @@ def test_mx_unmergeable_blocks(kind, n_i, M, N, K, path):
                                                     ("mx", "e4m3", "product", "small"),
                                                     ("mx", "e4m3", "error", "large")])
 def test_decomposition_variants_end_to_end(fam, fmt_o, decomp, order):
-    """Weights packed with another decomposition metric and order (Section 7's
+    """Weights packed with another decomposition metric and order (Section 6.4's
     decomposition study) go through the same kernels: the GEMM matches the
     oracle's product of its own decomposition on every path."""
     import dataclasses

@@ -1,5 +1,5 @@
 """Pins for the decomposition-metric variants of the oracle (Section 5,
-"Stage 2", and Section 7's decomposition study: magnitude, weight-activation
+"Stage 2", and Section 6.4's decomposition study: magnitude, weight-activation
 product and quantization-error metrics, taken "Large" or "Small").
 
 What pins them (none re-types the oracle's formula):

@@ -163,6 +163,36 @@ def test_reconstruction_error_bounds(cfg):
         assert (err[mo] <= np.maximum(2.0 ** -4 * np.abs(W64[mo]), 2.0 ** -10 * Eo[mo]) + 64 * Eo[mo] * (np.abs(W64[mo]) / Eo[mo] > 448)).all()
 
 
+@pytest.mark.parametrize("cfg", [INT18, INT18_I8, INT116], ids=["e4m3-1:8", "int8-1:8", "e4m3-1:16"])
+def test_row_outlier_scale_maps_the_row_maximum_to_qmax(cfg):
+    """INT family, one outlier scale per row (reading R5: s_o = amax/qmax).  The
+    outlier of largest magnitude in each row must come out as +-qmax: 448, the
+    largest finite OCP E4M3FN value (codes 0x7E / 0xFE), or 127 for int8; no
+    other outlier exceeds it, and |code| decodes back to |w| / s_o within half
+    a step.  A wrong qmax (240, the fnuz maximum, or 127 for e4m3) or a scale
+    taken over the inliers instead of the outliers fails here."""
+    W = synth.make_w(2, 0, 64, 512)
+    L = S.pack_logical(W, cfg)
+    mo, code = L["mask_o"], L["code_o_dense"]
+    qmax = 127.0 if cfg.fmt_o == "int8" else 448.0
+    if cfg.fmt_o == "int8":
+        v = code.view(np.int8).astype(np.float64)
+    else:
+        v = F.e4m3_decode(code)
+    absW = np.where(mo, np.abs(W), 0)
+    for n in range(W.shape[0]):
+        k = int(np.argmax(absW[n]))
+        assert mo[n, k] and absW[n, k] > 0
+        assert abs(v[n, k]) == qmax, (n, k, v[n, k])
+        if cfg.fmt_o == "e4m3":
+            assert code[n, k] in (0x7E, 0xFE)
+        else:
+            assert code[n, k] in (127, 129)  # +127 / -127 as int8 bits
+        assert np.abs(v[n][mo[n]]).max() == qmax
+        # the scale is the row amax over the outliers only, divided by qmax
+        assert np.float32(L["scale_o"][n]) == np.float32(np.float32(absW[n, k]) / np.float32(qmax))
+
+
 def test_int4_unit_scale_grid_is_exact():
     """Blocks whose inlier amax is 7 get s = 1 and integer codes equal to W."""
     rng = np.random.default_rng(5)

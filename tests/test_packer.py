@@ -305,7 +305,7 @@ def test_absent_outlier_position_is_free(c):
         assert not np.any(absent & (po == pj)), f"slot {j}"
 
 
-# ---- decomposition-metric variants (Section 5, "Stage 2"; Section 7's study)
+# ---- decomposition-metric variants (Section 5, "Stage 2"; Section 6.4's study)
 DECOMPS = [(d, o) for d in ("same", "magnitude", "product", "error", "output_error")
            for o in ("large", "small") if (d, o) != ("same", "large")]
 
