@@ -7,9 +7,15 @@ every layer of the workload, per-token activation quantization
 (sdq_quantize_act) followed by the decomposed GEMM (sdq_gemm).  The weights
 were packed offline (sdq_pack, host); the packer's time is reported beside
 the line, never inside the step.  Every input is resident in HBM when the
-timed region starts, and distinct copies of the packed weights (>= 512 MB,
-twice the 256 MB Infinity Cache) are rotated so each launch streams its
-weights from HBM.
+timed region starts: distinct copies of the packed weights, activations and
+outputs (>= 512 MB, twice the 256 MB Infinity Cache) are rotated, and a
+512 MB fill runs between the untimed and the timed graph replay, so that each
+timed launch streams its weights from HBM whatever the step count.
+
+The default workload is the LLaMA-7B MLP prefill (gate, up and down
+projections at 2048 tokens, MX 1:8 e4m3 + 2:8 e2m1); the same line carries the
+LLaMA-7B attention-projection decode (one token, INT 1:8 e4m3 + 3:8 int4)
+under "decode", with its own HBM roofline.
 
 Prints one JSON line: dense-equivalent TFLOP/s of the step (2*M*N*K per layer),
 the roofline object of the dominant kernel (the GEMM) measured with HIP events
@@ -33,7 +39,7 @@ import numpy as np  # noqa: E402
 import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
-MFMA_PEAK_TFLOPS = {"fp8": 5033.0, "f16": 2516.6}
+FLUSH_BYTES = 512 * 1024 * 1024  # twice the Infinity Cache
 
 WORKLOADS = {
     # name: (workload id, layer indices, M)
@@ -65,8 +71,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="llama7b-attn-decode",
+    p.add_argument("--workload", default="llama7b-mlp-prefill",
                    help="|".join(WORKLOADS) + "|sweep (with --layer/--M/--fmt)")
+    p.add_argument("--no-decode", action="store_true",
+                   help="leave out the LLaMA-7B attention decode figures that the default line carries")
     p.add_argument("--layer", type=int, default=0, help="block-sweep layer index (0..6)")
     p.add_argument("--M", type=int, default=0,
                    help="token count: block sweep (default 1) or the dual block workload (default 4096)")

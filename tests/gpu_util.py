@@ -5,14 +5,36 @@ import numpy as np
 import pytest
 
 REL_TOL = 1e-3  # max relative error (1%-RMS floor) and normwise relative error vs the fp64 oracle
-# MX family: gfx950's scaled fp8/fp4 matrix instruction sums its 64 products in a
-# fixed-point window about 2^-17.5 below the largest product of the instruction
-# (measured), so outputs that cancel lose relative accuracy.  The check there is
-# normwise <= 1e-3 plus a componentwise bound against the sum of |terms|: at
-# most 32 nonzero products per instruction (1 outlier + 3 inliers per 8), each
-# off by less than one window unit, give at most 32 * 2^-17.5 = 2^-12.5 of the
-# sum of |terms|; 2^-12 leaves room for the measured window.
-MX_TERM_TOL = 2.0 ** -12
+
+# gfx950's scaled matrix instruction (v_mfma_scale_f32_32x32x64_f8f6f4), which
+# the MX and dual families use, is not an exact dot product.  What it does with
+# their products is pinned on designed inputs in test_gpu_mx_accumulation.py:
+#   * its products reach the fp32 accumulator as partial sums of 16 K (fp8
+#     operands) or 32 K (fp4 x fp4), each rounded to nearest even as it is
+#     added: at most 2^-24 of the running sum, which is at most the sum of
+#     |terms|, per partial sum.  An MX output takes K/16 of them, or up to K/8
+#     where blocks that cannot merge their inliers into the outliers' fp8
+#     operand add them with a second (fp8 x fp4) instruction;
+#   * inside one 32-K scale block a dominant product costs the others low-order
+#     bits: at most 2^-12 of the block's largest product (worst found on the
+#     workload data: 2^-12.58, a product of 72 among eleven below 0.22).
+# With the final scaling by s_a and the store (two more roundings), and the sum
+# of the blocks' largest products bounded by the sum of |terms|, an MX output
+# satisfies |Y - Y_ref| <= (2^-12 + (K/8 + 2) * 2^-24) * sum_k |a_k w_k|.
+# In the dual family's fp4 x fp4 branch every product of a block lies within
+# 2^7.2 of the block's largest (e2m1 codes on both sides, one scale per block
+# each) and has at most 4 significant bits, so no block loses bits inside the
+# 12-bit window; only the roundings remain: (K/32 + 2) * 2^-24, plus nothing
+# for the int8 outlier branch, which is exact in int32.
+MX_BLOCK_LOSS = 2.0 ** -12
+
+
+def mx_term_tol(K: int) -> float:
+    return MX_BLOCK_LOSS + (K / 8 + 2) * 2.0 ** -24
+
+
+def dual_term_tol(K: int) -> float:
+    return (K / 32 + 2) * 2.0 ** -24
 
 
 def torch_cuda():
@@ -45,10 +67,10 @@ def assert_close(Y, Yref, what=""):
     return mr, nr
 
 
-def assert_close_terms(Y, Yref, Tabs, what=""):
-    """Normwise <= REL_TOL and |Y - Yref| <= MX_TERM_TOL * sum_k |a_k w_k| per output."""
+def assert_close_terms(Y, Yref, Tabs, K, what=""):
+    """MX family: normwise <= REL_TOL and |Y - Yref| <= mx_term_tol(K) * sum_k |a_k w_k| per output."""
     Y = np.asarray(Y, np.float64)
     _, nr = rel_errors(Y, Yref)
     comp = float(np.max(np.abs(Y - Yref) / np.maximum(Tabs, 1e-30))) if Y.size else 0.0
-    assert nr <= REL_TOL and comp <= MX_TERM_TOL, f"{what}: norm_rel={nr:.3e} term_rel={comp:.3e}"
+    assert nr <= REL_TOL and comp <= mx_term_tol(K), f"{what}: norm_rel={nr:.3e} term_rel={comp:.3e}"
     return nr, comp

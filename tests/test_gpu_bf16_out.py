@@ -17,7 +17,7 @@ import pytest
 
 import synth
 from oracle import sdq as S
-from tests.gpu_util import MX_TERM_TOL, say, torch_cuda
+from tests.gpu_util import mx_term_tol, say, torch_cuda
 
 import paper_2406_13868_amd as sdq
 
@@ -123,7 +123,7 @@ def test_bf16_with_unmerged_blocks_matches_oracle(path):
     Yref, _, _, _ = S.reference(X, W, cfg_o)
     A = np.abs(S.dequant_act(*S.quantize_act(X, cfg_o), cfg_o))
     T = A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
-    excess = np.abs(Y - Yref) - (2.0 ** -8 * np.abs(Yref) + (2.0 ** -9 + MX_TERM_TOL) * T)
+    excess = np.abs(Y - Yref) - (2.0 ** -8 * np.abs(Yref) + (2.0 ** -9 + mx_term_tol(K)) * T)
     assert float(excess.max()) <= 0.0, f"worst excess {float(excess.max()):.3e}"
 
 

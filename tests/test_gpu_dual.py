@@ -6,25 +6,22 @@ X -> sdq_quantize_act_dual (GPU) -> A_o, A_i; W -> sdq_pack (host) ->
 sdq_gemm_dual (GPU).  The expected values come from the oracle alone.
 
 Tolerance: the outlier branch is exact in int32.  The inlier branch runs
-gfx950's scaled fp4 x fp4 matrix instruction, which sums its products in a
-fixed-point window about 2^-17.5 below the instruction's largest product (as
-the MX family measures).  One instruction holds at most 64 nonzero products
-per output, so an output is off by at most 64 * 2^-17.5 = 2^-11.5 of the sum of
-|terms|; the check takes 2^-11 componentwise plus 1e-3 normwise.
+gfx950's scaled fp4 x fp4 matrix instruction, which adds its products to the
+fp32 accumulator as partial sums of 32 K, each rounded to nearest even; inside
+a scale block every fp4 x fp4 product is exact in the instruction's window
+(tests/gpu_util.py, dual_term_tol).  An output is therefore off by at most
+(K/32 + 2) * 2^-24 of the sum of |terms|, and 1e-3 normwise.
 """
 import numpy as np
 import pytest
 
 import synth
 from oracle import sdq as S
-from tests.gpu_util import REL_TOL, rel_errors, say, torch_cuda
+from tests.gpu_util import REL_TOL, dual_term_tol, rel_errors, say, torch_cuda
 
 import paper_2406_13868_amd as sdq
 
 pytestmark = pytest.mark.gpu
-
-DUAL_TERM_TOL = 2.0 ** -11
-
 
 def _cfgs(n_o=1, n_i=6, metric="magnitude"):
     return (sdq.Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8", metric),
@@ -54,7 +51,8 @@ def _check(Y, X, W, cfg_o, what):
     T = np.abs(A_o) @ np.abs(S.dequant_outliers(L)).T + np.abs(A_i) @ np.abs(S.dequant_inliers(L)).T
     _, nr = rel_errors(Y, Yref)
     comp = float(np.max(np.abs(Y - Yref) / np.maximum(T, 1e-30))) if Y.size else 0.0
-    assert nr <= REL_TOL and comp <= DUAL_TERM_TOL, f"{what}: norm_rel={nr:.3e} term_rel={comp:.3e}"
+    say(f"{what}: norm_rel={nr:.3e} term_rel={comp:.3e}")
+    assert nr <= REL_TOL and comp <= dual_term_tol(W.shape[1]), f"{what}: norm_rel={nr:.3e} term_rel={comp:.3e}"
 
 
 @pytest.mark.parametrize("M,K", [(1, 128), (5, 256), (64, 4096), (33, 1024),

@@ -56,7 +56,7 @@ def abs_terms(X, W, cfg_o, act_norm=None):
 
 def check(Y, Yref, X, W, cfg_o, what="", act_norm=None):
     if cfg_o.family == "mx":
-        return assert_close_terms(Y, Yref, abs_terms(X, W, cfg_o, act_norm), what)
+        return assert_close_terms(Y, Yref, abs_terms(X, W, cfg_o, act_norm), W.shape[1], what)
     return assert_close(Y, Yref, what)
 
 
@@ -427,7 +427,7 @@ def test_mx_unmergeable_blocks(kind, n_i, M, N, K, path):
     Yref, _, _, _ = S.reference(X, W, cfg_o, an)
     A = np.abs(S.dequant_act(*S.quantize_act(X, cfg_o), cfg_o))
     T = A @ (np.abs(S.dequant_outliers(L)) + np.abs(S.dequant_inliers(L))).T
-    assert_close_terms(Y, Yref, T, f"{kind} n_i={n_i} M={M}")
+    assert_close_terms(Y, Yref, T, K, f"{kind} n_i={n_i} M={M}")
 
 
 @pytest.mark.parametrize("fam,fmt_o,decomp,order", [("int", "e4m3", "output_error", "small"),
