@@ -108,16 +108,42 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(name: str):
-    """HBM bytes per GEMM launch from committed counter runs, if they were taken
-    on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{name}.json")
+def profile_figures(kind: str, name: str):
+    """Counter figures of a workload from a committed rocprofv3 summary
+    (profiles/<kind>_<name>.txt, 'key: value' lines), used only while the
+    kernel-source hash recorded with them matches the current sources."""
+    path = os.path.join(ROOT, "profiles", f"{kind}_{name}.txt")
     if not os.path.exists(path):
         return None
-    d = json.load(open(path))
+    d = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            d[k.strip()] = v.strip()
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return d.get("hbm_bytes_per_launch")
+    d["source"] = f"profiles/{kind}_{name}.txt"
+    return d
+
+
+def host_description():
+    """CPU model and the BLAS numpy calls, for the CPU baseline."""
+    model = None
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = None
+    try:
+        cfg = np.show_config(mode="dicts")
+        b = cfg["Build Dependencies"]["blas"]
+        blas = f"{b.get('name')} {b.get('version', '')}".strip()
+    except Exception:  # pragma: no cover - older numpy
+        pass
+    return model, blas
 
 
 def main():
@@ -147,29 +173,65 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
         return
 
-    if a.workload == "sweep":
+    res = measure(a, torch, sdq, a.workload, a.M, full=True)
+    if res is None:  # counter-collection mode
+        return
+    line = {
+        "metric": "dense-equivalent TFLOP/s and % roofline of sdq_gemm, LLaMA-7B layer shapes",
+        "value": res["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": res["dtype"],
+        "data": "synthetic (seeded generators shaped like the named layers; no weights or datasets)",
+        "config": res["config"],
+        "roofline": res["roofline"],
+        "cpu_baseline": res["cpu_baseline"],
+    }
+    line.update(res["extra"])
+    if a.workload == "llama7b-mlp-prefill" and not a.no_decode and a.counters == 0:
+        d = measure(a, torch, sdq, "llama7b-attn-decode", 0, full=False)
+        line["decode"] = {"workload": d["config"]["workload"], "formats": d["config"]["formats"],
+                          "value": d["value"], "unit": "TFLOP/s", "ms_per_step": d["ms_per_step"],
+                          "roofline": d["roofline"],
+                          "gemm_dense_equiv_tflops": d["extra"]["gemm_dense_equiv_tflops"]}
+    print(json.dumps(line))
+
+
+def measure(a, torch, sdq, workload, M_arg, full):
+    """Time one workload: the step (activation quantization + GEMM of every
+    layer) and the GEMM alone, both as HIP graphs over rotated copies, after a
+    512 MB fill that leaves no weights in the Infinity Cache.  full: also the
+    vendor context and the CPU oracle."""
+    dev = torch.device("cuda:0")
+    if workload == "sweep":
         wid = 5
         fmt = synth.WORKLOADS[5].formats[a.fmt]
         layers = [a.layer]
-        M = a.M or 1
+        M = M_arg or 1
         wl_name = f"llama7b block sweep {synth.WORKLOADS[5].layers[a.layer].name} M={M} {fmt.label}"
     else:
-        wid, layers, M = WORKLOADS[a.workload]
-        if a.M and wid == 6:
-            M = a.M
+        wid, layers, M = WORKLOADS[workload]
+        if M_arg and wid == 6:
+            M = M_arg
         fmt = synth.WORKLOADS[wid].formats[0]
         wl_name = synth.WORKLOADS[wid].name
         if wid == 6:
             wl_name += f" M={M}"
     W_def = synth.WORKLOADS[wid]
     cfg = sdq.Config.of(fmt)
-    if a.inlier_scale:
+    if a.inlier_scale and full:
         import dataclasses
         if cfg.family != "int":
             raise SystemExit("--inlier-scale applies to the INT family only")
         cfg = dataclasses.replace(cfg, sfmt_i=a.inlier_scale)
         wl_name += f", {a.inlier_scale} inlier scales (two-level)"
-    if a.y_dtype != "f32":
+    if a.y_dtype != "f32" and full:
         import dataclasses
         cfg = dataclasses.replace(cfg, y_dtype=a.y_dtype)
         wl_name += f", {a.y_dtype} output"
@@ -184,7 +246,7 @@ def main():
         t0 = time.perf_counter()
         blob = sdq.pack(W, cfg)
         t_pack += time.perf_counter() - t0
-        if li == layers[0]:
+        if li == layers[0] and full:
             t0 = time.perf_counter()
             sdq.pack(W, cfg, n_threads=1)
             t_pack1 = time.perf_counter() - t0
@@ -208,7 +270,8 @@ def main():
     # the calls are ordered on one stream
     ws_bytes = 0 if dual else max(sdq.gemm_workspace_size(cfg, M, L.N, L.K) for L in Ls)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
-    stream = torch.cuda.current_stream()
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+
     def quant(r, j):
         if dual:
             sdq.quantize_act_dual(Xd[r][j], cfg, out=(Xq[r][j], sa[r][j], Xi[r][j], Ea[r][j]))
@@ -258,10 +321,15 @@ def main():
                 fn(start + i)
         return g
 
-    def timed(g, n):
+    def timed(g, n, cold=True):
+        """ms per call of one replay of g (n calls), timed with HIP events on the
+        launch stream between two synchronizations; with cold, a 512 MB fill
+        on the same stream first evicts the Infinity Cache (outside the events)."""
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         st = torch.cuda.current_stream()
+        if cold:
+            flush.fill_(1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(st)
         g.replay()
         e1.record(st)
@@ -276,7 +344,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"counter_launches": a.counters * len(Ls), "rotated_copies": R,
                           "kernel_source_hash": kernel_source_hash()}))
-        return
+        return None
 
     # ---------------------------------------------------------------- timed steps
     for i in range(a.warmup):
@@ -287,17 +355,18 @@ def main():
     ms_step = timed(g_step, a.steps)
 
     # ---------------------------------------------- the GEMM kernel alone (dominant kernel)
-    n_g = max(a.steps, 2 * R)
+    n_g = max(a.steps, 2 * R, 64)
     g_gemm = capture(gemms, n_g, 0)
     timed(g_gemm, n_g)
     gemm_us = timed(g_gemm, n_g) * 1e3
     gemm_hot_us = gemm_b2b_us = None
-    if a.context:
+    if a.context and full:
         g_hot = capture(gemms_hot, n_g, 0)
-        timed(g_hot, n_g)
-        gemm_hot_us = timed(g_hot, n_g) * 1e3
+        timed(g_hot, n_g, cold=False)
+        gemm_hot_us = round(timed(g_hot, n_g, cold=False) * 1e3, 3)
         # eager launches (host launch rate included)
         torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
         b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         b0.record(stream)
         for i in range(n_g):
@@ -305,61 +374,69 @@ def main():
         b1.record(stream)
         torch.cuda.synchronize()
         gemm_b2b_us = round(b0.elapsed_time(b1) * 1e3 / n_g, 3)
-        gemm_hot_us = round(gemm_hot_us, 3)
+    del g_step, g_gemm
 
     flops = sum(2.0 * M * L.N * L.K for L in Ls)
+    eff_frac = fmt.n_o / fmt.m_o + fmt.n_i / fmt.m_i
     y_bytes = 2 if cfg.y_dtype == "bf16" else 4
     alg_bytes = logical + sum(M * L.K + 4 * M + y_bytes * M * L.N for L in Ls)
     paths = [] if dual else sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
     hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family != "int" and M < 256)
+    tkey = workload if workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
+    if a.inlier_scale and full:
+        tkey += f"_{a.inlier_scale}_scales"
+    gemm_s = gemm_us * 1e-6
     if hbm_bound:
-        achieved = alg_bytes / (gemm_us * 1e-6) / 1e9
+        achieved = alg_bytes / gemm_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
-        achieved = flops / (gemm_us * 1e-6) / 1e12
-        peak = round(dual_mfma_peak(), 1) if dual else MFMA_PEAK_TFLOPS["fp8" if cfg.family == "mx" else "f16"]
+        achieved = flops / gemm_s / 1e12
+        # the contraction's own low-precision dtype: fp8 (MX), int8 x int4 (INT,
+        # priced at the int8 rate), and for the dual family the instruction mix
+        # of its fp4 x fp4 and int8 x int8 branches
+        peak = round(dual_mfma_peak(), 1) if dual else MFMA_PEAK["fp8" if cfg.family == "mx" else "int8"]
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
-    tkey = a.workload if a.workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
-    if a.inlier_scale:
-        tkey += f"_{a.inlier_scale}_scales"
-    roof["traffic"] = measured_traffic(tkey)
+        if dual:
+            roof["frac_of_fp4_dense_peak"] = round(achieved / MFMA_PEAK["fp4"], 4)
+        if cfg.family == "int":
+            # the INT matrix path issues f16 instructions (the exact hi/lo split)
+            roof["issued_dtype"] = "f16"
+            roof["frac_of_issued_dtype_peak"] = round(achieved / MFMA_PEAK["f16"], 4)
+        roof["effectual_tflops"] = round(flops * eff_frac / gemm_s / 1e12, 1)
+        mf = profile_figures("mfma", tkey)
+        if mf is not None:
+            # issued matrix work from SQ_INSTS_VALU_MFMA_MOPS_* x 512 per GEMM call, and
+            # the time those instructions take at their own dtypes' dense peaks
+            issued = float(mf["issued_flop_per_call"]) * len(Ls)
+            at_peak_s = float(mf["issued_us_at_peak_per_call"]) * 1e-6 * len(Ls)
+            roof["mfma_issued_tflops"] = round(issued / gemm_s / 1e12, 1)
+            roof["mfma_issued_frac"] = round(at_peak_s / gemm_s, 4)
+            roof["mfma_busy_frac"] = float(mf["mfma_busy_frac"])
+            roof["issued_over_effectual"] = round(issued / (flops * eff_frac), 3)
+            roof["mfma_counters_source"] = mf["source"]
+    tr = profile_figures("traffic", tkey)
+    roof["traffic"] = int(float(tr["hbm_bytes_per_launch"])) if tr else None
+    roof["traffic_source"] = (f"{tr['source']} (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE, copy-calibrated)"
+                              if tr else None)
     roof["kernel_us"] = round(gemm_us / len(Ls), 3)
     # kernels per GEMM call: the two-pass path's time is both passes together
     roof["kernels_per_call"] = 2 if sdq.PATH_DENSE in paths else 1
+    roof["timing"] = (f"HIP events around one graph replay of {n_g} GEMM calls over {R} rotated copies, "
+                      "after a 512 MB fill")
 
-    vendor = None if a.no_vendor else vendor_context(torch, Ls, M, a.rotate_mb, max(a.steps, 20))
-
-    # ---------------------------------------------------------------- CPU oracle
+    vendor = None if (a.no_vendor or not full) else vendor_context(torch, Ls, M, a.rotate_mb, max(a.steps, 20))
     cpu = None
-    if not a.no_cpu_baseline:
+    if full and not a.no_cpu_baseline:
         cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds, a.inlier_scale)
 
     value = flops / (ms_step * 1e-3) / 1e12
-    line = {
-        "metric": "dense-equivalent TFLOP/s and % roofline of sdq_gemm, LLaMA-7B layer shapes",
-        "value": round(value, 4),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": a.steps,
-        "warmup": a.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": {"int": "int8", "mx": "fp8", "dual": "int8+fp4"}[cfg.family],
-        "data": "synthetic (seeded generators shaped like the named layers; no weights or datasets)",
-        "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
-                   "formats": fmt.label,
-                   "gemm_path": "dual mfma" if dual else ["decode", "mfma", "dense (two passes)"][paths[-1] - 1],
-                   "parallelism": "none (one GPU)"},
-        "roofline": roof,
-        "cpu_baseline": cpu,
+    extra = {
         "gemm_us_graph": round(gemm_us, 3),
         "gemm_us_eager": gemm_b2b_us,
         "gemm_us_cache_resident": gemm_hot_us,
-        "gemm_dense_equiv_tflops": round(flops / (gemm_us * 1e-6) / 1e12, 3),
+        "gemm_dense_equiv_tflops": round(flops / gemm_s / 1e12, 3),
         "vendor_dense_context": vendor,
         "logical_bytes": int(logical),
         "physical_bytes": int(phys),
@@ -369,7 +446,18 @@ def main():
         "packer_s_one_thread_first_layer": round(t_pack1, 3),
         "kernel_source_hash": kernel_source_hash(),
     }
-    print(json.dumps(line))
+    return {
+        "value": round(value, 4),
+        "ms_per_step": round(ms_step, 5),
+        "dtype": {"int": "int8", "mx": "fp8", "dual": "int8+fp4"}[cfg.family],
+        "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
+                   "formats": fmt.label,
+                   "gemm_path": "dual mfma" if dual else ["decode", "mfma", "dense (two passes)"][paths[-1] - 1],
+                   "parallelism": "none (one GPU)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
 
 
 def vendor_context(torch, Ls, M, rotate_mb, n):
@@ -433,8 +521,11 @@ def vendor_context(torch, Ls, M, rotate_mb, n):
 
 
 def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
-    """The oracle as it stands, on this host: activation quantization plus the
-    fp64 decomposed product of every layer, repeated for about `seconds`."""
+    """The oracle as it stands, on this host, over a bounded sample of the
+    workload: its decomposition and quantization (pack) of the first rows of
+    every layer, timed once, then its activation quantization and fp64
+    decomposed product of those rows for at most 64 tokens, repeated for about
+    `seconds`."""
     from oracle import sdq as S
     try:
         from threadpoolctl import threadpool_info
@@ -442,9 +533,12 @@ def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
     cfg_o = S.config_from(fmt, sfmt_i=sfmt_i)
-    # bound the sample: at most 64 tokens per layer
     ms = min(M, 64)
-    packs = [S.pack_logical(W, cfg_o) for W in Ws]  # offline stage, not timed
+    rows = 1024
+    t0 = time.perf_counter()
+    packs = [S.pack_logical(W[:rows], cfg_o) for W in Ws]
+    t_pack = time.perf_counter() - t0
+    n_w = sum(min(rows, W.shape[0]) * W.shape[1] for W in Ws)
     reps, t, flops = 0, 0.0, 0.0
     while t < seconds or reps == 0:
         t0 = time.perf_counter()
@@ -457,10 +551,14 @@ def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
             flops += 2.0 * ms * Lg["N"] * Lg["K"]
         t += time.perf_counter() - t0
         reps += 1
+    model, blas = host_description()
     return {"value": round(flops / t / 1e12, 8), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{reps} repetitions of numpy quantize_act + fp64 gemm over {len(Ws)} layer(s) "
-                      f"at {ms} token(s), {t:.1f} s"}
+            "sample": f"{reps} repetitions of numpy quantize_act + fp64 gemm over the first {rows} rows of "
+                      f"{len(Ws)} layer(s) at {ms} token(s), {t:.1f} s",
+            "oracle_pack_s": round(t_pack, 2),
+            "oracle_pack_weights_per_s": round(n_w / t_pack, 1),
+            "cpu_model": model, "blas": blas}
 
 
 if __name__ == "__main__":
