@@ -51,7 +51,8 @@ typedef enum {
   SDQ_ERR_BUFFER_TOO_SMALL = -4, /* output buffer smaller than required        */
   SDQ_ERR_HIP = -5,              /* a HIP call or kernel launch failed         */
   SDQ_ERR_UNSUPPORTED = -6,      /* well-formed but not implemented            */
-  SDQ_ERR_VALUE = -7             /* input value out of range (e.g. non-finite) */
+  SDQ_ERR_VALUE = -7,            /* input value out of range (e.g. non-finite) */
+  SDQ_ERR_TOO_LARGE = -8         /* needs more than sdq_gemm_static's scratch  */
 } sdq_status;
 
 /* Format families.
@@ -298,6 +299,30 @@ sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, 
 sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, void* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);
+
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture that may not call hipMalloc, tight serving loops, harnesses that
+ * forbid allocation.  sdq_gemm_ws without a workspace argument: where the path
+ * takes a workspace (SDQ_PATH_DENSE) it uses a static device array of
+ * SDQ_STATIC_SCRATCH_BYTES (48 MiB) compiled into the library, which every GPU
+ * the library runs on holds until the process ends.  Arguments, paths and
+ * results are sdq_gemm_ws's (the same kernels, bit for bit); SDQ_PATH_AUTO
+ * chooses as sdq_gemm_ws does.
+ *   - Returns SDQ_ERR_TOO_LARGE, before any GPU work, when the chosen path
+ *     needs more scratch than the array holds (32 * ceil(N/32) * K bytes for
+ *     SDQ_PATH_DENSE, e.g. 43 MiB for an 11008 x 4096 layer fits and a 16384 x
+ *     4096 one does not; SDQ_PATH_MFMA and SDQ_PATH_DECODE need none).
+ *   - Every call on a GPU shares that GPU's array, which keeps the last call's
+ *     contents.  Its contents on entry are ignored: the first pass writes every
+ *     byte the second reads.  Calls that overlap on one GPU (other streams,
+ *     other host threads) race on the array; order them on one stream.
+ *   - Allocates nothing (no hipMalloc, hipFree or allocating library call):
+ *     the array's device address is looked up with hipGetSymbolAddress on the
+ *     first call with each device current, and kept. */
+#define SDQ_STATIC_SCRATCH_BYTES (48u * 1024u * 1024u)
+sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                           const void* packed, int64_t N, int64_t K, void* Y, void* stream,
+                           int32_t path);
 
 /* Dual family (SDQ_FAMILY_DUAL; Section 5.1's int8 A_o / fp4 A_i): the two
  * activation tensors of every token, from one read of X.

@@ -28,7 +28,8 @@ from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_DUAL, FAMILY_INT, FAMILY_MX, FM
 
 __all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
            "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
-           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual"]
+           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual",
+           "gemm_static"]
 
 _FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
 
@@ -336,6 +337,25 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
                                       _dev(packed, "packed"), N, K, _dev(Y, "Y"),
                                       _dev(ws, "workspace"), ws.numel() * ws.element_size(),
                                       _stream(stream), path), "sdq_gemm_ws")
+    return Y
+
+
+def gemm_static(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PATH_AUTO,
+                stream=None):
+    """gemm() without a workspace: sdq_gemm_static, whose two-pass path uses the
+    library's static 48 MiB scratch array (nothing is allocated by the call)."""
+    import torch
+    if Xq.dim() != 2:
+        raise ValueError("Xq must be [M, K]")
+    M = Xq.shape[0]
+    _need(Xq, (M, K), torch.uint8, "Xq")
+    _need(s_a, (M,), torch.float32, "s_a")
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
+    Y = _out(out, M, N, cfg, Xq.device)
+    _same_device(Xq, s_a, packed, Y)
+    _lib.check(_lib.lib().sdq_gemm_static(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
+                                          _dev(packed, "packed"), N, K, _dev(Y, "Y"),
+                                          _stream(stream), path), "sdq_gemm_static")
     return Y
 
 

@@ -11,7 +11,7 @@ SDQ_OK = 0
 STATUS = {
     0: "SDQ_OK", -1: "SDQ_ERR_NULL", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_CONFIG",
     -4: "SDQ_ERR_BUFFER_TOO_SMALL", -5: "SDQ_ERR_HIP", -6: "SDQ_ERR_UNSUPPORTED",
-    -7: "SDQ_ERR_VALUE",
+    -7: "SDQ_ERR_VALUE", -8: "SDQ_ERR_TOO_LARGE",
 }
 FAMILY_INT, FAMILY_MX, FAMILY_DUAL = 0, 1, 2
 FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
@@ -27,8 +27,9 @@ EXPORTS = (
     "sdq_status_string", "sdq_check", "sdq_pack_size", "sdq_logical_bytes", "sdq_pack",
     "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
     "sdq_gemm_path", "sdq_linear", "sdq_gemm_workspace_size", "sdq_gemm_ws",
-    "sdq_quantize_act_dual", "sdq_gemm_dual",
+    "sdq_quantize_act_dual", "sdq_gemm_dual", "sdq_gemm_static",
 )
+STATIC_SCRATCH_BYTES = 48 * 1024 * 1024
 
 
 class sdq_config(C.Structure):
@@ -77,6 +78,7 @@ def lib() -> C.CDLL:
             "sdq_linear": (C.c_int, [cfgp, vp, C.c_int32, i64, vp, vp, vp, i64, i64, vp, vp]),
             "sdq_quantize_act_dual": (C.c_int, [cfgp, vp, C.c_int32, i64, i64, vp, vp, vp, vp, vp]),
             "sdq_gemm_dual": (C.c_int, [cfgp, vp, vp, vp, vp, i64, vp, i64, i64, vp, vp]),
+            "sdq_gemm_static": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)

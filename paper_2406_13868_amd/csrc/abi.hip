@@ -49,6 +49,8 @@ extern "C" const char* sdq_status_string(sdq_status s) {
     case SDQ_ERR_HIP: return "SDQ_ERR_HIP: a HIP call or kernel launch failed";
     case SDQ_ERR_UNSUPPORTED: return "SDQ_ERR_UNSUPPORTED: configuration or path not implemented";
     case SDQ_ERR_VALUE: return "SDQ_ERR_VALUE: input value out of range";
+    case SDQ_ERR_TOO_LARGE:
+      return "SDQ_ERR_TOO_LARGE: the path needs more scratch than sdq_gemm_static's static array holds";
   }
   return "unknown sdq_status";
 }
@@ -161,6 +163,32 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   if (log_enabled())
     std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> mx_dense (two passes)\n", (long long)M,
                  (long long)N, (long long)K);
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, const float* s_a,
+                                      int64_t M, const void* packed, int64_t N, int64_t K, void* Y,
+                                      void* stream, int32_t path) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
+  if (path != SDQ_PATH_DENSE) return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
+  if (!(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
+  if (mx_dense_workspace_bytes(N, K) > kStaticScratchBytes) return SDQ_ERR_TOO_LARGE;
+  if (M == 0) return SDQ_OK;
+  if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
+      reinterpret_cast<uintptr_t>(Y) % 4)
+    return SDQ_ERR_SHAPE;
+  const hipError_t e = launch_mx_dense_static(c, static_cast<const uint8_t*>(Xq), s_a, M,
+                                              static_cast<const uint8_t*>(packed), N, K, Y,
+                                              static_cast<hipStream_t>(stream));
+  if (log_enabled())
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> mx_dense (two passes, static scratch)\n",
+                 (long long)M, (long long)N, (long long)K);
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 

@@ -31,6 +31,8 @@
 // one per CU and requests its data four chunks ahead instead.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include <type_traits>
 
 #include "kernels.h"
@@ -426,6 +428,54 @@ hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   if (c.n_i == 1) return launch_ni<1>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
   if (c.n_i == 2) return launch_ni<2>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
   return launch_ni<3>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+}
+
+}  // namespace sdq
+
+// ------------------------------------------------------------ static scratch
+// The workspace of sdq_gemm_static, for callers that cannot allocate: one
+// array per GPU, which that GPU holds until the process ends.  In host code
+// the array's name stands for a host-side shadow, not a device address, so it
+// is never passed to a kernel or a copy: the device address is looked up once
+// per device with hipGetSymbolAddress and only that address is used.
+static __device__ __align__(256) uint8_t scratch[sdq::kStaticScratchBytes];
+
+namespace sdq {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's address on the current device (looked up on the first
+// call with that device current).
+hipError_t static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_mx_dense_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                                  const uint8_t* blob, int64_t N, int64_t K, void* Y,
+                                  hipStream_t st) {
+  if (mx_dense_workspace_bytes(N, K) > kStaticScratchBytes) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = static_scratch(&ws);
+  if (e != hipSuccess) return e;
+  return launch_mx_dense(c, Xq, s_a, M, blob, N, K, Y, ws, st);
 }
 
 }  // namespace sdq

@@ -285,6 +285,15 @@ def test_gemm_workspace_size_and_validation():
     assert L.sdq_gemm_ws(C.byref(c), p, p, 300, p, 100, 384, p, p, need, None, 9) == -3
     assert L.sdq_gemm_ws(C.byref(c), p, p, 0, p, 100, 384, p, None, 0, None, 3) == 0   # M = 0
     assert L.sdq_gemm_ws(C.byref(it.c()), p, p, 300, p, 100, 384, p, p, need, None, 3) == -6
+    # the entry point without a workspace refuses, on the host, what the static
+    # scratch cannot hold, and otherwise validates like sdq_gemm_ws
+    big_n = 16384
+    assert L.sdq_gemm_static(C.byref(c), p, p, 600, p, big_n, 4096, p, None, 3) == -8
+    assert L.sdq_gemm_static(C.byref(c), p, p, 300, p, 100, 384, p, None, 9) == -3
+    assert L.sdq_gemm_static(C.byref(c), None, p, 300, p, 100, 384, p, None, 3) == -1
+    assert L.sdq_gemm_static(C.byref(c), p, p, 0, p, 100, 384, p, None, 3) == 0   # M = 0
+    assert L.sdq_gemm_static(C.byref(it.c()), p, p, 300, p, 100, 384, p, None, 3) == -6
+    assert b"SDQ_ERR_TOO_LARGE" in L.sdq_status_string(-8)
     assert L.sdq_gemm_ex(C.byref(c), p, p, 300, p, 100, 384, p, None, 3) == -6  # needs a workspace
 
 
