@@ -79,9 +79,14 @@ def parse():
     p.add_argument("--M", type=int, default=0,
                    help="token count: block sweep (default 1) or the dual block workload (default 4096)")
     p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
-    p.add_argument("--inlier-scale", default="", choices=["", "e4m3"],
-                   help="INT family: two-level e4m3 inlier scales instead of the workload's fp16 "
-                        "(the quantized scale format of the paper's Section 6.4 study)")
+    p.add_argument("--inlier-scale", default="", choices=["", "e4m3", "ue6m2"],
+                   help="INT family: two-level e4m3 or ufp8-e6m2 inlier scales instead of the workload's "
+                        "fp16 (the quantized scale formats of the paper's Section 6.4 study)")
+    p.add_argument("--qv", type=int, default=0, choices=[0, 16, 32, 64],
+                   help="INT family: dense K per inlier scale (Q-Vector length; 0 = the family's 16)")
+    p.add_argument("--scale-table", action="store_true",
+                   help="INT workloads: GEMM time and bandwidth for every inlier scale format (fp16, e4m3, "
+                        "e6m2) and Q-Vector (16, 32, 64), against the bits per weight; one JSON object")
     p.add_argument("--y-dtype", default="f32", choices=["f32", "bf16"],
                    help="GEMM output type (bf16: the fp32 result rounded to nearest even)")
     p.add_argument("--rotate-mb", type=float, default=512.0)
@@ -173,7 +178,20 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
         return
 
-    res = measure(a, torch, sdq, a.workload, a.M, full=True)
+    if a.scale_table:
+        rows = []
+        for sf in ("", "e4m3", "ue6m2"):
+            for qv in (16, 32, 64):
+                r = measure(a, torch, sdq, a.workload, a.M, full=False, scale=(sf, qv))
+                ro = r["roofline"]
+                rows.append({"scales": sf or "f16", "qv": qv, "bits_per_weight": r["extra"]["bits_per_weight"],
+                             "gemm_us": ro["kernel_us"], "bound": ro["bound"], "achieved": ro["achieved"],
+                             "unit": ro["unit"], "frac": ro["frac"],
+                             "gemm_dense_equiv_tflops": r["extra"]["gemm_dense_equiv_tflops"]})
+        print(json.dumps({"scale_table": rows, "workload": r["config"]["workload"],
+                          "kernel_source_hash": kernel_source_hash()}))
+        return
+    res = measure(a, torch, sdq, a.workload, a.M, full=True, scale=(a.inlier_scale, a.qv))
     if res is None:  # counter-collection mode
         return
     line = {
@@ -203,7 +221,7 @@ def main():
     print(json.dumps(line))
 
 
-def measure(a, torch, sdq, workload, M_arg, full):
+def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
     """Time one workload: the step (activation quantization + GEMM of every
     layer) and the GEMM alone, both as HIP graphs over rotated copies, after a
     512 MB fill that leaves no weights in the Infinity Cache.  full: also the
@@ -225,12 +243,13 @@ def measure(a, torch, sdq, workload, M_arg, full):
             wl_name += f" M={M}"
     W_def = synth.WORKLOADS[wid]
     cfg = sdq.Config.of(fmt)
-    if a.inlier_scale and full:
+    sfmt, qv = scale
+    if sfmt or qv:
         import dataclasses
         if cfg.family != "int":
-            raise SystemExit("--inlier-scale applies to the INT family only")
-        cfg = dataclasses.replace(cfg, sfmt_i=a.inlier_scale)
-        wl_name += f", {a.inlier_scale} inlier scales (two-level)"
+            raise SystemExit("--inlier-scale and --qv apply to the INT family only")
+        cfg = dataclasses.replace(cfg, sfmt_i=sfmt, qv_i=qv)
+        wl_name += f", {sfmt or 'fp16'}{' (two-level)' if sfmt == 'e4m3' else ''} inlier scales per {cfg.qv} K"
     if a.y_dtype != "f32" and full:
         import dataclasses
         cfg = dataclasses.replace(cfg, y_dtype=a.y_dtype)
@@ -383,8 +402,8 @@ def measure(a, torch, sdq, workload, M_arg, full):
     paths = [] if dual else sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
     hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family != "int" and M < 256)
     tkey = workload if workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
-    if a.inlier_scale and full:
-        tkey += f"_{a.inlier_scale}_scales"
+    if sfmt or qv:
+        tkey += f"_{sfmt or 'f16'}_qv{cfg.qv}_scales"
     gemm_s = gemm_us * 1e-6
     if hbm_bound:
         achieved = alg_bytes / gemm_s / 1e9
@@ -429,7 +448,7 @@ def measure(a, torch, sdq, workload, M_arg, full):
     vendor = None if (a.no_vendor or not full) else vendor_context(torch, Ls, M, a.rotate_mb, max(a.steps, 20))
     cpu = None
     if full and not a.no_cpu_baseline:
-        cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds, a.inlier_scale)
+        cpu = cpu_baseline(Ws, Xs, fmt, M, a.cpu_seconds, sfmt, qv)
 
     value = flops / (ms_step * 1e-3) / 1e12
     extra = {
@@ -439,6 +458,7 @@ def measure(a, torch, sdq, workload, M_arg, full):
         "gemm_dense_equiv_tflops": round(flops / gemm_s / 1e12, 3),
         "vendor_dense_context": vendor,
         "logical_bytes": int(logical),
+        "bits_per_weight": round(8.0 * logical / sum(L.N * L.K for L in Ls), 4),
         "physical_bytes": int(phys),
         "algorithmic_bytes_per_launch": int(alg_bytes),
         "rotated_copies": R,
@@ -520,7 +540,7 @@ def vendor_context(torch, Ls, M, rotate_mb, n):
     return out
 
 
-def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
+def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i="", qv=0):
     """The oracle as it stands, on this host, over a bounded sample of the
     workload: its decomposition and quantization (pack) of the first rows of
     every layer, timed once, then its activation quantization and fp64
@@ -532,7 +552,7 @@ def cpu_baseline(Ws, Xs, fmt, M, seconds, sfmt_i=""):
         threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
-    cfg_o = S.config_from(fmt, sfmt_i=sfmt_i)
+    cfg_o = S.config_from(fmt, sfmt_i=sfmt_i, qv=qv)
     ms = min(M, 64)
     rows = 1024
     t0 = time.perf_counter()

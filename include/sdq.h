@@ -84,7 +84,7 @@ enum {
 };
 enum { SDQ_ORDER_LARGE = 0, SDQ_ORDER_SMALL = 1 };
 /* Inlier scale format (sdq_config.sfmt_i). */
-enum { SDQ_SCALE_DEFAULT = 0, SDQ_SCALE_E4M3 = 1 };
+enum { SDQ_SCALE_DEFAULT = 0, SDQ_SCALE_E4M3 = 1, SDQ_SCALE_UE6M2 = 2 };
 enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
 /* sdq_gemm_ex / sdq_gemm_ws kernel choice. */
 enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3 };
@@ -111,17 +111,26 @@ enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE
  * choice needs n_o = 1.
  *   sfmt_i  inlier scale format (Section 3.3: scales are quantized too;
  *           Section 6.4 compares 8-bit scale formats): SDQ_SCALE_DEFAULT (INT
- *           fp16 per 16 K, MX e8m0 per 32 K) or, INT family only,
- *           SDQ_SCALE_E4M3: VS-Quant's two levels, an fp8-e4m3 scale per 16
- *           K times one power-of-two scale 2^E per row, E the smallest with
- *           every vector scale amax/7 of the row <= 448 * 2^E.
+ *           fp16, MX e8m0) or, INT family only,
+ *           SDQ_SCALE_E4M3: VS-Quant's two levels, an fp8-e4m3 scale per
+ *           Q-Vector times one power-of-two scale 2^E per row, E the smallest
+ *           with every vector scale amax/7 of the row <= 448 * 2^E, or
+ *           SDQ_SCALE_UE6M2: one unsigned fp8 scale per Q-Vector (6 exponent
+ *           bits with bias 31, 2 mantissa bits), nearest even; the packer
+ *           requires every nonzero one to lie in [2^-22, 7168] (exponent
+ *           field 9..43), where an int4 code times the scale is exact in
+ *           fp16, and returns SDQ_ERR_VALUE otherwise.
  *   y_dtype element type of the GEMM output Y: SDQ_DTYPE_F32 (0, the
  *           default) or SDQ_DTYPE_BF16 (half the output bytes).  A bf16
  *           output is the fp32 output rounded to nearest even, bit for bit,
  *           with one exception: on SDQ_PATH_DENSE, outputs whose wave met a
  *           block that did not merge its inliers are rounded twice (the main
  *           sum to bf16, then that value plus those inliers), an extra error
- *           below 2^-9 of the main sum.  The packer ignores it. */
+ *           below 2^-9 of the main sum.  The packer ignores it.
+ *   qv_i    Q-Vector length of the inlier scales (Section 3.3): dense K
+ *           positions of one row that share a scale.  0 = the family's
+ *           (INT 16, MX and dual 32); the INT family also takes 32 or 64,
+ *           which halve or quarter the scale bytes. */
 typedef struct {
   int32_t family;
   int32_t n_o, m_o, fmt_o;
@@ -131,6 +140,7 @@ typedef struct {
   int32_t decomp, order;
   int32_t sfmt_i;
   int32_t y_dtype;
+  int32_t qv_i;
 } sdq_config;
 
 /* Static description of an error code (never NULL). */
@@ -175,10 +185,11 @@ sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_t K, size_t
  * With decomp SAME and order LARGE the two procedures select the same sets.
  * Quantization (IEEE fp32 arithmetic, round-to-nearest-even):
  *   INT outliers: s_o[n] = amax_row / qmax (qmax 127 or 448), q = enc(W / s_o)
- *   INT inliers:  s = fp16(amax_block16 / 7), q = clamp(rne(W / s), -7, 7);
- *                 with SDQ_SCALE_E4M3, v = amax_block16 / 7 (fp32), the row's
- *                 E as in sdq_config, code = e4m3(v * 2^-E), s = value(code)
- *                 * 2^E (exact), q as above
+ *   INT inliers:  per Q-Vector of qv_i dense K, s = fp16(amax / 7),
+ *                 q = clamp(rne(W / s), -7, 7); with SDQ_SCALE_E4M3,
+ *                 v = amax / 7 (fp32), the row's E as in sdq_config,
+ *                 code = e4m3(v * 2^-E), s = value(code) * 2^E (exact); with
+ *                 SDQ_SCALE_UE6M2, code = ue6m2(amax / 7), s = value(code)
  *   MX:           E = floor(log2 amax_block32) - emax (8 for e4m3, 2 for
  *                 e2m1), q = enc(W / 2^E) saturating
  *   an all-zero block gets a zero scale (E = -127) and zero codes.
@@ -195,8 +206,9 @@ sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N, int64_t K,
  *   scale_o        INT: float [N];  MX: uint8 e8m0 [N][K/32]
  *   pos_i, code_i  uint8 [N][K/m_i][n_i]  (int4 codes as int8 bits, e2m1
  *                  codes as the low nibble)
- *   scale_i        INT: uint16 fp16 bits [N][K/16] (SDQ_SCALE_E4M3: uint8
- *                  e4m3 codes [N][K/16]);  MX: uint8 e8m0 [N][K/32]
+ *   scale_i        INT: uint16 fp16 bits [N][K/qv] (SDQ_SCALE_E4M3 and
+ *                  SDQ_SCALE_UE6M2: uint8 codes [N][K/qv]);  MX: uint8 e8m0
+ *                  [N][K/32]
  *   scale_i_row    SDQ_SCALE_E4M3 only: float [N], the row scale 2^E (0 for
  *                  a row without inlier magnitude); may be NULL
  * Any pointer for a branch with n = 0 may be NULL. */

@@ -130,11 +130,12 @@ class Config:
 
 
 def config_from(fmt, metric: str = "magnitude", decomp: str = "same", order: str = "large",
-                sfmt_i: str = "") -> Config:
+                sfmt_i: str = "", qv: int = 0) -> Config:
     """Build an oracle Config from a plain format description (duck-typed)."""
     fmt_a = "int8+e2m1" if fmt.family == "dual" else fmt.fmt_a
     return Config(fmt.family, fmt.n_o, fmt.m_o, fmt.fmt_o, fmt.n_i, fmt.m_i,
-                  fmt.fmt_i, fmt_a, metric, decomp, order, sfmt_i or getattr(fmt, "sfmt_i", ""))
+                  fmt.fmt_i, fmt_a, metric, decomp, order, sfmt_i or getattr(fmt, "sfmt_i", ""),
+                  qv or getattr(fmt, "qv_i", 0))
 
 
 # ---------------------------------------------------------------------------

@@ -47,8 +47,9 @@ class Config:
     metric: str = "magnitude"  # significance: "magnitude" | "product"
     decomp: str = "same"       # outlier metric: "same" | "magnitude" | "product" | "error" | "output_error"
     order: str = "large"       # outliers by the largest ("large") or smallest ("small") decomp metric
-    sfmt_i: str = ""           # inlier scales: "" (int fp16 / mx e8m0) | "e4m3" (int, two-level)
+    sfmt_i: str = ""           # inlier scales: "" (int fp16 / mx e8m0) | "e4m3" (int, two-level) | "ue6m2" (int)
     y_dtype: str = "f32"       # GEMM output: "f32" | "bf16" (the fp32 result rounded to nearest even)
+    qv_i: int = 0              # dense K per inlier scale: 0 = the family's (int 16, mx/dual 32); int 16/32/64
 
     @staticmethod
     def int_family(n_o=1, m_o=8, fmt_o="e4m3", n_i=3, metric="magnitude") -> "Config":
@@ -75,6 +76,16 @@ class Config:
         return self.family == "mx"
 
     @property
+    def qv(self) -> int:
+        """Dense K positions per inlier scale."""
+        return self.qv_i or (16 if self.family == "int" else 32)
+
+    @property
+    def byte_scales(self) -> bool:
+        """INT-family inlier scales of one byte (e4m3, e6m2) rather than fp16."""
+        return self.sfmt_i in ("e4m3", "ue6m2")
+
+    @property
     def e8m0_inliers(self) -> bool:
         """Inlier scales are e8m0 per 32 K (mx and dual families)."""
         return self.family in ("mx", "dual")
@@ -87,7 +98,7 @@ class Config:
                                METRIC_PRODUCT if self.metric == "product" else METRIC_MAGNITUDE,
                                _lib.DECOMP[self.decomp], _lib.ORDER[self.order],
                                _lib.SCALE[self.sfmt_i],
-                               {"f32": DTYPE_F32, "bf16": DTYPE_BF16}[self.y_dtype])
+                               {"f32": DTYPE_F32, "bf16": DTYPE_BF16}[self.y_dtype], self.qv_i)
 
     def y_torch_dtype(self):
         import torch
@@ -145,7 +156,7 @@ def pack_logical(W: np.ndarray, cfg: Config, act_norm: Optional[np.ndarray] = No
         scale_i = np.zeros((N, K // 32), np.uint8)
     else:
         scale_o = np.zeros(N, np.float32)
-        scale_i = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
+        scale_i = np.zeros((N, K // cfg.qv), np.uint8 if cfg.byte_scales else np.uint16)
     scale_i_row = np.zeros(N, np.float32)
     _lib.check(_lib.lib().sdq_pack_logical(
         C.byref(cfg.c()), _p(W), N, K, _p(an), _p(pos_o), _p(code_o), _p(scale_o), _p(pos_i),
@@ -164,7 +175,7 @@ def unpack_dense(blob: np.ndarray, cfg: Config, N: int, K: int) -> Dict[str, np.
         so, si = np.zeros(N, np.float32), np.zeros((N, K // 32), np.uint8)
     else:
         so = np.zeros(N, np.float32)
-        si = np.zeros((N, K // 16), np.uint8 if cfg.sfmt_i == "e4m3" else np.uint16)
+        si = np.zeros((N, K // cfg.qv), np.uint8 if cfg.byte_scales else np.uint16)
     sr = np.zeros(N, np.float32)
     _lib.check(_lib.lib().sdq_unpack_dense(C.byref(cfg.c()), _p(blob), blob.nbytes, N, K, _p(co),
                                            _p(ci), _p(so), _p(si), _p(sr)), "sdq_unpack_dense")

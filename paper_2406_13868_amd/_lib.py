@@ -18,7 +18,7 @@ FMT_INT8, FMT_INT4, FMT_E4M3, FMT_E2M1 = 1, 2, 3, 4
 METRIC_MAGNITUDE, METRIC_PRODUCT = 0, 1
 DECOMP = {"same": 0, "magnitude": 1, "product": 2, "error": 3, "output_error": 4}
 ORDER = {"large": 0, "small": 1}
-SCALE = {"": 0, "e4m3": 1}
+SCALE = {"": 0, "e4m3": 1, "ue6m2": 2}
 DTYPE_F32, DTYPE_BF16 = 0, 1
 PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE = 0, 1, 2, 3
 
@@ -37,7 +37,7 @@ class sdq_config(C.Structure):
                 ("fmt_o", C.c_int32), ("n_i", C.c_int32), ("m_i", C.c_int32),
                 ("fmt_i", C.c_int32), ("fmt_a", C.c_int32), ("metric", C.c_int32),
                 ("decomp", C.c_int32), ("order", C.c_int32), ("sfmt_i", C.c_int32),
-                ("y_dtype", C.c_int32)]
+                ("y_dtype", C.c_int32), ("qv_i", C.c_int32)]
 
 
 class SDQError(RuntimeError):

@@ -33,6 +33,8 @@
 //     depend on timing.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 #include "tile_out.h"
 
@@ -64,7 +66,21 @@ struct DecodeArgs {
   int M, N, K, n_chunks;
   int64_t scales_off, rows_off, irow_off;
   bool y_bf16 = false;  // Y as bf16
+  int qs = 0;           // log2(qv / 16): 16-K blocks per inlier scale = 1 << qs
+  int srow = 16;        // bytes of one row's inlier scales in a chunk: (128 / qv) * (2 or 1)
 };
+
+// Inlier scale formats of the INT family (template parameter SF).
+enum ScaleFmt { kScaleF16 = 0, kScaleE4M3 = 1, kScaleE6M2 = 2 };
+
+// Value of a ufp8-e6m2 code: (4 + m) * 2^(e - 33), or m * 2^-32 for e = 0
+// (exact in fp32: a 3-bit integer times a power of two).
+__device__ __forceinline__ float e6m2_to_f32(uint32_t code) {
+  const uint32_t e = (code >> 2) & 63u, m = code & 3u;
+  const float mant = float(e ? 4u + m : m);
+  const uint32_t ee = e ? e : 1u;
+  return mant * __uint_as_float((ee + 94u) << 23);  // 2^(ee - 33)
+}
 
 // LDS bytes of one wave's activation region: MT tokens x (8S chunks + the zero chunk).
 __host__ __device__ constexpr int wave_lds_bytes(int MT, int S) {
@@ -131,14 +147,17 @@ __device__ __forceinline__ uint2 quant8(const float* v, float inv) {
 
 struct StepBuf {
   uint4 w0, w1;  // group words of (row, j) for h = 0 and h = 1
-  uint2 sc;      // the four scales of blocks 4j..4j+3: fp16 pairs, or e4m3 bytes of .x
+  uint2 sc;      // the lane's inlier scales (K [64j, 64j + 64) of the chunk): 1, 2 or 4
+                 // fp16 values, or 1, 2 or 4 bytes (e4m3, e6m2), from the low end
 };
 
 // FUSE: 0 = activations from Xq/s_a, 1 = quantize fp32 X, 2 = quantize bf16 X.
-// SC8: two-level inlier scales (e4m3 per block, a power of two per row).
-template <int MT, bool OUT_INT8, int FUSE, int S, int KS, int SPW, bool SC8>
+// SF: inlier scale format (ScaleFmt); kScaleE4M3 is VS-Quant's two levels (an
+// e4m3 code per Q-Vector, a power of two per row).
+template <int MT, bool OUT_INT8, int FUSE, int S, int KS, int SPW, int SF>
 __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a) {
-  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
+  constexpr bool SC8 = SF == kScaleE4M3;
+  const int kSB = kTileN * a.srow;               // inlier scale bytes per (tile, chunk)
   constexpr int kWG = SPW * KS;                  // waves per workgroup
   extern __shared__ __align__(16) uint8_t xs[];  // [wave][MT][8S + 1][kXStride]
   __shared__ float red[kWG][kDecodeMaxM];
@@ -190,7 +209,9 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
   const uint8_t* tbase = a.blob + size_t(t) * KC * kWordBytesPerTC;
   const uint8_t* sbase = a.blob + a.scales_off + size_t(t) * KC * kSB;
   const uint32_t woff = uint32_t(row * 2 + j) * 16;
-  const uint32_t soff = SC8 ? uint32_t(row * 8 + j * 4) : uint32_t(row * 16 + j * 8);
+  // the lane covers K [64j, 64j + 64) of a chunk: half of its row's scales
+  const int lbytes = a.srow >> 1;  // 8, 4, 2 or 1 (wave-uniform)
+  const uint32_t soff = uint32_t(row * a.srow + j * lbytes);
   StepBuf buf[S];
 #pragma unroll
   for (int d = 0; d < S; ++d) {
@@ -198,10 +219,11 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
     const uint8_t* wp = tbase + (uint32_t(c) * kWordBytesPerTC + woff);
     buf[d].w0 = *reinterpret_cast<const uint4*>(wp);
     buf[d].w1 = *reinterpret_cast<const uint4*>(wp + 1024);  // h = 1: 32 rows x 32 bytes further
-    if constexpr (SC8)
-      buf[d].sc = make_uint2(*reinterpret_cast<const uint32_t*>(sbase + (uint32_t(c) * kSB + soff)), 0u);
-    else
-      buf[d].sc = *reinterpret_cast<const uint2*>(sbase + (uint32_t(c) * kSB + soff));
+    const uint8_t* sp = sbase + (uint32_t(c) * kSB + soff);
+    if (lbytes == 8) buf[d].sc = *reinterpret_cast<const uint2*>(sp);
+    else if (lbytes == 4) buf[d].sc = make_uint2(*reinterpret_cast<const uint32_t*>(sp), 0u);
+    else if (lbytes == 2) buf[d].sc = make_uint2(*reinterpret_cast<const uint16_t*>(sp), 0u);
+    else buf[d].sc = make_uint2(*sp, 0u);
   }
   // 16 * s_o: the inlier dot products carry a factor 16, folded out at the end.
   const float so16 = 16.f * reinterpret_cast<const float*>(a.blob + a.rows_off)[t * kTileN + row];
@@ -314,17 +336,19 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
     const StepBuf& cur = buf[d];
     const uint32_t wa[4] = {cur.w0.x, cur.w0.y, cur.w0.z, cur.w0.w};
     const uint32_t wb[4] = {cur.w1.x, cur.w1.y, cur.w1.z, cur.w1.w};
+    // the scale of 16-K block q of the lane is its scale q >> qs
     float scl[4];
-    if constexpr (SC8) {
-      scl[0] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 0);
-      scl[1] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 1);
-      scl[2] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 2);
-      scl[3] = __builtin_amdgcn_cvt_f32_fp8(int(cur.sc.x), 3);
-    } else {
-      scl[0] = float(f16lo(cur.sc.x));
-      scl[1] = float(f16hi(cur.sc.x));
-      scl[2] = float(f16lo(cur.sc.y));
-      scl[3] = float(f16hi(cur.sc.y));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = q >> a.qs;
+      if constexpr (SF == kScaleF16) {
+        const uint32_t wd = e < 2 ? cur.sc.x : cur.sc.y;
+        scl[q] = float((e & 1) ? f16hi(wd) : f16lo(wd));
+      } else {
+        const uint32_t byte = (cur.sc.x >> (8 * e)) & 0xFFu;
+        if constexpr (SF == kScaleE4M3) scl[q] = __builtin_amdgcn_cvt_f32_fp8(int(byte), 0);
+        else scl[q] = e6m2_to_f32(byte);
+      }
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -410,17 +434,17 @@ hipError_t launch_s(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(unsigned(L.n_tiles * (kTileN / kSliceRows) / SPW));
   const dim3 block(SPW * KS * 64);
   const size_t lds = size_t(SPW) * KS * wave_lds_bytes(MT, S);
-  if (c.sc8) {
+  const int sf = c.sc8 ? kScaleE4M3 : c.e6m2 ? kScaleE6M2 : kScaleF16;
+  auto go = [&](auto sfc) {
+    constexpr int SF = decltype(sfc)::value;
     if (c.fmt_o == SDQ_FMT_INT8)
-      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW, true>), grid, block, lds, st, a);
+      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW, SF>), grid, block, lds, st, a);
     else
-      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW, true>), grid, block, lds, st, a);
-  } else {
-    if (c.fmt_o == SDQ_FMT_INT8)
-      hipLaunchKernelGGL((int_decode_kernel<MT, true, FUSE, S, KS, SPW, false>), grid, block, lds, st, a);
-    else
-      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW, false>), grid, block, lds, st, a);
-  }
+      hipLaunchKernelGGL((int_decode_kernel<MT, false, FUSE, S, KS, SPW, SF>), grid, block, lds, st, a);
+  };
+  if (sf == kScaleE4M3) go(std::integral_constant<int, kScaleE4M3>{});
+  else if (sf == kScaleE6M2) go(std::integral_constant<int, kScaleE6M2>{});
+  else go(std::integral_constant<int, kScaleF16>{});
   return hipGetLastError();
 }
 
@@ -464,6 +488,12 @@ hipError_t launch_fuse(const Cfg& c, const DecodeArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// Q-Vector and scale width of the configuration into the kernel arguments.
+void set_scale_args(const Cfg& c, DecodeArgs& a) {
+  a.qs = c.qv == 64 ? 2 : c.qv == 32 ? 1 : 0;
+  a.srow = (kChunkK / c.qv) * c.scale_bytes();
+}
+
 bool decode_fused_fits(int64_t M, int64_t K) { return M <= kFusedMaxM && decode_fits(M, K); }
 
 bool decode_fits(int64_t M, int64_t K) {
@@ -478,6 +508,7 @@ hipError_t launch_int_decode(const Cfg& c, const uint8_t* Xq, const float* s_a, 
   DecodeArgs a{Xq, s_a, nullptr, nullptr, nullptr, blob, Y, int(M), int(N), int(K),
                int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
   a.y_bf16 = c.y_bf16;
+  set_scale_args(c, a);
   return launch_fuse<0>(c, a, st);
 }
 
@@ -488,6 +519,7 @@ hipError_t launch_int_decode_fused(const Cfg& c, const void* X, int x_dtype, int
   DecodeArgs a{nullptr, nullptr, X, s_a_out, Xq_out, blob, Y, int(M), int(N), int(K),
                int(L.n_chunks), L.scales_off, L.rows_off, L.irow_off};
   a.y_bf16 = c.y_bf16;
+  set_scale_args(c, a);
   if (x_dtype == SDQ_DTYPE_BF16) return launch_fuse<2>(c, a, st);
   return launch_fuse<1>(c, a, st);
 }

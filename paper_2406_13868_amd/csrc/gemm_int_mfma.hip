@@ -48,19 +48,43 @@ struct MfmaArgs {
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off, rows_off, irow_off;
   bool y_bf16 = false;  // Y as bf16
+  int qs = 0;           // log2(qv / 16): 16-K blocks per inlier scale = 1 << qs
+  int srow = 16;        // bytes of one row's inlier scales in a chunk: (128 / qv) * (2 or 1)
 };
 
-// The fp16 inlier scale of block kb from a row's scale registers sv: fp16
-// pairs (two per dword), or with two-level e4m3 scales one e4m3 code per byte
-// (four per dword), converted exactly (every e4m3 value is an fp16 value).
-template <bool SC8>
-__device__ __forceinline__ _Float16 block_scale(const uint32_t* sv, int kb) {
-  if constexpr (SC8) {
-    return (_Float16)__builtin_amdgcn_cvt_f32_fp8(int(sv[kb >> 2] >> (8 * (kb & 3))), 0);
+// Inlier scale formats of the INT family (template parameter SF).
+enum ScaleFmt { kScaleF16 = 0, kScaleE4M3 = 1, kScaleE6M2 = 2 };
+
+// The fp16 inlier scale of 16-K block kb (its scale kb >> qs) from a row's
+// scale registers sv: fp16 pairs (two per dword), or one code per byte (four
+// per dword): e4m3 (every value is an fp16 value) or ufp8-e6m2, whose values
+// (4 + m) * 2^(e - 33) the packer keeps within [2^-22, 7168], where they and
+// their products with an int4 code are exact in fp16.
+template <int SF>
+__device__ __forceinline__ _Float16 block_scale(const uint32_t* sv, int kb, int qs) {
+  const int e = kb >> qs;
+  if constexpr (SF == kScaleF16) {
+    const uint32_t sw = sv[e >> 1];
+    return __builtin_bit_cast(_Float16, (unsigned short)((e & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
   } else {
-    const uint32_t sw = sv[kb >> 1];
-    return __builtin_bit_cast(_Float16, (unsigned short)((kb & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
+    const uint32_t byte = (sv[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+    if constexpr (SF == kScaleE4M3) {
+      return (_Float16)__builtin_amdgcn_cvt_f32_fp8(int(byte), 0);
+    } else {
+      const uint32_t ex = byte >> 2, m = byte & 3u;
+      const float v = ex ? float(4u + m) * __uint_as_float((ex + 94u) << 23) : 0.f;  // code 0: scale 0
+      return (_Float16)v;
+    }
   }
+}
+
+// A row's inlier scales of one chunk (srow = 16, 8, 4 or 2 bytes, naturally
+// aligned), into the low end of four dwords.
+__device__ __forceinline__ uint4 load_row_scales_chunk(const uint8_t* p, int srow) {
+  if (srow == 16) return *reinterpret_cast<const uint4*>(p);
+  if (srow == 8) { const uint2 v = *reinterpret_cast<const uint2*>(p); return make_uint4(v.x, v.y, 0, 0); }
+  if (srow == 4) return make_uint4(*reinterpret_cast<const uint32_t*>(p), 0, 0, 0);
+  return make_uint4(*reinterpret_cast<const uint16_t*>(p), 0, 0, 0);
 }
 
 // Four int8 -> four f16 (two dwords), exact: f16(1024 + (b ^ 0x80)) - 1152 = b.
@@ -135,9 +159,11 @@ __device__ __forceinline__ void outlier_i8(uint32_t w, uint32_t& lo, uint32_t& h
   hi = pos < 4u ? 0u : v;
 }
 
-template <int MS, int NI, bool OUT_INT8, bool SC8>
+template <int MS, int NI, bool OUT_INT8, int SF>
 __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
-  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
+  constexpr bool SC8 = SF == kScaleE4M3;       // two-level: a power of two per row
+  constexpr bool ONE = SF != kScaleF16;        // q * s exact in one fp16 fragment
+  const int kSB = kTileN * a.srow;             // inlier scale bytes per (tile, chunk)
   constexpr int BM = 32 * MS;
   __shared__ __align__(16) _Float16 xs[2][BM * kLdsRow];
 
@@ -184,18 +210,13 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   // ---- weight stream of this wave's tile
   // lane (col, h): the 32 bytes at ((h*32 + col)*2 + j)*16, j = 0, 1
   const uint8_t* wbase = a.blob + size_t(tile_ok ? tile : 0) * KC * kWordBytesPerTC + size_t(lane) * 32;
-  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kSB + col * (kSB / kTileN);
+  const uint8_t* sbase = a.blob + a.scales_off + size_t(tile_ok ? tile : 0) * KC * kSB + col * a.srow;
   uint4 wr0, wr1, sr;
   auto load_w = [&](int c) {
     if (tile_ok) {
       wr0 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC);
       wr1 = *reinterpret_cast<const uint4*>(wbase + size_t(c) * kWordBytesPerTC + 16);
-      if constexpr (SC8) {
-        const uint2 s8 = *reinterpret_cast<const uint2*>(sbase + size_t(c) * kSB);
-        sr = make_uint4(s8.x, s8.y, 0, 0);
-      } else {
-        sr = *reinterpret_cast<const uint4*>(sbase + size_t(c) * kSB);
-      }
+      sr = load_row_scales_chunk(sbase + size_t(c) * kSB, a.srow);
     } else {
       wr0 = wr1 = sr = make_uint4(0, 0, 0, 0);
     }
@@ -219,11 +240,11 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
     if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
 #pragma unroll 2
     for (int kb = 0; kb < 8; ++kb) {
-      const _Float16 s = block_scale<SC8>(sv, kb);
+      const _Float16 s = block_scale<SF>(sv, kb, a.qs);
       h8 bh, bl;
-      if constexpr (SC8) {
-        // an int4 code times an e4m3 scale has at most 7 significant bits:
-        // exact in fp16, so one fragment carries the scaled inlier
+      if constexpr (ONE) {
+        // an int4 code times an e4m3 (e6m2) scale has at most 7 (6)
+        // significant bits: exact in fp16, so one fragment carries it
         const h8 sv8 = {s, s, s, s, s, s, s, s};
         bh = inlier_f16<NI>(wv[kb]) * sv8;
       } else {
@@ -238,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
       for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bh, acc[ms], 0, 0, 0);
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
-      if constexpr (!SC8) {
+      if constexpr (!ONE) {
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
       }
@@ -276,9 +297,11 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
 // takes group i on lane half 0 and group 8 + i on lane half 1, so that each
 // lane's activations for a chunk are 64 contiguous bytes (four 16-byte loads
 // per 32-token sub-tile) and its group words two 16-byte runs.
-template <int MS, int NI, bool OUT_INT8, int NW, bool SC8>
+template <int MS, int NI, bool OUT_INT8, int NW, int SF>
 __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a) {
-  constexpr int kSB = SC8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
+  constexpr bool SC8 = SF == kScaleE4M3;       // two-level: a power of two per row
+  constexpr bool ONE = SF != kScaleF16;        // q * s exact in one fp16 fragment
+  const int kSB = kTileN * a.srow;             // inlier scale bytes per (tile, chunk)
   constexpr int BM = 32 * MS;
   __shared__ float red[NW / 2][16][64];
 
@@ -298,11 +321,11 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
       buffer_rsrc(a.blob + a.scales_off + size_t(tile) * KC * kSB, uint32_t(KC) * kSB);
   const __amdgpu_buffer_rsrc_t xr =
       buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, BM)) * uint32_t(a.K));
-  const uint32_t woff = uint32_t(col * 2 + h) * 16, soff = uint32_t(col) * (kSB / kTileN);
+  const uint32_t woff = uint32_t(col * 2 + h) * 16, soff = uint32_t(col) * uint32_t(a.srow);
   const uint32_t xoff = uint32_t(col) * uint32_t(a.K) + uint32_t(h) * 64;
 
   struct Stage {
-    uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's eight block scales (fp16, or e4m3 in .x/.y)
+    uint4 w0, w1, sc;   // words of h' = 0 and h' = 1, the row's scales of the chunk (from the low end)
     uint4 x[MS][4];     // 64 activation bytes per sub-tile
   };
   auto ld16 = [](__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t so) __attribute__((always_inline)) {
@@ -313,12 +336,17 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
   auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
     st.w0 = ld16(wr, woff, uint32_t(c) * kWordBytesPerTC);
     st.w1 = ld16(wr, woff + 1024, uint32_t(c) * kWordBytesPerTC);
-    if constexpr (SC8) {
+    // the row's scales of the chunk: a.srow bytes, naturally aligned
+    if (a.srow == 16) {
+      st.sc = ld16(sr, soff, uint32_t(c) * kSB);
+    } else if (a.srow == 8) {
       typedef unsigned int u2_ __attribute__((ext_vector_type(2)));
       const u2_ q = __builtin_bit_cast(u2_, __builtin_amdgcn_raw_buffer_load_b64(sr, soff, uint32_t(c) * kSB, 0));
       st.sc = make_uint4(q[0], q[1], 0, 0);
+    } else if (a.srow == 4) {
+      st.sc = make_uint4(__builtin_amdgcn_raw_buffer_load_b32(sr, soff, uint32_t(c) * kSB, 0), 0, 0, 0);
     } else {
-      st.sc = ld16(sr, soff, uint32_t(c) * kSB);
+      st.sc = make_uint4(__builtin_amdgcn_raw_buffer_load_b16(sr, soff, uint32_t(c) * kSB, 0), 0, 0, 0);
     }
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms)
@@ -347,16 +375,9 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
     for (int i = 0; i < 8; ++i) {
       const uint32_t w = wv[i & 1][i >> 1];
       // the scale of 16-K block kb = 4h + (i >> 1) of group 8h + i
-      _Float16 s;
-      if constexpr (SC8) {
-        s = (_Float16)__builtin_amdgcn_cvt_f32_fp8(int((h ? sv[1] : sv[0]) >> (8 * ((i >> 1) & 3))), 0);
-      } else {
-        // half (kb & 1) = ((i >> 1) & 1) of dword kb >> 1 = 2h + (i >> 2)
-        const uint32_t sw = h ? sv[2 + (i >> 2)] : sv[i >> 2];
-        s = __builtin_bit_cast(_Float16, (unsigned short)(((i >> 1) & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
-      }
+      const _Float16 s = block_scale<SF>(sv, 4 * h + (i >> 1), a.qs);
       h8 bh, bl;
-      if constexpr (SC8) {
+      if constexpr (ONE) {
         const h8 sv8 = {s, s, s, s, s, s, s, s};
         bh = inlier_f16<NI>(w) * sv8;  // exact in fp16 (at most 7 significant bits)
       } else {
@@ -395,7 +416,7 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms) acco[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bo, acco[ms], 0, 0, 0);
       }
-      if constexpr (!SC8) {
+      if constexpr (!ONE) {
 #pragma unroll
         for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
       }
@@ -464,44 +485,46 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
       store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * fmaf(so, float(acco[ms][e]), gi * acc[ms][e]));
 }
 
-template <int MS, int NI, int NW, bool SC8>
+template <int MS, int NI, int NW, int SF>
 hipError_t launch_splitk(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
   const dim3 block(NW * 64);
   if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, true, NW, SC8>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, true, NW, SF>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, false, NW, SC8>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_splitk_kernel<MS, NI, false, NW, SF>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
-template <int MS, int NI, bool SC8>
+template <int MS, int NI, int SF>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   if constexpr (MS <= 2) {
     // few tokens: split K inside the workgroup so that about 2048+ waves run
     const int64_t waves4 = int64_t(a.n_tiles) * 4 * ((a.M + 32 * MS - 1) / (32 * MS));
-    if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SC8>(c, a, st);
-    return launch_splitk<MS, NI, 8, SC8>(c, a, st);
+    if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SF>(c, a, st);
+    return launch_splitk<MS, NI, 8, SF>(c, a, st);
   }
   const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
   const dim3 block(kThreads);
   if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SC8>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SF>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false, SC8>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false, SF>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
-template <int MS, bool SC8>
+template <int MS, int SF>
 hipError_t launch_ms_sc(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.n_i == 1) return launch_ms_ni<MS, 1, SC8>(c, a, st);
-  if (c.n_i == 2) return launch_ms_ni<MS, 2, SC8>(c, a, st);
-  return launch_ms_ni<MS, 3, SC8>(c, a, st);
+  if (c.n_i == 1) return launch_ms_ni<MS, 1, SF>(c, a, st);
+  if (c.n_i == 2) return launch_ms_ni<MS, 2, SF>(c, a, st);
+  return launch_ms_ni<MS, 3, SF>(c, a, st);
 }
 
 template <int MS>
 hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  return c.sc8 ? launch_ms_sc<MS, true>(c, a, st) : launch_ms_sc<MS, false>(c, a, st);
+  if (c.sc8) return launch_ms_sc<MS, kScaleE4M3>(c, a, st);
+  if (c.e6m2) return launch_ms_sc<MS, kScaleE6M2>(c, a, st);
+  return launch_ms_sc<MS, kScaleF16>(c, a, st);
 }
 
 }  // namespace
@@ -512,6 +535,8 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   MfmaArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
              L.scales_off, L.rows_off, L.irow_off};
   a.y_bf16 = c.y_bf16;
+  a.qs = c.qv == 64 ? 2 : c.qv == 32 ? 1 : 0;
+  a.srow = (kChunkK / c.qv) * c.scale_bytes();
   if (M <= 32) return launch_ms<1>(c, a, st);
   // 33..64 tokens: one 64-token block expands every weight once; when that
   // leaves fewer workgroups than compute units, two 32-token blocks fill the

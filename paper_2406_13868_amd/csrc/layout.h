@@ -5,7 +5,10 @@
 // every (tile t, chunk c), in this order:
 //
 //   section A  group words     512 x 32-bit   [t][c] (2 KiB)
-//   section B  block scales    INT: 512 B (fp16) or 256 B (e4m3), MX: 256 B   [t][c]
+//   section B  block scales    INT: 32 rows x 128/qv scales (qv = 16, 32 or
+//                              64 dense K per scale) of 2 B (fp16) or 1 B
+//                              (e4m3, e6m2): 512 B for fp16 per 16 K;
+//                              MX: 256 B   [t][c]
 //   section C  row scales      INT only: fp32 [t][32] outlier scales, then
 //                              with e4m3 block scales fp32 [t][32] inlier
 //                              row scales (powers of two)
@@ -83,12 +86,13 @@ struct Layout {
   int scale_bytes_per_tc = 0;
 };
 
-// sc8: INT family with e4m3 block scales (and inlier row scales at irow_off)
-inline Layout make_layout(bool mx, int64_t N, int64_t K, bool sc8 = false) {
+// INT family: qv dense K per inlier scale (16, 32 or 64) of sb bytes (fp16 2,
+// e4m3 and e6m2 1); sc8: two-level e4m3 scales (inlier row scales at irow_off)
+inline Layout make_layout(bool mx, int64_t N, int64_t K, bool sc8 = false, int qv = 16, int sb = 2) {
   Layout L;
   L.n_tiles = (N + kTileN - 1) / kTileN;
   L.n_chunks = K / kChunkK;
-  L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : sc8 ? kInt8ScaleBytesPerTC : kIntScaleBytesPerTC;
+  L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : kTileN * (kChunkK / qv) * sb;
   L.words_off = 0;
   L.scales_off = L.n_tiles * L.n_chunks * kWordBytesPerTC;
   L.rows_off = L.scales_off + L.n_tiles * L.n_chunks * L.scale_bytes_per_tc;
@@ -139,6 +143,10 @@ inline int mx_word_index(int g, int r) {
 }
 inline int int_scale_byte(int kb, int r) { return (r * 8 + kb) * 2; }
 inline int int8_scale_byte(int kb, int r) { return r * 8 + kb; }
+// INT family, general Q-Vector: byte offset of scale b (0 .. 128/qv - 1 within
+// the chunk) of tile row r, scales of sb bytes.  A row's scales of one chunk
+// are contiguous: (128/qv) * sb bytes at r * (128/qv) * sb.
+inline int int_scale_off(int b, int r, int qv, int sb) { return (r * (kChunkK / qv) + b) * sb; }
 inline int mx_scale_byte(int b, int r, int branch) {
   const int s = b >> 1, h = b & 1;
   return ((h * 32 + r) * 2 + s) * 2 + branch;

@@ -118,6 +118,30 @@ uint8_t enc_e2m1(double x) {
   return uint8_t(s | ((E + 1) << 1) | mq);
 }
 
+// Nearest-even ufp8 E6M2 code of a >= 0 (6 exponent bits with bias 31, 2
+// mantissa bits, no sign; exponent field 0 holds m/4 * 2^-30), saturating at
+// the largest code, 1.75 * 2^32.
+uint8_t enc_ue6m2(double a) {
+  const double kMax = 1.75 * 4294967296.0;
+  if (a > kMax) a = kMax;
+  if (a < std::ldexp(1.0, -30)) {  // subnormal spacing 2^-32
+    const int q = int(std::nearbyint(std::ldexp(a, 32)));  // 4 becomes the first normal code
+    return uint8_t(q);
+  }
+  int e;
+  const double f = std::frexp(a, &e);  // a = f * 2^e, f in [0.5, 1)
+  int E = e - 1;
+  int mq = int(std::nearbyint((2.0 * f - 1.0) * 4.0));
+  if (mq == 4) { ++E; mq = 0; }
+  return uint8_t(((E + 31) << 2) | mq);
+}
+
+// Value of a ufp8 E6M2 code (exact in fp32).
+float ue6m2_value(uint8_t code) {
+  const int e = code >> 2, m = code & 3;
+  return e ? std::ldexp(float(4 + m), e - 33) : std::ldexp(float(m), -32);
+}
+
 int floor_log2f(float a) {
   int e;
   std::frexp(a, &e);
@@ -160,26 +184,40 @@ struct Scratch {
         V(size_t(K / 16)), SC(size_t(K / 16)) {}
 };
 
-// INT-family inlier scales of one row over the positions `mask8`: per 16-K
-// block v = amax / 7 (fp32) stored as fp16 (eff = that fp16 value) or, with
-// two-level e4m3 scales, as e4m3(v * 2^-E) with E the smallest exponent that
-// puts the row's largest v within 448 * 2^E (eff = value * 2^E, exact).
-// Writes eff to V and the stored scales to SC; returns the row scale 2^E
-// (0 for a row without inlier magnitude, always 0 for fp16 scales).
+// INT-family inlier scales of one row over the positions `mask8`: per
+// Q-Vector of c.qv dense K, v = amax / 7 (fp32), stored as fp16 (eff = that
+// fp16 value); with two-level e4m3 scales as e4m3(v * 2^-E), E the smallest
+// exponent that puts the row's largest v within 448 * 2^E (eff = value * 2^E,
+// exact); or as ufp8-e6m2(v) (eff = its value, exact).  Writes eff to V and
+// the stored scales to SC; returns the row scale 2^E (0 for a row without
+// inlier magnitude, always 0 for fp16 and e6m2 scales).  A nonzero e6m2 scale
+// must have exponent field 9..43 ([2^-22, 7168], where an int4 code times it is
+// exact in fp16): SDQ_ERR_VALUE otherwise, as for an fp16 overflow.
 sdq_status int_inlier_scales(const Cfg& c, const float* w, int64_t K, const uint8_t* mask8, float* V,
                              uint16_t* SC, float* row_scale) {
-  const int64_t B = K / 16;
+  const int qv = c.qv;
+  const int64_t B = K / qv;
   float vmax = 0.f;
   for (int64_t b = 0; b < B; ++b) {
     float a = 0.f;
-    for (int kk = 0; kk < 16; ++kk) {
-      const int64_t k = b * 16 + kk;
+    for (int kk = 0; kk < qv; ++kk) {
+      const int64_t k = b * qv + kk;
       if ((mask8[k / 8] >> (k % 8)) & 1u) a = std::fmax(a, std::fabs(w[k]));
     }
     V[b] = a / 7.0f;
     vmax = std::fmax(vmax, V[b]);
   }
   *row_scale = 0.f;
+  if (c.e6m2) {
+    for (int64_t b = 0; b < B; ++b) {
+      const uint8_t code = enc_ue6m2(double(V[b]));
+      const int e = code >> 2;
+      if (code != 0 && (e < 9 || e > 43)) return SDQ_ERR_VALUE;  // beyond the exact fp16 range
+      SC[b] = code;
+      V[b] = ue6m2_value(code);
+    }
+    return SDQ_OK;
+  }
   if (!c.sc8) {
     for (int64_t b = 0; b < B; ++b) {
       const uint16_t h = f32_to_f16_bits(V[b]);
@@ -209,7 +247,7 @@ sdq_status int_inlier_scales(const Cfg& c, const float* w, int64_t K, const uint
 sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* keep8, float* D,
                         float* V, uint16_t* SC) {
   const bool mx_in = c.mx || c.dual;  // fp4 inliers with e8m0 scales per 32 K
-  const int qv = mx_in ? 32 : 16;
+  const int qv = mx_in ? 32 : c.qv;
   if (!mx_in) {
     float row;
     const sdq_status st = int_inlier_scales(c, w, K, keep8, V, SC, &row);
@@ -232,7 +270,7 @@ sdq_status inlier_error(const Cfg& c, const float* w, int64_t K, const uint8_t* 
           deq = std::ldexp((q & 8u) ? -mag[q & 7u] : mag[q & 7u], E);
         }
       } else {
-        const float sc = V[k0 / 16];
+        const float sc = V[k0 / qv];
         if (sc != 0.f) deq = float(clamp_int(int(std::nearbyint(w[k] / sc)), -7, 7)) * sc;
       }
       D[k] = ((keep8[k / 8] >> (k % 8)) & 1u) ? std::fabs(w[k] - deq) : 0.f;
@@ -410,26 +448,28 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
             if ((om[gg] >> p) & 1u)
               ocode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(w[k0 + 8 * gg + p] / s_o)), -127, 127)));
     } else {
-      for (int hb = 0; hb < 2; ++hb) {  // two 16-K blocks
-        const int64_t kb = k0 / 16 + hb;
+      const int qv = c.qv, sbytes = c.scale_bytes();
+      for (int gg = 0; gg < 4; ++gg) {  // the four 8-groups of the span
+        const int64_t kg = k0 + 8 * gg;
+        const int64_t kb = kg / qv;      // its Q-Vector
         const float s = sc.V[kb];
+        for (int p = 0; p < 8; ++p)
+          if (((im[gg] >> p) & 1u) && s != 0.f) {
+            const float v = w[kg + p] / s;
+            icode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(v)), -7, 7)));
+          }
+        if (kg % qv != 0) continue;  // the Q-Vector's scale is written at its first group
         const uint16_t h = sc.SC[kb];
-        for (int gg = 2 * hb; gg < 2 * hb + 2; ++gg)
-          for (int p = 0; p < 8; ++p)
-            if (((im[gg] >> p) & 1u) && s != 0.f) {
-              const float v = w[k0 + 8 * gg + p] / s;
-              icode[8 * gg + p] = uint8_t(int8_t(clamp_int(int(std::nearbyint(v)), -7, 7)));
-            }
         if (out.scale_i) {
-          if (c.sc8) static_cast<uint8_t*>(out.scale_i)[n * (K / 16) + kb] = uint8_t(h);
-          else static_cast<uint16_t*>(out.scale_i)[n * (K / 16) + kb] = h;
+          if (sbytes == 1) static_cast<uint8_t*>(out.scale_i)[n * (K / qv) + kb] = uint8_t(h);
+          else static_cast<uint16_t*>(out.scale_i)[n * (K / qv) + kb] = h;
         }
         if (out.blob) {
-          const int64_t ch = k0 / kChunkK;
-          const int kbl = int((k0 % kChunkK) / 16) + hb;
+          const int64_t ch = kg / kChunkK;
+          const int kbl = int((kg % kChunkK) / qv);
           uint8_t* sb = out.blob + out.lay->scales_off + (t * out.lay->n_chunks + ch) * out.lay->scale_bytes_per_tc;
-          if (c.sc8) sb[int8_scale_byte(kbl, int(r))] = uint8_t(h);
-          else std::memcpy(sb + int_scale_byte(kbl, int(r)), &h, 2);
+          if (sbytes == 1) sb[int_scale_off(kbl, int(r), qv, 1)] = uint8_t(h);
+          else std::memcpy(sb + int_scale_off(kbl, int(r), qv, 2), &h, 2);
         }
       }
       if (c.n_o && s_o != 0.f) {
@@ -599,8 +639,8 @@ extern "C" sdq_status sdq_logical_bytes(const sdq_config* cfg, int64_t N, int64_
     bits += (K / 32) * 8;               // inlier e8m0
     if (c.n_o) bits += 32;              // outlier fp32 per row
   } else {
-    bits += (K / 16) * (c.sc8 ? 8 : 16);  // inlier fp16, or e4m3 ...
-    if (c.sc8) bits += 32;                // ... with an fp32 (power of two) per row
+    bits += (K / c.qv) * 8 * c.scale_bytes();  // inlier fp16, or e4m3 / e6m2 ...
+    if (c.sc8) bits += 32;                     // ... e4m3 with an fp32 (power of two) per row
     if (c.n_o) bits += 32;                // outlier fp32 per row
   }
   *bytes = size_t((bits * N + 7) / 8);
@@ -714,13 +754,14 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
           static_cast<uint8_t*>(scale_i)[bi] = sc[mx_scale_byte(b, r, 1)];
         }
       } else {
-        for (int kb = 0; kb < 8; ++kb) {
-          if (c.sc8) {
-            static_cast<uint8_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = sc[int8_scale_byte(kb, r)];
+        const int nb = kChunkK / c.qv;
+        for (int kb = 0; kb < nb; ++kb) {
+          if (c.scale_bytes() == 1) {
+            static_cast<uint8_t*>(scale_i)[n * (K / c.qv) + ch * nb + kb] = sc[int_scale_off(kb, r, c.qv, 1)];
           } else {
             uint16_t h;
-            std::memcpy(&h, sc + int_scale_byte(kb, r), 2);
-            static_cast<uint16_t*>(scale_i)[n * (K / 16) + ch * 8 + kb] = h;
+            std::memcpy(&h, sc + int_scale_off(kb, r, c.qv, 2), 2);
+            static_cast<uint16_t*>(scale_i)[n * (K / c.qv) + ch * nb + kb] = h;
           }
         }
       }

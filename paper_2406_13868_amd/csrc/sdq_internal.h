@@ -12,10 +12,16 @@ struct Cfg {
   bool dual;  // dual family (int8 outliers, fp4 inliers, int8 + fp4 activations)
   int n_o, m_o, fmt_o, n_i, m_i, fmt_i, fmt_a, metric, decomp, order;
   bool sc8;     // INT family with two-level e4m3 inlier scales
+  bool e6m2;    // INT family with ufp8-e6m2 inlier scales
+  int qv;       // dense K per inlier scale (INT 16, 32 or 64; MX and dual 32)
   bool y_bf16;  // the GEMM writes Y as bf16 (nearest even of the fp32 result)
+  // INT family: bytes per inlier scale (fp16 2, e4m3 and e6m2 1)
+  int scale_bytes() const { return (sc8 || e6m2) ? 1 : 2; }
 };
 
-inline Layout layout_for(const Cfg& c, int64_t N, int64_t K) { return make_layout(c.mx, N, K, c.sc8); }
+inline Layout layout_for(const Cfg& c, int64_t N, int64_t K) {
+  return make_layout(c.mx, N, K, c.sc8, c.qv, c.scale_bytes());
+}
 
 // Whether packing this configuration reads act_norm.
 inline bool needs_act_norm(const Cfg& c) {
@@ -36,8 +42,14 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   if (c->order != SDQ_ORDER_LARGE && c->order != SDQ_ORDER_SMALL) return SDQ_ERR_CONFIG;
   // a decomposition other than the default chooses among outliers
   if ((c->decomp != SDQ_DECOMP_SAME || c->order != SDQ_ORDER_LARGE) && c->n_o == 0) return SDQ_ERR_CONFIG;
-  if (c->sfmt_i != SDQ_SCALE_DEFAULT && c->sfmt_i != SDQ_SCALE_E4M3) return SDQ_ERR_CONFIG;
-  if (c->sfmt_i == SDQ_SCALE_E4M3 && c->family != SDQ_FAMILY_INT) return SDQ_ERR_CONFIG;
+  if (c->sfmt_i != SDQ_SCALE_DEFAULT && c->sfmt_i != SDQ_SCALE_E4M3 && c->sfmt_i != SDQ_SCALE_UE6M2)
+    return SDQ_ERR_CONFIG;
+  if (c->sfmt_i != SDQ_SCALE_DEFAULT && c->family != SDQ_FAMILY_INT) return SDQ_ERR_CONFIG;
+  if (c->family == SDQ_FAMILY_INT) {
+    if (c->qv_i != 0 && c->qv_i != 16 && c->qv_i != 32 && c->qv_i != 64) return SDQ_ERR_CONFIG;
+  } else if (c->qv_i != 0 && c->qv_i != 32) {
+    return SDQ_ERR_CONFIG;
+  }
   if (c->y_dtype != SDQ_DTYPE_F32 && c->y_dtype != SDQ_DTYPE_BF16) return SDQ_ERR_CONFIG;
   if (mx) {
     if (c->fmt_o != SDQ_FMT_E4M3 || c->fmt_i != SDQ_FMT_E2M1 || c->fmt_a != SDQ_FMT_E4M3)
@@ -77,6 +89,8 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
     out->decomp = c->decomp;
     out->order = c->order;
     out->sc8 = c->sfmt_i == SDQ_SCALE_E4M3;
+    out->e6m2 = c->sfmt_i == SDQ_SCALE_UE6M2;
+    out->qv = c->qv_i ? c->qv_i : (c->family == SDQ_FAMILY_INT ? 16 : 32);
     out->y_bf16 = c->y_dtype == SDQ_DTYPE_BF16;
   }
   return SDQ_OK;

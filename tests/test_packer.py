@@ -448,3 +448,79 @@ def test_dual_sizes_and_validation():
                            None, None) == -3
     assert L.sdq_gemm_dual(C.byref(cfg), None, None, None, None, 1, None, 32, 128, None, None) == -1
     assert L.sdq_gemm_dual(C.byref(cfg), None, None, None, None, 0, None, 32, 128, None, None) == 0
+
+
+# ---- Q-Vector 32 / 64 and ufp8-e6m2 inlier scales (Section 3.3: quantized
+# scale factors and their vector length; Section 6.4's scale-format study)
+@pytest.mark.parametrize("qv", [16, 32, 64])
+@pytest.mark.parametrize("sfmt", ["", "e4m3", "ue6m2"])
+@pytest.mark.parametrize("c", [c for c in CONFIGS if c[0] == "int"], ids=_ids)
+def test_qvector_and_scale_formats_match_oracle(c, sfmt, qv):
+    import dataclasses
+    fam, n_o, m_o, fmt_o, n_i = c
+    lib, ora = _cfgs(fam, n_o, m_o, fmt_o, n_i)
+    lib = dataclasses.replace(lib, sfmt_i=sfmt, qv_i=qv)
+    ora = dataclasses.replace(ora, sfmt_i=sfmt, qv=qv)
+    N, K = 40, 384
+    W = synth.make_w(1, 0, N, K)
+    W[5, :] = 0.0                   # a row without inlier magnitude
+    W[7, 64:128] = 0.0              # all-zero Q-Vectors inside a row
+    Lg, Lo = sdq.pack_logical(W, lib), S.pack_logical(W, ora)
+    def bits(a):  # stored scales: fp16 bits, or one byte per code
+        return a.view(np.uint16) if a.dtype in (np.float16, np.uint16) else a.astype(np.uint8)
+    assert Lg["scale_i"].shape == (N, K // qv)
+    assert np.array_equal(Lg["pos_i"], Lo["pos_i"].astype(np.uint8))
+    assert np.array_equal(Lg["code_i"].view(np.int8), Lo["code_i"].astype(np.int8))
+    assert np.array_equal(bits(Lg["scale_i"]), bits(Lo["scale_i"]))
+    if sfmt == "e4m3":
+        assert np.array_equal(Lg["scale_i_row"].view(np.uint32), Lo["scale_i_row"].view(np.uint32))
+    if n_o:
+        assert np.array_equal(Lg["code_o"], Lo["code_o"])
+    U = sdq.unpack_dense(sdq.pack(W, lib), lib, N, K)
+    assert np.array_equal(bits(U["scale_i"]), bits(Lo["scale_i"]))
+    assert np.array_equal(U["code_i_dense"].view(np.int8), Lo["code_i_dense"].astype(np.int8))
+
+
+def test_qvector_sizes_follow_the_scale_bits():
+    """Logical and physical bytes shrink by the scale bits the longer Q-Vector saves."""
+    N, K = 4096, 4096
+    L = _lib.lib()
+    def sizes(**kw):
+        c = sdq.Config("int", 1, 8, "e4m3", 3, **kw).c()
+        lb, pb = C.c_size_t(), C.c_size_t()
+        assert L.sdq_logical_bytes(C.byref(c), N, K, C.byref(lb)) == 0
+        assert L.sdq_pack_size(C.byref(c), N, K, C.byref(pb)) == 0
+        return lb.value, pb.value
+    l16, p16 = sizes()
+    for qv in (32, 64):
+        l, p = sizes(qv_i=qv)
+        saved = N * (K // 16 - K // qv) * 2        # fp16 scales no longer stored
+        assert l16 - l == saved and p16 - p == saved
+    l6, p6 = sizes(sfmt_i="ue6m2", qv_i=64)
+    assert l16 - l6 == N * (K // 16) * 2 - N * (K // 64)  # one byte per 64 K
+    # validation: INT takes 16/32/64, the MX and dual families only their 32
+    c = sdq.Config("int", 1, 8, "e4m3", 3).c()
+    pb = C.c_size_t()
+    for bad in (8, 48, 128):
+        c.qv_i = bad
+        assert L.sdq_pack_size(C.byref(c), 32, 256, C.byref(pb)) == -3
+    mx = sdq.Config("mx", 1, 8, "e4m3", 2, 8, "e2m1", "e4m3").c()
+    mx.qv_i = 64
+    assert L.sdq_pack_size(C.byref(mx), 32, 256, C.byref(pb)) == -3
+    mx.qv_i, mx.sfmt_i = 32, 2
+    assert L.sdq_pack_size(C.byref(mx), 32, 256, C.byref(pb)) == -3   # e6m2 is INT only
+
+
+def test_e6m2_scales_outside_the_fp16_exact_range_are_refused():
+    """A nonzero ufp8-e6m2 scale must lie in [2^-22, 7168] (exponent field
+    9..43), where an int4 code times it is exact in fp16; the packer refuses
+    weights whose Q-Vector scale falls outside, as it refuses an fp16 overflow."""
+    lib = sdq.Config("int", 1, 8, "e4m3", 3, sfmt_i="ue6m2")
+    W = synth.make_w(1, 0, 32, 256)
+    sdq.pack(W, lib)                                   # workload-scale weights fit
+    for scale in (1e-7, 1e7):
+        with pytest.raises(sdq.SDQError) as e:
+            sdq.pack(W * np.float32(scale), lib)
+        assert e.value.status == -7
+    Z = np.zeros((32, 256), np.float32)                # zero scales are fine
+    sdq.pack(Z, lib)
