@@ -30,7 +30,8 @@ def _run(X: np.ndarray, dtype: str, cfgs):
 @pytest.mark.parametrize("case", [(1, 16, 256, "f32"), (2, 1, 4096, "bf16"), (4, 64, 4096, "bf16"),
                                   (4, 64, 16384, "bf16"), (3, 40, 11008, "bf16"),
                                   (2, 3, 32768, "bf16"), (1, 5, 128, "f32"), (2, 2, 65536, "bf16"),
-                                  (1, 2, 131072, "f32"), (2, 8, 8192, "bf16")],
+                                  (1, 2, 131072, "f32"), (2, 8, 8192, "bf16"),
+                                  (2, 256, 8192, "bf16"), (1, 300, 4224, "f32")],
                          ids=lambda c: f"w{c[0]}-{c[1]}x{c[2]}-{c[3]}")
 def test_act_quant_bit_exact(fam, case):
     wid, M, K, dt = case

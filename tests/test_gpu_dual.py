@@ -97,7 +97,7 @@ def test_gemm_dual_matches_oracle(n_o, n_i, M, N, K):
 
 
 @pytest.mark.parametrize("M", [1, 2])
-@pytest.mark.parametrize("N,K", [(256, 128), (70, 256), (544, 1152), (96, 4096), (40, 11008)])
+@pytest.mark.parametrize("N,K", [(256, 128), (70, 256), (544, 1152), (96, 4096), (40, 11008), (96, 6144)])
 def test_gemm_dual_decode_matches_oracle(M, N, K):
     """One and two tokens (the vector decode kernel; two tokens at K = 11008
     exceed its register budget and take the matrix kernel): one chunk of K
@@ -239,3 +239,21 @@ def test_dual_hip_graph_replays_match_eager(M, y_dtype):
         assert torch.equal(Y.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
         sdq.gemm_dual(Xo, s_a, Xi, Ea, blob, N, K, cfg, out=torch.empty_like(Y))
         torch.cuda.synchronize()
+
+
+def test_gemm_dual_decode_eight_steps_per_wave():
+    """A wide layer whose K parts take eight steps per wave at one token
+    (8192 x 14464: 1024 slices x 113 chunks), checked on a seeded sample of
+    rows (rows are independent, so the oracle packs only those)."""
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs()
+    N, K = 8192, 14464
+    W = synth.make_w(2, 3, N, K)
+    X = synth.make_x(2, 1, K)
+    blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+    say("dual decode S=8", N, K)
+    Xo, s_a, Xi, Ea = sdq.quantize_act_dual(torch.from_numpy(X).cuda(), cfg)
+    Y = sdq.gemm_dual(Xo, s_a, Xi, Ea, blob, N, K, cfg)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(8).choice(N, 48, replace=False))
+    _check(Y.cpu().numpy()[:, rows], X, W[rows], cfg_o, "dual decode S=8")
