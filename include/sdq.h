@@ -87,7 +87,7 @@ enum { SDQ_ORDER_LARGE = 0, SDQ_ORDER_SMALL = 1 };
 enum { SDQ_SCALE_DEFAULT = 0, SDQ_SCALE_E4M3 = 1, SDQ_SCALE_UE6M2 = 2 };
 enum { SDQ_DTYPE_F32 = 0, SDQ_DTYPE_BF16 = 1 };
 /* sdq_gemm_ex / sdq_gemm_ws kernel choice. */
-enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3 };
+enum { SDQ_PATH_AUTO = 0, SDQ_PATH_DECODE = 1, SDQ_PATH_MFMA = 2, SDQ_PATH_DENSE = 3, SDQ_PATH_SPLITK = 4 };
 
 /* One SDQ configuration (the paper's SDQ-k:m-n_o:m{fmt}-n_i:m{fmt} naming,
  * Section 6 "Methodology", restricted to what the kernels implement):
@@ -259,7 +259,8 @@ sdq_status sdq_gemm(const sdq_config* cfg, const void* Xq, const float* s_a, int
  * vector kernel, INT family, any M up to 8), SDQ_PATH_MFMA (matrix-core
  * kernels, any M) or SDQ_PATH_AUTO (what sdq_gemm does).  Returns
  * SDQ_ERR_UNSUPPORTED for a path that does not serve the configuration and
- * for SDQ_PATH_DENSE, which takes a workspace (sdq_gemm_ws). */
+ * for SDQ_PATH_DENSE and SDQ_PATH_SPLITK, which take a workspace
+ * (sdq_gemm_ws). */
 sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, void* Y, void* stream,
                        int32_t path);
@@ -280,8 +281,17 @@ sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x_dtype, int
  * SDQ_PATH_MFMA). */
 sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K, int32_t* path);
 
+/* The path sdq_gemm_ws and sdq_gemm_static take with SDQ_PATH_AUTO
+ * (SDQ_PATH_DECODE, SDQ_PATH_MFMA, SDQ_PATH_DENSE or SDQ_PATH_SPLITK). */
+sdq_status sdq_gemm_path_ws(const sdq_config* cfg, int64_t M, int64_t N, int64_t K, int32_t* path);
+
 /* Device workspace that sdq_gemm_ws needs (the product is sdq_gemm's,
- * Section 5.1).  SDQ_PATH_DENSE, the two-pass matrix-core path of the MX
+ * Section 5.1).  Two paths take one.
+ * SDQ_PATH_SPLITK, the INT family's matrix-core path for 9 to 256 tokens,
+ * splits K into ranges of 128-K chunks handled by different workgroups, each
+ * of which converts its activations to the matrix instruction's f16 once for
+ * four row tiles; the partial sums of the ranges go to the workspace and a
+ * second kernel adds them in range order.  SDQ_PATH_DENSE, the two-pass matrix-core path of the MX
  * family with outliers, first expands every packed weight once into the dense
  * fp8 B operand of the matrix instruction (both branches of a 32-K block
  * merged into one e4m3 value per position under the outlier's e8m0 scale,
@@ -290,11 +300,16 @@ sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
  * 128 tokens (at 512 tokens and more the two passes take less time).
  *   path   SDQ_PATH_AUTO (what sdq_gemm_ws takes: SDQ_PATH_DENSE for the MX
  *          family with outliers when M >= 512 and ceil(N/256) * ceil(M/128)
- *          >= 160, else what sdq_gemm takes), or
- *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE
- *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE, 0 for the other paths
+ *          >= 160; SDQ_PATH_SPLITK for the INT family up to 256 tokens
+ *          where sdq_gemm would take the matrix cores and K >= 8192, or
+ *          M >= 64 and N >= 8192, or M >= 128; else what sdq_gemm takes), or
+ *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE / SDQ_PATH_SPLITK
+ *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE; 4 * S * M * N for
+ *          SDQ_PATH_SPLITK, with S (the number of K ranges, at most K / 512)
+ *          chosen from M, N and K so that about 2048 waves run; 0 for the
+ *          other paths
  * Returns SDQ_ERR_UNSUPPORTED for SDQ_PATH_DENSE outside the MX family with
- * outliers. */
+ * outliers and for SDQ_PATH_SPLITK outside the INT family. */
 sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
                                    int32_t path, size_t* bytes);
 
@@ -307,7 +322,10 @@ sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, 
  * bit when every block merged its inliers (each accumulator takes the same
  * matrix instructions in the same order); the inliers of blocks that did not
  * merge are added after the last chunk instead of within their chunk, a
- * different fp32 rounding order. */
+ * different fp32 rounding order.  SDQ_PATH_SPLITK adds the fp32 partial
+ * sums s_o * acc_o + acc of its K ranges in range order before scaling by
+ * s_a, another fixed rounding order than SDQ_PATH_MFMA's (its products are
+ * as exact; integer-grid inputs give the same results). */
 sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, void* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);
@@ -315,7 +333,7 @@ sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, 
 /* For callers that cannot allocate device memory: code under HIP graph
  * capture that may not call hipMalloc, tight serving loops, harnesses that
  * forbid allocation.  sdq_gemm_ws without a workspace argument: where the path
- * takes a workspace (SDQ_PATH_DENSE) it uses a static device array of
+ * takes a workspace (SDQ_PATH_DENSE, SDQ_PATH_SPLITK) it uses a static device array of
  * SDQ_STATIC_SCRATCH_BYTES (48 MiB) compiled into the library, which every GPU
  * the library runs on holds until the process ends.  Arguments, paths and
  * results are sdq_gemm_ws's (the same kernels, bit for bit); SDQ_PATH_AUTO
@@ -323,7 +341,8 @@ sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, 
  *   - Returns SDQ_ERR_TOO_LARGE, before any GPU work, when the chosen path
  *     needs more scratch than the array holds (32 * ceil(N/32) * K bytes for
  *     SDQ_PATH_DENSE, e.g. 43 MiB for an 11008 x 4096 layer fits and a 16384 x
- *     4096 one does not; SDQ_PATH_MFMA and SDQ_PATH_DECODE need none).
+ *     4096 one does not; sdq_gemm_workspace_size's figure for
+ *     SDQ_PATH_SPLITK; SDQ_PATH_MFMA and SDQ_PATH_DECODE need none).
  *   - Every call on a GPU shares that GPU's array, which keeps the last call's
  *     contents.  Its contents on entry are ignored: the first pass writes every
  *     byte the second reads.  Calls that overlap on one GPU (other streams,

@@ -23,12 +23,12 @@ import numpy as np
 from . import _lib
 from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_DUAL, FAMILY_INT, FAMILY_MX, FMT_E2M1, FMT_E4M3, FMT_INT4,
                    FMT_INT8, METRIC_MAGNITUDE, METRIC_PRODUCT, PATH_AUTO, PATH_DECODE, PATH_MFMA,
-                   PATH_DENSE,
+                   PATH_DENSE, PATH_SPLITK,
                    SDQError)
 
 __all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
            "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
-           "PATH_MFMA", "PATH_DENSE", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual",
+           "PATH_MFMA", "PATH_DENSE", "PATH_SPLITK", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual",
            "gemm_static"]
 
 _FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
@@ -323,7 +323,8 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
          stream=None, workspace=None):
     """Y[M, N] = s_a * (Xq @ (W_o + W_i)^T) on the GPU (fp32 or bf16 output by cfg.y_dtype).
 
-    Paths that take a workspace (the two-pass MX path for many tokens) use
+    Paths that take a workspace (the two-pass MX path for many tokens, the
+    INT family's split-K path for tens to hundreds of tokens) use
     `workspace` (a uint8 CUDA tensor of at least gemm_workspace_size bytes)
     or a fresh one."""
     import torch
@@ -336,7 +337,7 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
     Y = _out(out, M, N, cfg, Xq.device)
     _same_device(Xq, s_a, packed, Y, workspace)
     ws_bytes = gemm_workspace_size(cfg, M, N, K, path)
-    if ws_bytes == 0:
+    if ws_bytes == 0 and path not in (PATH_DENSE, PATH_SPLITK):
         _lib.check(_lib.lib().sdq_gemm_ex(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
                                           _dev(packed, "packed"), N, K, _dev(Y, "Y"),
                                           _stream(stream), path), "sdq_gemm")
@@ -399,9 +400,10 @@ def linear(X, packed, N: int, K: int, cfg: Config, out=None, xq=None, scales=Non
 
 
 def gemm_path(cfg: Config, M: int, N: int, K: int, workspace: bool = False) -> int:
-    """The path sdq_gemm takes (or sdq_gemm_ws, with workspace=True)."""
-    if workspace and gemm_workspace_size(cfg, M, N, K) > 0:
-        return PATH_DENSE
+    """The path sdq_gemm takes (or sdq_gemm_ws and sdq_gemm_static, with workspace=True)."""
     p = C.c_int32()
-    _lib.check(_lib.lib().sdq_gemm_path(C.byref(cfg.c()), M, N, K, C.byref(p)), "sdq_gemm_path")
+    if workspace:
+        _lib.check(_lib.lib().sdq_gemm_path_ws(C.byref(cfg.c()), M, N, K, C.byref(p)), "sdq_gemm_path_ws")
+    else:
+        _lib.check(_lib.lib().sdq_gemm_path(C.byref(cfg.c()), M, N, K, C.byref(p)), "sdq_gemm_path")
     return p.value

@@ -20,14 +20,14 @@ DECOMP = {"same": 0, "magnitude": 1, "product": 2, "error": 3, "output_error": 4
 ORDER = {"large": 0, "small": 1}
 SCALE = {"": 0, "e4m3": 1, "ue6m2": 2}
 DTYPE_F32, DTYPE_BF16 = 0, 1
-PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE = 0, 1, 2, 3
+PATH_AUTO, PATH_DECODE, PATH_MFMA, PATH_DENSE, PATH_SPLITK = 0, 1, 2, 3, 4
 
 # Every exported symbol, as declared in include/sdq.h.
 EXPORTS = (
     "sdq_status_string", "sdq_check", "sdq_pack_size", "sdq_logical_bytes", "sdq_pack",
     "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
     "sdq_gemm_path", "sdq_linear", "sdq_gemm_workspace_size", "sdq_gemm_ws",
-    "sdq_quantize_act_dual", "sdq_gemm_dual", "sdq_gemm_static",
+    "sdq_quantize_act_dual", "sdq_gemm_dual", "sdq_gemm_static", "sdq_gemm_path_ws",
 )
 STATIC_SCRATCH_BYTES = 48 * 1024 * 1024
 
@@ -72,6 +72,7 @@ def lib() -> C.CDLL:
             "sdq_gemm": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp]),
             "sdq_gemm_ex": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),
             "sdq_gemm_path": (C.c_int, [cfgp, i64, i64, i64, P(C.c_int32)]),
+            "sdq_gemm_path_ws": (C.c_int, [cfgp, i64, i64, i64, P(C.c_int32)]),
             "sdq_gemm_workspace_size": (C.c_int, [cfgp, i64, i64, i64, C.c_int32, P(C.c_size_t)]),
             "sdq_gemm_ws": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_size_t, vp,
                                       C.c_int32]),

@@ -26,6 +26,7 @@ SOURCES = [
     "act_quant.hip",
     "gemm_int_decode.hip",
     "gemm_int_mfma.hip",
+    "gemm_int_split.hip",
     "gemm_mx_mfma.hip",
     "gemm_mx_dense.hip",
     "gemm_dual.hip",

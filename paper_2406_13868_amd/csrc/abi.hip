@@ -31,10 +31,40 @@ int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
 // and a grid of at least 160 workgroups of 256 outputs x 128 tokens (measured:
 // 4096x4096 at M = 1024, 128 workgroups, takes 42 us in one pass against 48
 // in two; 11008x4096 at M = 512, 172 workgroups, 56 against 52).
+//
+// The INT family's split-K path where it measured faster than the matrix-core
+// path without a workspace: long rows (4096x16384 at M = 16..64: 30-36 us
+// against 40-45), 64 tokens and more on wide layers (11008x4096 at M = 64:
+// 34 against 44; 16384x4096: 34 against 36) and 128 tokens and more (4096x4096
+// at M = 256: 33 against 34; 11008x4096: 78 against 92).  It loses on small
+// grids, where its second pass over the partial sums costs more than the
+// fuller GPU saves (4096x4096 at M = 64: 19 against 16 us; 16384x4096 at
+// M = 32: 29 against 25).
+bool split_wins(int64_t M, int64_t N, int64_t K) {
+  if (M > kSplitMaxM) return false;
+  return K >= 8192 || (M >= 64 && N >= 8192) || M >= 128;
+}
+
 int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t N, int64_t K) {
   const int64_t wgs = (N + 255) / 256 * ((M + 127) / 128);
   if (c.mx && c.n_o > 0 && M >= kDenseMinM && wgs >= 160) return SDQ_PATH_DENSE;
-  return auto_path(c, M, K);
+  const int32_t p = auto_path(c, M, K);
+  if (!c.mx && p == SDQ_PATH_MFMA && split_wins(M, N, K)) return SDQ_PATH_SPLITK;
+  return p;
+}
+
+// Workspace bytes of a path that takes one (0 for the others).
+size_t path_workspace_bytes(int32_t path, int64_t M, int64_t N, int64_t K) {
+  if (path == SDQ_PATH_DENSE) return mx_dense_workspace_bytes(N, K);
+  if (path == SDQ_PATH_SPLITK) return int_split_workspace_bytes(M, N, K);
+  return 0;
+}
+
+// Whether a workspace path serves the configuration.
+bool path_serves(const Cfg& c, int32_t path) {
+  if (path == SDQ_PATH_DENSE) return c.mx && c.n_o > 0;
+  if (path == SDQ_PATH_SPLITK) return !c.mx;
+  return true;
 }
 
 }  // namespace
@@ -87,6 +117,18 @@ extern "C" sdq_status sdq_gemm_path(const sdq_config* cfg, int64_t M, int64_t N,
   return SDQ_OK;
 }
 
+extern "C" sdq_status sdq_gemm_path_ws(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
+                                       int32_t* path) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!path) return SDQ_ERR_NULL;
+  if (M < 0) return SDQ_ERR_SHAPE;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;
+  *path = auto_path_ws(c, M, N, K);
+  return SDQ_OK;
+}
+
 extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const float* s_a,
                                   int64_t M, const void* packed, int64_t N, int64_t K, void* Y,
                                   void* stream, int32_t path) {
@@ -94,8 +136,8 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
-  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
-  if (path == SDQ_PATH_DENSE) return SDQ_ERR_UNSUPPORTED;  // needs a workspace: sdq_gemm_ws
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_SPLITK) return SDQ_ERR_CONFIG;
+  if (path == SDQ_PATH_DENSE || path == SDQ_PATH_SPLITK) return SDQ_ERR_UNSUPPORTED;  // sdq_gemm_ws
   if (c.dual) return SDQ_ERR_UNSUPPORTED;                  // two activation tensors: sdq_gemm_dual
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
@@ -132,11 +174,11 @@ extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, 
   if (s != SDQ_OK) return s;
   if (!bytes) return SDQ_ERR_NULL;
   if (M < 0) return SDQ_ERR_SHAPE;
-  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_SPLITK) return SDQ_ERR_CONFIG;
   if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
-  if (path == SDQ_PATH_DENSE && !(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
-  *bytes = path == SDQ_PATH_DENSE ? mx_dense_workspace_bytes(N, K) : 0;
+  if (!path_serves(c, path)) return SDQ_ERR_UNSUPPORTED;
+  *bytes = path_workspace_bytes(path, M, N, K);
   return SDQ_OK;
 }
 
@@ -147,22 +189,26 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
-  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_SPLITK) return SDQ_ERR_CONFIG;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
-  if (path != SDQ_PATH_DENSE) return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
-  if (!(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
+  if (path != SDQ_PATH_DENSE && path != SDQ_PATH_SPLITK)
+    return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
+  if (!path_serves(c, path)) return SDQ_ERR_UNSUPPORTED;
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y || !workspace) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
       reinterpret_cast<uintptr_t>(workspace) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
-  if (ws_bytes < mx_dense_workspace_bytes(N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
-  const hipError_t e = launch_mx_dense(c, static_cast<const uint8_t*>(Xq), s_a, M,
-                                       static_cast<const uint8_t*>(packed), N, K, Y, workspace,
-                                       static_cast<hipStream_t>(stream));
+  if (ws_bytes < path_workspace_bytes(path, M, N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  const auto* xq = static_cast<const uint8_t*>(Xq);
+  const auto* blob = static_cast<const uint8_t*>(packed);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense(c, xq, s_a, M, blob, N, K, Y, workspace, st)
+                                              : launch_int_split(c, xq, s_a, M, blob, N, K, Y, workspace, st);
   if (log_enabled())
-    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> mx_dense (two passes)\n", (long long)M,
-                 (long long)N, (long long)K);
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s\n", (long long)M, (long long)N,
+                 (long long)K, path == SDQ_PATH_DENSE ? "mx_dense (two passes)" : "int_split (K ranges)");
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 
@@ -173,22 +219,26 @@ extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, con
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
-  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_DENSE) return SDQ_ERR_CONFIG;
+  if (path < SDQ_PATH_AUTO || path > SDQ_PATH_SPLITK) return SDQ_ERR_CONFIG;
+  if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
-  if (path != SDQ_PATH_DENSE) return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
-  if (!(c.mx && c.n_o > 0)) return SDQ_ERR_UNSUPPORTED;
-  if (mx_dense_workspace_bytes(N, K) > kStaticScratchBytes) return SDQ_ERR_TOO_LARGE;
+  if (path != SDQ_PATH_DENSE && path != SDQ_PATH_SPLITK)
+    return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
+  if (!path_serves(c, path)) return SDQ_ERR_UNSUPPORTED;
+  if (path_workspace_bytes(path, M, N, K) > kStaticScratchBytes) return SDQ_ERR_TOO_LARGE;
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
       reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
-  const hipError_t e = launch_mx_dense_static(c, static_cast<const uint8_t*>(Xq), s_a, M,
-                                              static_cast<const uint8_t*>(packed), N, K, Y,
-                                              static_cast<hipStream_t>(stream));
+  const auto* xq = static_cast<const uint8_t*>(Xq);
+  const auto* blob = static_cast<const uint8_t*>(packed);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense_static(c, xq, s_a, M, blob, N, K, Y, st)
+                                              : int_split_static(c, xq, s_a, M, blob, N, K, Y, st);
   if (log_enabled())
-    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> mx_dense (two passes, static scratch)\n",
-                 (long long)M, (long long)N, (long long)K);
+    std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s, static scratch\n", (long long)M,
+                 (long long)N, (long long)K, path == SDQ_PATH_DENSE ? "mx_dense (two passes)" : "int_split");
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 

@@ -23,22 +23,20 @@
 
 #include <type_traits>
 
+#include "int_frag.h"
 #include "kernels.h"
 #include "tile_out.h"
 
 namespace sdq {
 namespace {
 
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef float f16v __attribute__((ext_vector_type(16)));
-typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+using namespace intfrag;
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int64_t kCUs = 256;                      // compute units of an MI355X
 constexpr int kRowPad = 8;                        // f16 elements of padding per LDS row
 constexpr int kLdsRow = kChunkK + kRowPad;        // 136 f16 = 272 bytes
-constexpr uint32_t kOutPosMagic = (1u << 21) | (1u << 14) | (1u << 7);
 
 struct MfmaArgs {
   const uint8_t* Xq;
@@ -51,113 +49,6 @@ struct MfmaArgs {
   int qs = 0;           // log2(qv / 16): 16-K blocks per inlier scale = 1 << qs
   int srow = 16;        // bytes of one row's inlier scales in a chunk: (128 / qv) * (2 or 1)
 };
-
-// Inlier scale formats of the INT family (template parameter SF).
-enum ScaleFmt { kScaleF16 = 0, kScaleE4M3 = 1, kScaleE6M2 = 2 };
-
-// The fp16 inlier scale of 16-K block kb (its scale kb >> qs) from a row's
-// scale registers sv: fp16 pairs (two per dword), or one code per byte (four
-// per dword): e4m3 (every value is an fp16 value) or ufp8-e6m2, whose values
-// (4 + m) * 2^(e - 33) the packer keeps within [2^-22, 7168], where they and
-// their products with an int4 code are exact in fp16.
-template <int SF>
-__device__ __forceinline__ _Float16 block_scale(const uint32_t* sv, int kb, int qs) {
-  const int e = kb >> qs;
-  if constexpr (SF == kScaleF16) {
-    const uint32_t sw = sv[e >> 1];
-    return __builtin_bit_cast(_Float16, (unsigned short)((e & 1) ? (sw >> 16) : (sw & 0xFFFFu)));
-  } else {
-    const uint32_t byte = (sv[e >> 2] >> (8 * (e & 3))) & 0xFFu;
-    if constexpr (SF == kScaleE4M3) {
-      return (_Float16)__builtin_amdgcn_cvt_f32_fp8(int(byte), 0);
-    } else {
-      const uint32_t ex = byte >> 2, m = byte & 3u;
-      const float v = ex ? float(4u + m) * __uint_as_float((ex + 94u) << 23) : 0.f;  // code 0: scale 0
-      return (_Float16)v;
-    }
-  }
-}
-
-// A row's inlier scales of one chunk (srow = 16, 8, 4 or 2 bytes, naturally
-// aligned), into the low end of four dwords.
-__device__ __forceinline__ uint4 load_row_scales_chunk(const uint8_t* p, int srow) {
-  if (srow == 16) return *reinterpret_cast<const uint4*>(p);
-  if (srow == 8) { const uint2 v = *reinterpret_cast<const uint2*>(p); return make_uint4(v.x, v.y, 0, 0); }
-  if (srow == 4) return make_uint4(*reinterpret_cast<const uint32_t*>(p), 0, 0, 0);
-  return make_uint4(*reinterpret_cast<const uint16_t*>(p), 0, 0, 0);
-}
-
-// Four int8 -> four f16 (two dwords), exact: f16(1024 + (b ^ 0x80)) - 1152 = b.
-__device__ __forceinline__ void i8x4_to_f16x4(uint32_t x, uint32_t& lo, uint32_t& hi) {
-  const uint32_t xb = x ^ 0x80808080u;
-  const uint32_t a = __builtin_amdgcn_perm(0x64646464u, xb, 0x04010400u);
-  const uint32_t b = __builtin_amdgcn_perm(0x64646464u, xb, 0x04030402u);
-  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-  const h2 bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
-  lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2, a) + bias);
-  hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2, b) + bias);
-}
-
-// Dense fp16 inlier fragment of one group word: element p = int4 code at
-// position p (0 where the group has no inlier).
-template <int NI>
-__device__ __forceinline__ h8 inlier_f16(uint32_t w) {
-  uint32_t D = 0;
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const uint32_t q = (w >> (8 * j + 4)) & 0xFu;
-    const uint32_t sh = ((w >> (8 * j)) & 7u) << 2;
-    D |= q << sh;
-  }
-  const uint32_t Db = D ^ 0x88888888u;  // biased nibbles q + 8
-  const uint32_t Ds = Db >> 4;
-  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-  const h2 bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
-  u4v out;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const uint32_t sel = uint32_t(v) | 0x0C00u | (uint32_t(4 + v) << 16) | 0x0C000000u;
-    const uint32_t t = (__builtin_amdgcn_perm(Ds, Db, sel) & 0x000F000Fu) | 0x64006400u;
-    out[v] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2, t) + bias);
-  }
-  return __builtin_bit_cast(h8, out);
-}
-
-// Exact split of the scaled inlier fragment q * s (q an int4 code, s the
-// block's fp16 scale) into two fp16 fragments: hi = f16(q*s) and the residual
-// lo = q*s - hi, which one fused multiply-add produces exactly (q*s has at
-// most 14 significant bits and is a multiple of the lowest bit of s, so the
-// residual is an fp16 number).  Two MFMAs on hi and lo then add q*s*a
-// exactly into the fp32 accumulator, with no per-block scaling of partials.
-__device__ __forceinline__ void scaled_hi_lo(h8 q, _Float16 s, h8& hi, h8& lo) {
-  const h8 sv = {s, s, s, s, s, s, s, s};
-  hi = q * sv;
-  lo = __builtin_elementwise_fma(q, sv, -hi);
-}
-
-// Dense fp16 outlier fragment of one group word (one non-zero at most).
-template <bool OUT_INT8>
-__device__ __forceinline__ h8 outlier_f16(uint32_t w) {
-  float f;
-  if constexpr (OUT_INT8) f = (float)(int(w) >> 24);
-  else f = __builtin_amdgcn_cvt_f32_fp8(int(w), 3);
-  const uint32_t hb = uint32_t(__builtin_bit_cast(unsigned short, (_Float16)f));
-  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
-  const uint32_t val = hb << ((pos & 1u) << 4);
-  const uint32_t d = pos >> 1;
-  u4v out;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) out[v] = d == uint32_t(v) ? val : 0u;
-  return __builtin_bit_cast(h8, out);
-}
-
-// Dense int8 outlier bytes of one group word (position p at byte p of lo:hi).
-__device__ __forceinline__ void outlier_i8(uint32_t w, uint32_t& lo, uint32_t& hi) {
-  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
-  const uint32_t v = (w >> 24) << ((pos & 3u) << 3);
-  lo = pos < 4u ? v : 0u;
-  hi = pos < 4u ? 0u : v;
-}
 
 template <int MS, int NI, bool OUT_INT8, int SF>
 __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
@@ -333,7 +224,12 @@ __global__ __launch_bounds__(NW * 64, 2) void int_mfma_splitk_kernel(MfmaArgs a)
     const u4_ q = __builtin_bit_cast(u4_, __builtin_amdgcn_raw_buffer_load_b128(r, v, so, 0));
     return make_uint4(q[0], q[1], q[2], q[3]);
   };
-  auto load = [&](int c, Stage& st) __attribute__((always_inline)) {
+  auto load = [&](int cv, Stage& st) __attribute__((always_inline)) {
+    // The chunk index derives from the wave index, which the compiler does
+    // not know to be wave-uniform; read it into a scalar register here so
+    // that the loads take it as their scalar offset (otherwise every load is
+    // wrapped in a loop over the distinct values of its lanes).
+    const int c = __builtin_amdgcn_readfirstlane(cv);
     st.w0 = ld16(wr, woff, uint32_t(c) * kWordBytesPerTC);
     st.w1 = ld16(wr, woff + 1024, uint32_t(c) * kWordBytesPerTC);
     // the row's scales of the chunk: a.srow bytes, naturally aligned

@@ -73,6 +73,16 @@ bool decode_fused_fits(int64_t M, int64_t K);
 hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 
+// INT family, matrix-core kernel with K split across workgroups (tens to a
+// few hundred tokens): partial sums of the K ranges in `workspace` (at least
+// int_split_workspace_bytes(M, N, K) bytes, 16-byte aligned), then a second
+// kernel adds them in range order and scales by s_a.
+constexpr int64_t kSplitMaxM = 256;
+size_t int_split_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_int_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                            const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
+                            hipStream_t st);
+
 // MX family, scaled matrix-core kernel (any M).
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                           const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
@@ -91,5 +101,9 @@ constexpr size_t kStaticScratchBytes = size_t(48) << 20;
 hipError_t launch_mx_dense_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                                   const uint8_t* blob, int64_t N, int64_t K, void* Y,
                                   hipStream_t st);
+// launch_int_split with the same static array as the workspace (the caller
+// checks the size).
+hipError_t int_split_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                            const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 
 }  // namespace sdq

@@ -61,8 +61,8 @@ def check(Y, Yref, X, W, cfg_o, what="", act_norm=None):
 
 
 def _paths(fam, M, n_o=1):
-    if fam == "int" and M <= 8:
-        return [sdq.PATH_DECODE, sdq.PATH_MFMA]
+    if fam == "int":
+        return ([sdq.PATH_DECODE] if M <= 8 else []) + [sdq.PATH_MFMA, sdq.PATH_SPLITK]
     if fam == "mx" and n_o:
         return [sdq.PATH_MFMA, sdq.PATH_DENSE]
     return [sdq.PATH_MFMA]

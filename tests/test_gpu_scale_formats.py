@@ -39,7 +39,7 @@ def _run(X, W, cfg, path):
 
 
 def _paths(M):
-    return [sdq.PATH_DECODE, sdq.PATH_MFMA] if M <= 8 else [sdq.PATH_MFMA]
+    return ([sdq.PATH_DECODE] if M <= 8 else []) + [sdq.PATH_MFMA, sdq.PATH_SPLITK]
 
 
 @pytest.mark.parametrize("combo", COMBOS, ids=ID)

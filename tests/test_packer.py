@@ -253,6 +253,25 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(mx, 512, 11008, 4096, workspace=True) == sdq.PATH_DENSE
     assert sdq.gemm_path(mx, 1024, 4096, 4096, workspace=True) == sdq.PATH_MFMA
     assert sdq.gemm_path(mx, 2048, 4096, 4096, workspace=True) == sdq.PATH_DENSE
+    # the INT split-K path where it measured faster than the matrix-core path
+    for (M, N, K) in ((16, 4096, 16384), (64, 4096, 16384), (64, 11008, 4096), (64, 16384, 4096),
+                      (128, 4096, 4096), (256, 11008, 4096)):
+        assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_SPLITK, (M, N, K)
+        assert sdq.gemm_workspace_size(cfg, M, N, K) > 0
+    for (M, N, K) in ((16, 16384, 4096), (32, 16384, 4096), (64, 4096, 4096), (257, 4096, 4096),
+                      (4096, 4096, 4096)):
+        assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_MFMA, (M, N, K)
+        assert sdq.gemm_workspace_size(cfg, M, N, K) == 0
+    assert sdq.gemm_path(cfg, 4, 4096, 4096, workspace=True) == sdq.PATH_DECODE
+    assert sdq.gemm_path(cfg, 4, 4096, 16384) == sdq.PATH_MFMA  # the decode kernel does not fit
+    assert sdq.gemm_path(cfg, 4, 4096, 16384, workspace=True) == sdq.PATH_SPLITK
+    # its workspace: 4 * S * M * N bytes with S K ranges of at least 4 chunks
+    for (M, N, K) in ((64, 16384, 4096), (16, 4096, 16384), (0, 4096, 4096), (200, 100, 128)):
+        b = sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK)
+        S = b // max(4 * M * N, 1)
+        assert b == 4 * S * M * N and 1 <= max(S, 1) <= max(1, K // 512), (M, N, K, S)
+    with pytest.raises(sdq.SDQError):
+        sdq.gemm_workspace_size(mx, 64, 4096, 4096, sdq.PATH_SPLITK)
 
 
 def test_gemm_workspace_size_and_validation():

@@ -1,8 +1,9 @@
 """GPU: sdq_gemm_static, the entry point that allocates nothing, against
 sdq_gemm_ws (the same product with a caller-owned workspace), through the C
-ABI.  Two calls in a row on the two-pass MX path, the second with a smaller
-input, must each equal the workspace entry point bit for bit; the static
-scratch array keeps the first call's contents, which the second must not see.
+ABI.  Two calls in a row on each path that takes a workspace (the two-pass
+MX path and the INT split-K path), the second with a smaller input, must each
+equal the workspace entry point bit for bit; the static scratch array keeps
+the first call's contents, which the second must not see.
 A shape whose workspace exceeds the array is refused before any GPU work."""
 import ctypes as C
 
@@ -64,3 +65,30 @@ def test_static_entry_refuses_a_workspace_beyond_the_array():
     with pytest.raises(sdq.SDQError) as e:
         sdq.gemm_static(Xq, s_a, blob, N, K, CFG, path=sdq.PATH_DENSE)
     assert e.value.status == -8
+
+
+def test_static_entry_equals_workspace_entry_split_k():
+    """The INT family's split-K path (partial sums of K ranges in the scratch
+    array): two calls in a row, the second smaller, each bit for bit equal to
+    sdq_gemm_ws with a caller-owned workspace."""
+    torch = torch_cuda()
+    cfg = sdq.Config.int_family(1, 8, "int8", 3)
+    for (M, N, K, seed) in ((64, 4128, 16384, 1), (20, 1000, 2048, 2)):
+        assert 0 < sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK) <= _lib.STATIC_SCRATCH_BYTES
+        W = synth.make_w(4, 10 + seed, N, K)
+        blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+        Xq, s_a = sdq.quantize_act(torch.from_numpy(synth.make_x(4, M, K, seed=seed)).cuda(), cfg)
+        ws = torch.full((sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK),), 0x7F,
+                        dtype=torch.uint8, device="cuda")  # stale contents must not matter
+        say("static scratch split-K", M, N, K)
+        Y_ws = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=sdq.PATH_SPLITK, workspace=ws)
+        Y_st = torch.full((M, N), float("nan"), device="cuda")
+        st = _lib.lib().sdq_gemm_static(C.byref(cfg.c()), C.c_void_p(Xq.data_ptr()),
+                                        C.c_void_p(s_a.data_ptr()), M, C.c_void_p(blob.data_ptr()), N, K,
+                                        C.c_void_p(Y_st.data_ptr()),
+                                        C.c_void_p(torch.cuda.current_stream().cuda_stream), sdq.PATH_SPLITK)
+        assert st == 0, _lib.STATUS.get(st, st)
+        torch.cuda.synchronize()
+        a, b = Y_ws.cpu().numpy(), Y_st.cpu().numpy()
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), \
+            f"M={M} N={N} K={K}: {int(np.sum(a != b))} outputs differ"
