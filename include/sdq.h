@@ -302,7 +302,7 @@ sdq_status sdq_gemm_path_ws(const sdq_config* cfg, int64_t M, int64_t N, int64_t
  *          family with outliers when M >= 512 and ceil(N/256) * ceil(M/128)
  *          >= 160; SDQ_PATH_SPLITK for the INT family up to 256 tokens
  *          where sdq_gemm would take the matrix cores and K >= 8192, or
- *          M >= 64 and N >= 8192, or M >= 128; else what sdq_gemm takes), or
+ *          M >= 64 and N >= 8192, or M = 256; else what sdq_gemm takes), or
  *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE / SDQ_PATH_SPLITK
  *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE; 4 * S * M * N for
  *          SDQ_PATH_SPLITK, with S (the number of K ranges, at most K / 512)

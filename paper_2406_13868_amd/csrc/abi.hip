@@ -33,16 +33,17 @@ int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
 // in two; 11008x4096 at M = 512, 172 workgroups, 56 against 52).
 //
 // The INT family's split-K path where it measured faster than the matrix-core
-// path without a workspace: long rows (4096x16384 at M = 16..64: 30-36 us
-// against 40-45), 64 tokens and more on wide layers (11008x4096 at M = 64:
-// 34 against 44; 16384x4096: 34 against 36) and 128 tokens and more (4096x4096
-// at M = 256: 33 against 34; 11008x4096: 78 against 92).  It loses on small
-// grids, where its second pass over the partial sums costs more than the
-// fuller GPU saves (4096x4096 at M = 64: 19 against 16 us; 16384x4096 at
-// M = 32: 29 against 25).
+// path without a workspace: long rows (4096x16384 at M = 16 and 64: 25.4 and
+// 33.0 us against 36.0 and 41.3), 64 tokens and more on wide layers
+// (11008x4096 at M = 64: 32.7 against 42.4; 16384x4096: 32.6 against 34.4)
+// and 256 tokens (4096x4096: 31.5 against 32.3; 11008x4096: 73.3 against
+// 89.8).  It loses on small grids, where its second pass over the partial
+// sums costs more than the fuller GPU saves (4096x4096 at M = 64 and 128:
+// 18.9 and 24.4 against 15.6 and 22.2; 16384x4096 at M = 16: 25.4 against
+// 22.2).
 bool split_wins(int64_t M, int64_t N, int64_t K) {
   if (M > kSplitMaxM) return false;
-  return K >= 8192 || (M >= 64 && N >= 8192) || M >= 128;
+  return K >= 8192 || (M >= 64 && N >= 8192) || M >= 256;
 }
 
 int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t N, int64_t K) {

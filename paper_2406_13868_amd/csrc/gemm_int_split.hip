@@ -151,10 +151,13 @@ __global__ __launch_bounds__(kSplitThreads) void int_split_kernel(SplitArgs a) {
   auto compute = [&](const Stage& st, int buf) __attribute__((always_inline)) {
     const uint32_t wv[2][4] = {{st.w0.x, st.w0.y, st.w0.z, st.w0.w}, {st.w1.x, st.w1.y, st.w1.z, st.w1.w}};
     const uint32_t sv[4] = {st.sc.x, st.sc.y, st.sc.z, st.sc.w};
+    _Float16 sb[4];  // the scales of blocks 4h .. 4h + 3, once per chunk
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sb[q] = block_scale<SF>(sv, 4 * h + q, a.qs);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const uint32_t w = wv[i & 1][i >> 1];
-      const _Float16 s = block_scale<SF>(sv, 4 * h + (i >> 1), a.qs);
+      const _Float16 s = sb[i >> 1];
       h8 bh, bl;
       if constexpr (ONE) {
         const h8 sv8 = {s, s, s, s, s, s, s, s};
@@ -236,7 +239,9 @@ __global__ __launch_bounds__(kSplitThreads) void int_split_kernel(SplitArgs a) {
 }
 
 // Y[m, n] = s_a[m] * (part[0][m, n] + part[1][m, n] + ... ) in range order,
-// four outputs per thread (V4: N a multiple of 4, so they share a row).
+// four outputs per thread (V4: N a multiple of 4, so they share a row).  The
+// partial sums of up to 16 ranges are requested together before any is
+// added (one memory round trip instead of one per range).
 template <bool V4>
 __global__ __launch_bounds__(256) void int_split_reduce(const float* part, const float* s_a, void* Y, int M,
                                                         int N, int S, bool y_bf16) {
@@ -244,10 +249,18 @@ __global__ __launch_bounds__(256) void int_split_reduce(const float* part, const
   const size_t i0 = (size_t(blockIdx.x) * 256 + threadIdx.x) * 4;
   if (i0 >= MN) return;
   if constexpr (V4) {
-    float4 v = *reinterpret_cast<const float4*>(part + i0);
-    for (int q = 1; q < S; ++q) {
-      const float4 u = *reinterpret_cast<const float4*>(part + size_t(q) * MN + i0);
-      v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+    constexpr int kMaxS = 16;
+    float4 u[kMaxS];
+#pragma unroll
+    for (int q = 0; q < kMaxS; ++q)
+      if (q < S) u[q] = *reinterpret_cast<const float4*>(part + size_t(q) * MN + i0);
+    float4 v = u[0];
+#pragma unroll
+    for (int q = 1; q < kMaxS; ++q)
+      if (q < S) { v.x += u[q].x; v.y += u[q].y; v.z += u[q].z; v.w += u[q].w; }
+    for (int q = kMaxS; q < S; ++q) {  // more ranges than the requests above hold
+      const float4 w = *reinterpret_cast<const float4*>(part + size_t(q) * MN + i0);
+      v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
     }
     const float sa = s_a[i0 / size_t(N)];
     if (y_bf16) {

@@ -65,25 +65,35 @@ __device__ __forceinline__ void i8x4_to_f16x4(uint32_t x, uint32_t& lo, uint32_t
 }
 
 // Dense fp16 inlier fragment of one group word: element p = int4 code at
-// position p (0 where the group has no inlier).
+// position p (0 where the group has no inlier).  The codes are first placed
+// as nibbles of one dword at their positions: byte j of the word holds slot
+// j's position in bits 0-2, so (w << 2) & 0x1C1C1C holds each slot's shift
+// 4 * position in a byte of its own, and a shift takes only the low five bits
+// of its amount.  The biased nibbles q + 8 then become fp16 1024 + q + 8
+// (0x6400 | nibble) and one packed add of -1032 gives q, two elements at a time.
 template <int NI>
 __device__ __forceinline__ h8 inlier_f16(uint32_t w) {
-  uint32_t D = 0;
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const uint32_t q = (w >> (8 * j + 4)) & 0xFu;
-    const uint32_t sh = ((w >> (8 * j)) & 7u) << 2;
-    D |= q << sh;
-  }
+  uint32_t p4 = (w << 2) & 0x001C1C1Cu;
+  // opaque, so that the shifts below take p4's bytes as they are (a shift
+  // reads the low five bits of its amount) instead of re-deriving them from w
+  asm("" : "+v"(p4));
+  uint32_t D = __builtin_amdgcn_ubfe(w, 4, 4) << p4;
+  if constexpr (NI > 1) D |= __builtin_amdgcn_ubfe(w, 12, 4) << (p4 >> 8);
+  if constexpr (NI > 2) D |= __builtin_amdgcn_ubfe(w, 20, 4) << (p4 >> 16);
   const uint32_t Db = D ^ 0x88888888u;  // biased nibbles q + 8
   const uint32_t Ds = Db >> 4;
+  // the two constants of the and-or in registers: a three-operand
+  // instruction takes no literal on this target, so with literals it would
+  // be two instructions
+  uint32_t lo_mask = 0x000F000Fu, f16_top = 0x64006400u;
+  asm("" : "+s"(lo_mask), "+v"(f16_top));
   typedef _Float16 h2 __attribute__((ext_vector_type(2)));
   const h2 bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
   u4v out;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const uint32_t sel = uint32_t(v) | 0x0C00u | (uint32_t(4 + v) << 16) | 0x0C000000u;
-    const uint32_t t = (__builtin_amdgcn_perm(Ds, Db, sel) & 0x000F000Fu) | 0x64006400u;
+    const uint32_t t = (__builtin_amdgcn_perm(Ds, Db, sel) & lo_mask) | f16_top;
     out[v] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2, t) + bias);
   }
   return __builtin_bit_cast(h8, out);
@@ -118,11 +128,14 @@ __device__ __forceinline__ h8 outlier_f16(uint32_t w) {
 }
 
 // Dense int8 outlier bytes of one group word (position p at byte p of lo:hi).
+// The outlier's position bits (bit 3 of bytes 0-2) gather into bits 24-26 of
+// one 24-bit product, whose bits 21-23 are zero, so one field extract gives
+// 8 * position; a 64-bit shift then places the code byte.
 __device__ __forceinline__ void outlier_i8(uint32_t w, uint32_t& lo, uint32_t& hi) {
-  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
-  const uint32_t v = (w >> 24) << ((pos & 3u) << 3);
-  lo = pos < 4u ? v : 0u;
-  hi = pos < 4u ? 0u : v;
+  const uint32_t p8 = __builtin_amdgcn_ubfe(__umul24(w & 0x00080808u, kOutPosMagic), 21, 6);
+  const uint64_t v = uint64_t(w >> 24) << p8;
+  lo = uint32_t(v);
+  hi = uint32_t(v >> 32);
 }
 
 }  // namespace intfrag

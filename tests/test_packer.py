@@ -255,10 +255,11 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(mx, 2048, 4096, 4096, workspace=True) == sdq.PATH_DENSE
     # the INT split-K path where it measured faster than the matrix-core path
     for (M, N, K) in ((16, 4096, 16384), (64, 4096, 16384), (64, 11008, 4096), (64, 16384, 4096),
-                      (128, 4096, 4096), (256, 11008, 4096)):
+                      (256, 4096, 4096), (256, 11008, 4096)):
         assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_SPLITK, (M, N, K)
         assert sdq.gemm_workspace_size(cfg, M, N, K) > 0
-    for (M, N, K) in ((16, 16384, 4096), (32, 16384, 4096), (64, 4096, 4096), (257, 4096, 4096),
+    for (M, N, K) in ((16, 16384, 4096), (32, 16384, 4096), (64, 4096, 4096), (128, 4096, 4096),
+                      (257, 4096, 4096),
                       (4096, 4096, 4096)):
         assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_MFMA, (M, N, K)
         assert sdq.gemm_workspace_size(cfg, M, N, K) == 0
