@@ -46,6 +46,8 @@ WORKLOADS = {
     "llama7b-attn-decode": (2, [0], 1),
     # q, k and v stacked along N, one launch (N = 12288)
     "llama7b-qkv-decode": (7, [0], 1),
+    # gate and up stacked along N, one launch (N = 22016)
+    "llama7b-gateup-decode": (8, [0], 1),
     "llama7b-mlp-prefill": (3, [0, 1, 2], 2048),
     "opt6.7b-ffn-decode": (4, [0, 1], 64),
     "tiny": (1, [0], 16),

@@ -142,6 +142,11 @@ WORKLOADS: Dict[int, Workload] = {
     # the attention recipe), single-token decode: one launch for three layers.
     7: Workload(7, "llama7b qkv-concatenated decode M=1 12288x4096", (Layer("qkv_proj", 12288, 4096),),
                 (1,), (INT_1x8_E4M3_3x8,), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
+    # LLaMA-7B gate and up projections stacked along N (one weight of 22016
+    # rows, the MLP recipe), single-token decode: they share their input.
+    8: Workload(8, "llama7b gate/up-concatenated decode M=1 22016x4096",
+                (Layer("gate_up_proj", 22016, 4096),), (1,), (INT_1x8_E4M3_3x8,), "bf16", 0.001, 0,
+                30.0, 0.02, 0.002, "t3"),
 }
 
 

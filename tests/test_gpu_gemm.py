@@ -291,6 +291,26 @@ def test_concatenated_projections_equal_separate(c, M):
         check(Yc[:, j * N:(j + 1) * N], Yref, X, W, cfg_o, f"projection {j}")
 
 
+@pytest.mark.parametrize("M", [1, 2])
+def test_stacked_gate_up_equals_separate_full_size(M):
+    """The LLaMA-7B gate and up projections (11008 x 4096 each) stacked into
+    one launch of 22016 rows: every output equals the two separate launches'
+    bit for bit on the decode path, and the oracle's within the tolerance."""
+    torch = torch_cuda()
+    cfg, cfg_o = _cfgs(*INT_CFGS[0])
+    N, K = 11008, 4096
+    X = synth.make_x(8, M, K)
+    Ws = [synth.make_w(8, j, N, K) for j in range(2)]
+    say("gate/up stacked", M)
+    Yc, Xq, s_a, _ = run_gpu(X, np.concatenate(Ws), cfg, path=sdq.PATH_DECODE, x_bf16=True)
+    for j, W in enumerate(Ws):
+        blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
+        Yj = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=sdq.PATH_DECODE).cpu().numpy()
+        assert np.array_equal(Yc[:, j * N:(j + 1) * N].view(np.uint32), Yj.view(np.uint32))
+        Yref, _, _, _ = S.reference(X, W, cfg_o)  # X holds bf16 values already
+        check(Yc[:, j * N:(j + 1) * N], Yref, X, W, cfg_o, f"gate/up projection {j}")
+
+
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[4], MX_CFGS[0]], ids=_ids)
 @pytest.mark.parametrize("M,dt", [(1, "bf16"), (2, "f32"), (3, "bf16"), (4, "f32"), (16, "bf16")])
 def test_linear_equals_quantize_then_gemm(c, M, dt):
