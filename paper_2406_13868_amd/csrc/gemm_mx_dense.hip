@@ -9,7 +9,7 @@
 //   pass 1, mx_densify_kernel: every (32-row tile, 128-K chunk) unit of the
 //     blob becomes its two merged e4m3 B fragments (mx_frag.h), written to a
 //     workspace in the order the matrix instruction reads them;
-//   pass 2, mx_dense_kernel: an fp8 x fp8 scaled-MFMA GEMM over the
+//   pass 2, mx_dense2_kernel: an fp8 x fp8 scaled-MFMA GEMM over the
 //     workspace, the outlier scales (Eo, the merged fragments' e8m0 scales)
 //     read from the blob's scale words.
 // Blocks whose inliers cannot merge (Ei - Eo outside [-5, 6]) carry only their
@@ -24,12 +24,10 @@
 // Pass 2 tiling: a workgroup of 4 waves owns 128 tokens and 8 row tiles (256
 // outputs); each wave owns 2 tiles x 4 sub-tiles of 32 tokens (8 accumulators
 // of 32x32), so every A fragment read from LDS feeds two matrix instructions.
-// Activations are staged per 128-K chunk in LDS (XOR-swizzled); B fragments
-// go from the workspace straight into registers.  A grid with at least two
-// workgroups per CU runs two per CU (two waves per SIMD hide each other's
-// waits; mx_dense2_kernel, three LDS buffers); a smaller grid runs one per CU
-// and requests its data four chunks ahead instead (mx_dense_kernel, two
-// buffers).
+// Activations are staged per 128-K chunk in LDS (three buffers,
+// XOR-swizzled); B fragments go from the workspace straight into registers.
+// Two workgroups run per CU where the grid has them (two waves per SIMD hide
+// each other's waits).
 //
 // What bounds pass 2 (counters on 2048 x 8192 x 4096): the vector memory
 // data path, not the matrix cores.  Every wave loads its own B fragments
@@ -57,7 +55,6 @@ constexpr int kDThreads = kDWaves * 64;
 constexpr int kDTiles = 2 * kDWaves;  // row tiles per workgroup
 constexpr int kDMS = 4;               // 32-token sub-tiles per wave
 constexpr int kDBM = 32 * kDMS;       // tokens per workgroup
-constexpr unsigned kCUs = 256;        // compute units of an MI355X
 
 // ---- pass 1 ----------------------------------------------------------------
 // One wave per (tile, chunk) unit u = tile * n_chunks + chunk, the order of
@@ -177,205 +174,9 @@ __device__ __forceinline__ void add_unmerged(const DenseArgs& a, const int (&til
   }
 }
 
-// One workgroup per CU (a grid that cannot fill two per CU): loads four
-// chunks ahead.  YB: Y as bf16 (a template parameter, so that each form has
-// one store and one read-back width).
-template <int NI, bool YB>
-__global__ __launch_bounds__(kDThreads, 1) void mx_dense_kernel(DenseArgs a) {
-  // fp8 activations of one 128-K chunk: 128 rows of 128 bytes, 16-byte piece
-  // p of row r at piece p ^ lds_swizzle(r)
-  __shared__ __align__(16) uint8_t xs[2][kDBM * kChunkK];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int col = lane & 31, h = lane >> 5;
-  int group, mblock;
-  tile_work(blockIdx.x, gridDim.x / a.m_blocks, a.m_blocks, group, mblock);
-  const int m0 = mblock * kDBM;
-  const int KC = a.n_chunks;
-  const int last = KC - 1;
-
-  int tile[2];
-  bool tok[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int t = group * kDTiles + 2 * wave + j;
-    tok[j] = t < a.n_tiles;
-    tile[j] = min(t, a.n_tiles - 1);  // spare waves recompute the last tile
-  }
-
-  // ---- activations of this block's rows (rows past M read 0, never stored)
-  const __amdgpu_buffer_rsrc_t xr_rsrc =
-      buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, kDBM)) * uint32_t(a.K));
-  // thread tid moves piece tid & 7 of rows (tid >> 3) + 32 i, i < 4; rows r
-  // and r + 32 i share their swizzle
-  const uint32_t xoff = uint32_t(tid >> 3) * uint32_t(a.K) + (tid & 7) * 16;
-  const uint32_t xrow32 = 32u * uint32_t(a.K);
-  const uint32_t xdst0 = uint32_t((tid >> 3) * kChunkK + (((tid & 7) ^ lds_swizzle(tid >> 3)) << 4));
-  // activation register sets, each loaded four chunks before its products
-  // and stored to LDS one chunk before them
-  struct XRegs { i4v r0, r1, r2, r3; };
-  auto load_x = [&](int c, XRegs& x) __attribute__((always_inline)) {
-    const uint32_t so = uint32_t(c) * kChunkK;
-    x.r0 = load16(xr_rsrc, xoff, so);
-    x.r1 = load16(xr_rsrc, xoff + xrow32, so);
-    x.r2 = load16(xr_rsrc, xoff + 2 * xrow32, so);
-    x.r3 = load16(xr_rsrc, xoff + 3 * xrow32, so);
-  };
-  auto store_x = [&](int buf, const XRegs& x) __attribute__((always_inline)) {
-    *reinterpret_cast<i4v*>(&xs[buf][xdst0]) = x.r0;
-    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 32 * kChunkK]) = x.r1;
-    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 64 * kChunkK]) = x.r2;
-    *reinterpret_cast<i4v*>(&xs[buf][xdst0 + 96 * kChunkK]) = x.r3;
-  };
-
-  // ---- B fragments and scale words of the wave's two tiles
-  __amdgpu_buffer_rsrc_t fr[2], sr[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    fr[j] = buffer_rsrc(a.frag + size_t(tile[j]) * KC * kUnitPieces, uint32_t(KC) * kUnitPieces * 16);
-    sr[j] = buffer_rsrc(a.blob + a.scales_off + size_t(tile[j]) * KC * kMxScaleBytesPerTC,
-                        uint32_t(KC) * kMxScaleBytesPerTC);
-  }
-  const uint32_t boff = uint32_t(lane) * 16, soff_l = uint32_t(lane) * 4;
-  struct BStep { i8v b[2]; };
-  auto load_b = [&](int c, int s, BStep& r) __attribute__((always_inline)) {
-    const uint32_t so = (uint32_t(c) * 2 + s) * 2048;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const i4v q0 = load16(fr[j], boff, so);
-      const i4v q1 = load16(fr[j], boff + 1024, so);
-      r.b[j] = __builtin_shufflevector(q0, q1, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
-  };
-  struct Scales { uint32_t w[2]; };
-  auto load_sc = [&](int c, Scales& r) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      r.w[j] = __builtin_amdgcn_raw_buffer_load_b32(sr[j], soff_l, uint32_t(c) * kMxScaleBytesPerTC, 0);
-  };
-
-  f16v acc[2][kDMS];
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int ms = 0; ms < kDMS; ++ms)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[j][ms][e] = 0.f;
-
-  // A-fragment byte offsets of this lane in a chunk buffer: row ms*32 + col,
-  // logical pieces 4s + h and 4s + h + 2 for step s
-  uint32_t aoff[2][2];
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-      aoff[s][u] = uint32_t(col * kChunkK + (((4 * s + h + 2 * u) ^ lds_swizzle(col)) << 4));
-
-  bool bad = false;  // this lane saw a block whose inliers did not merge
-  auto mfmas = [&](int buf, int s, const BStep& B, const Scales& S) __attribute__((always_inline)) {
-    int e[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) e[j] = int((S.w[j] >> (16 * s)) & 0xFFu);  // Eo of block 2s + h
-#pragma unroll
-    for (int ms = 0; ms < kDMS; ++ms) {
-      const i4v a0 = *reinterpret_cast<const i4v*>(&xs[buf][aoff[s][0] + ms * 32 * kChunkK]);
-      const i4v a1 = *reinterpret_cast<const i4v*>(&xs[buf][aoff[s][1] + ms * 32 * kChunkK]);
-      const i8v av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[j][ms] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, B.b[j], acc[j][ms], 0, 0, 0, 127, 0, e[j]);
-    }
-  };
-
-  // The products of a chunk stay before its barrier: the matrix intrinsic has
-  // no memory effects, so without this the compiler sinks them past the
-  // barrier and the loads of the next chunk no longer overlap them.
-  auto pin_acc = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int ms = 0; ms < kDMS; ++ms) asm volatile("" : "+a"(acc[j][ms]));
-  };
-
-  // ---- pipeline, four chunks deep.  Chunk c uses LDS buffer c & 1, B step
-  //      sets B[2(c & 3)] and B[2(c & 3) + 1], scale set S[c & 3] and, for its
-  //      activations, register set X[c & 3]; each set is refilled for chunk
-  //      c + 4 right after its use.  Activations of chunk c + 1 go from
-  //      registers to LDS after the products of chunk c.  Loads past the last
-  //      chunk re-read it (never used).
-  BStep B[8];
-  Scales S[4];
-  XRegs X[4];
-  load_x(0, X[0]);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    load_b(min(i, last), 0, B[2 * i]);
-    load_b(min(i, last), 1, B[2 * i + 1]);
-    load_sc(min(i, last), S[i]);
-    if (i > 0) load_x(min(i, last), X[i]);
-  }
-  store_x(0, X[0]);
-  load_x(min(4, last), X[0]);
-  __syncthreads();
-  // Every request of the prologue complete before the loop: the wait counts
-  // the compiler derives at the loop head then come from the loop's own
-  // order of requests alone, not from the stricter ones of the prologue.
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  // chunk c = base + I, I = c & 3 (a compile-time index into the sets)
-  auto chunk = [&](auto I, int c) __attribute__((always_inline)) {
-    constexpr int i = decltype(I)::value, buf = i & 1, nx = (i + 1) & 3;
-    mfmas(buf, 0, B[2 * i], S[i]);
-    load_b(min(c + 4, last), 0, B[2 * i]);
-    mfmas(buf, 1, B[2 * i + 1], S[i]);
-    load_b(min(c + 4, last), 1, B[2 * i + 1]);
-    bad |= unmerged(S[i].w[0]) || unmerged(S[i].w[1]);
-    load_sc(min(c + 4, last), S[i]);
-    store_x(buf ^ 1, X[nx]);  // chunk c + 1
-    load_x(min(c + 5, last), X[nx]);
-    pin_acc();
-    __syncthreads();
-  };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  int c = 0;
-  for (; c + 3 < KC; c += 4) {  // one exit, so the accumulators stay in place
-    chunk(I0{}, c);
-    chunk(I1{}, c + 1);
-    chunk(I2{}, c + 2);
-    chunk(I3{}, c + 3);
-  }
-  const int rem = KC - c;  // 0..3 chunks left, wave-uniform
-  if (rem > 0) chunk(I0{}, c);
-  if (rem > 1) chunk(I1{}, c + 1);
-  if (rem > 2) chunk(I2{}, c + 2);
-
-  const OutRows yr = out_rows(a.Y, YB, a.M, a.N, m0, kDBM);
-  // ---- outputs (a wave with a block that did not merge its inliers adds
-  //      them to its stored values below)
-  {
-    const RowScales<kDMS> rs = load_row_scales<kDMS>(a.s_a, a.M, m0, h);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (!tok[j]) continue;
-      const int n = tile[j] * kTileN + col;
-      if (n >= a.N) continue;
-#pragma unroll
-      for (int ms = 0; ms < kDMS; ++ms)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, ms, e, h, rs.v[ms][e] * acc[j][ms][e]);
-    }
-  }
-
-  if (__any(bad)) add_unmerged<NI, YB>(a, tile, tok, xr_rsrc, yr, m0, col, h, boff, soff_l, sr);
-}
-
-// Pass 2, a pipeline for two workgroups per CU.  Same tiling as
-// mx_dense_kernel (4 waves, 128 tokens x 256 outputs, each wave 2 row tiles x
-// 4 token sub-tiles); what differs is how the activations reach the matrix
-// instructions:
+// Pass 2: 4 waves own 128 tokens x 256 outputs (each wave 2 row tiles x 4
+// token sub-tiles), two workgroups per CU where the grid has them.  How the
+// activations reach the matrix instructions:
 //   - three LDS chunk buffers: the activations of chunk c + 2 are requested
 //     when chunk c starts and written to their buffer when it ends, so the
 //     next chunk's buffer is complete and visible before the barrier that
@@ -567,17 +368,10 @@ hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8
               L.scales_off, int((M + kDBM - 1) / kDBM)};
   const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
   const unsigned wgs = unsigned(groups * a.m_blocks);
-  if (wgs < 2 * kCUs) {
-    if (y_bf16)
-      hipLaunchKernelGGL((mx_dense_kernel<NI, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
-    else
-      hipLaunchKernelGGL((mx_dense_kernel<NI, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
-  } else {
-    if (y_bf16)
-      hipLaunchKernelGGL((mx_dense2_kernel<NI, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
-    else
-      hipLaunchKernelGGL((mx_dense2_kernel<NI, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
-  }
+  if (y_bf16)
+    hipLaunchKernelGGL((mx_dense2_kernel<NI, true>), dim3(wgs), dim3(kDThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((mx_dense2_kernel<NI, false>), dim3(wgs), dim3(kDThreads), 0, st, a);
   return hipGetLastError();
 }
 
