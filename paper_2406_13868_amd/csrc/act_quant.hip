@@ -94,6 +94,40 @@ __device__ __forceinline__ void quant_store8(const float (&v)[8], float inv, uin
   *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
 }
 
+// Eight consecutive elements as loaded (16 bytes of bf16 or 32 of fp32); a
+// bf16 row is kept in this form between its two uses, which halves the
+// registers of the widest rows (more rows in flight per compute unit).
+template <bool BF16>
+struct Raw8 {
+  uint4 q[BF16 ? 1 : 2];
+};
+template <bool BF16>
+__device__ __forceinline__ void load_raw8(const void* X, int64_t idx, Raw8<BF16>& r) {
+  if constexpr (BF16) {
+    r.q[0] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(X) + idx);
+  } else {
+    r.q[0] = *reinterpret_cast<const uint4*>(static_cast<const float*>(X) + idx);
+    r.q[1] = *reinterpret_cast<const uint4*>(static_cast<const float*>(X) + idx + 4);
+  }
+}
+template <bool BF16>
+__device__ __forceinline__ void widen8(const Raw8<BF16>& r, float (&v)[8]) {
+  if constexpr (BF16) {
+    const uint32_t w[4] = {r.q[0].x, r.q[0].y, r.q[0].z, r.q[0].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      v[4 * h] = __uint_as_float(r.q[h].x); v[4 * h + 1] = __uint_as_float(r.q[h].y);
+      v[4 * h + 2] = __uint_as_float(r.q[h].z); v[4 * h + 3] = __uint_as_float(r.q[h].w);
+    }
+  }
+}
+
 template <bool BF16, bool E4M3, int CH, int NT>
 __global__ __launch_bounds__(NT) void act_quant_regs(const void* __restrict__ X, int64_t K,
                                                      uint8_t* __restrict__ Xq,
@@ -101,15 +135,21 @@ __global__ __launch_bounds__(NT) void act_quant_regs(const void* __restrict__ X,
   __shared__ float red[NT / 64];
   const int64_t m = blockIdx.x;
   const int64_t P = K >> 3;  // pieces of 8 elements
-  float v[CH][8];
+  Raw8<BF16> r[CH];
   float amax = 0.f;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int64_t p = threadIdx.x + c * NT;
-    if (p < P) {
-      load8<BF16>(X, m * K + p * 8, v[c]);
+    if (p < P) load_raw8<BF16>(X, m * K + p * 8, r[c]);
+  }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[c][i]));
+  for (int c = 0; c < CH; ++c) {
+    const int64_t p = threadIdx.x + c * NT;
+    if (p < P) {
+      float v[8];
+      widen8<BF16>(r[c], v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(v[i]));
     }
   }
   amax = block_max<NT>(amax, red);
@@ -119,7 +159,11 @@ __global__ __launch_bounds__(NT) void act_quant_regs(const void* __restrict__ X,
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int64_t p = threadIdx.x + c * NT;
-    if (p < P) quant_store8<E4M3>(v[c], inv, Xq + m * K + p * 8);
+    if (p < P) {
+      float v[8];
+      widen8<BF16>(r[c], v);
+      quant_store8<E4M3>(v, inv, Xq + m * K + p * 8);
+    }
   }
 }
 
