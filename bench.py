@@ -442,8 +442,8 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
     roof["traffic_source"] = (f"{tr['source']} (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE, copy-calibrated)"
                               if tr else None)
     roof["kernel_us"] = round(gemm_us / len(Ls), 3)
-    # kernels per GEMM call: the two-pass path's time is both passes together
-    roof["kernels_per_call"] = 2 if sdq.PATH_DENSE in paths else 1
+    # kernels per GEMM call: a two-pass path's time is both passes together
+    roof["kernels_per_call"] = 2 if (sdq.PATH_DENSE in paths or sdq.PATH_SPLITK in paths) else 1
     roof["timing"] = (f"HIP events around one graph replay of {n_g} GEMM calls over {R} rotated copies, "
                       "after a 512 MB fill")
 
@@ -474,7 +474,8 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
         "dtype": {"int": "int8", "mx": "fp8", "dual": "int8+fp4"}[cfg.family],
         "config": {"workload": wl_name, "M": M, "layers": [[L.name, L.N, L.K] for L in Ls],
                    "formats": fmt.label,
-                   "gemm_path": "dual mfma" if dual else ["decode", "mfma", "dense (two passes)"][paths[-1] - 1],
+                   "gemm_path": "dual mfma" if dual else ", ".join(
+                       ["decode", "mfma", "dense (two passes)", "split-K (two passes)"][p - 1] for p in paths),
                    "parallelism": "none (one GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,
