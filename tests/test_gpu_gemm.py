@@ -370,36 +370,58 @@ def test_hip_graph_replays_match_eager(c):
         torch.cuda.synchronize()
 
 
-def test_hip_graph_replays_match_eager_two_pass():
-    """The two-pass MX path (workspace allocated before capture) replays like eager."""
+@pytest.mark.parametrize("which", ["mx-dense", "int-splitk"])
+def test_hip_graph_replays_match_eager_two_pass(which):
+    """The workspace paths (two-pass MX, INT split-K; workspace allocated
+    before capture) replay like eager, whatever the workspace held."""
     torch = torch_cuda()
-    cfg, _ = _cfgs(*MX_CFGS[1])
-    N, K, M = 544, 640, 600
+    if which == "mx-dense":
+        cfg, _ = _cfgs(*MX_CFGS[1])
+        N, K, M, path = 544, 640, 600, sdq.PATH_DENSE
+    else:
+        cfg, _ = _cfgs(*INT_CFGS[1])
+        N, K, M, path = 1000, 2304, 100, sdq.PATH_SPLITK
     X = torch.from_numpy(synth.make_x(2, M, K)).cuda()
     blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
     Xq, s_a = sdq.quantize_act(X, cfg)
-    ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_DENSE), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(sdq.gemm_workspace_size(cfg, M, N, K, path), dtype=torch.uint8, device="cuda")
     Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    say("graph two-pass")
-    sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
+    say("graph two-pass", which)
+    sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=path, workspace=ws)
     torch.cuda.synchronize()
     ref = Y.clone()
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=path, workspace=ws)
     torch.cuda.current_stream().wait_stream(side)
     with torch.cuda.graph(g):
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=sdq.PATH_DENSE, workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=Y, path=path, workspace=ws)
     for rep in range(4):
         Y.fill_(float("nan"))
         ws.fill_(0x5A)
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
-        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y), path=sdq.PATH_DENSE, workspace=ws)
+        sdq.gemm(Xq, s_a, blob, N, K, cfg, out=torch.empty_like(Y), path=path, workspace=ws)
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[3], INT_CFGS[5]], ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(9, 4128, 512), (31, 300, 2560), (33, 97, 4096), (64, 1000, 16384),
+                                   (100, 544, 1152), (129, 64, 8192), (200, 2080, 640), (256, 33, 128)])
+def test_split_k_ragged_shapes(c, M, N, K):
+    """The split-K path on token counts around its 32- and 64-token blocks,
+    row counts that leave a part of a 128-row group, K ranges from one chunk
+    to 128 (1 to 32 ranges), against the oracle."""
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(4, M, K)
+    W = synth.make_w(4, 3, N, K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    say("split-K ragged", _ids(c), M, N, K)
+    Y, _, _, _ = run_gpu(X, W, cfg, sdq.PATH_SPLITK)
+    check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} split-K")
 
 
 def _split_case(kind, N, K, rng):
