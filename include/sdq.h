@@ -29,7 +29,15 @@
  *     passed as void*; NULL = the default stream), enqueue their kernels on
  *     that stream and return without synchronizing.  A launch failure is
  *     reported as SDQ_ERR_HIP; a fault inside a kernel surfaces at the
- *     caller's next synchronization.
+ *     caller's next synchronization.  An error that an earlier HIP call on
+ *     the calling thread left pending (what hipGetLastError would return) is
+ *     read and dropped before the launches, so that it is not reported as the
+ *     call's own.
+ *   - The library links the HIP runtime by its soname (libamdhip64.so.7).  In
+ *     a process that also loads another copy of the runtime under another
+ *     file name (PyTorch's ROCm wheels carry one), load that copy first: the
+ *     library then shares it.  The other order leaves two runtimes in the
+ *     process, and the library's launches find no device.
  *   - Host entry points (pack, logical pack, unpack) take host pointers and
  *     are deterministic: the output does not depend on the thread count.
  */
@@ -147,7 +155,9 @@ typedef struct {
 const char* sdq_status_string(sdq_status s);
 
 /* Validate a configuration for a W of shape [N, K].  K must be a positive
- * multiple of 128 up to 2^22 and N positive up to 2^21.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
+ * multiple of 32 (and of qv_i when that is 64) up to 2^22 and N positive up
+ * to 2^21.  The kernels take K in chunks of 128: when K is not a multiple of
+ * 128 the blob pads the last chunk with zero codes and scales.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
  * SDQ_ERR_UNSUPPORTED without touching anything else. */
 sdq_status sdq_check(const sdq_config* cfg, int64_t N, int64_t K);
 
@@ -236,7 +246,7 @@ sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed, size_t by
  *   Xq     device, [M, K] row-major, 1 byte per element (int8 for the INT
  *          family, e4m3 bits for the MX family)
  *   s_a    device, [M] fp32
- * M = 0 is a no-op.  K must be a positive multiple of 128. */
+ * M = 0 is a no-op.  K as in sdq_check. */
 sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int32_t x_dtype,
                             int64_t M, int64_t K, void* Xq, float* s_a, void* stream);
 

@@ -49,6 +49,38 @@ class SDQError(RuntimeError):
 _lib = None
 
 
+def _bind_to_torch_runtime() -> None:
+    """libsdq.so asks for the HIP runtime by its soname, libamdhip64.so.7.
+    torch's ROCm wheel carries its own copy of the runtime (same soname), which
+    its libraries ask for as libamdhip64.so.  With torch imported first the
+    loader hands libsdq.so torch's copy.  Loaded the other way round, the
+    process would hold two HIP runtimes (and two HSA runtimes): the one torch
+    initialises owns the GPU and the library's launches find no device."""
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # no torch: the library's own runtime is the only one
+        pass
+
+
+def _hip_runtimes() -> set:
+    """Distinct files of the HIP runtime mapped into this process (Linux)."""
+    try:
+        with open("/proc/self/maps") as f:
+            maps = f.read()
+    except OSError:
+        return set()
+    return {os.path.realpath(line.split()[-1]) for line in maps.splitlines()
+            if "/libamdhip64.so" in line}
+
+
+def _check_one_runtime() -> None:
+    rts = _hip_runtimes()
+    if len(rts) > 1:
+        raise RuntimeError("two HIP runtimes are loaded in this process (" + ", ".join(sorted(rts)) +
+                           "): load libsdq.so after the runtime the rest of the process uses "
+                           "(import torch first)")
+
+
 def lib() -> C.CDLL:
     """Load libsdq.so; raises if it has not been built (there is no fallback)."""
     global _lib
@@ -56,7 +88,9 @@ def lib() -> C.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_2406_13868_amd.build` (no CPU fallback exists)")
+        _bind_to_torch_runtime()
         L = C.CDLL(LIB_PATH)
+        _check_one_runtime()
         P = C.POINTER
         cfgp = P(sdq_config)
         i64, vp, f32p, u8p = C.c_int64, C.c_void_p, P(C.c_float), P(C.c_uint8)

@@ -68,13 +68,21 @@ bool path_serves(const Cfg& c, int32_t path) {
   return true;
 }
 
+// The launchers report a failed launch through hipGetLastError, which also
+// returns an error that an earlier, unrelated HIP call on this thread left
+// pending (the runtime keeps one per thread until it is read).  Reading it
+// here, before the launches, keeps such an error from being reported as this
+// call's.  A sticky error (a faulted context) is not lost: every later launch
+// fails again.
+void drop_pending_error() { (void)hipGetLastError(); }
+
 }  // namespace
 
 extern "C" const char* sdq_status_string(sdq_status s) {
   switch (s) {
     case SDQ_OK: return "SDQ_OK: success";
     case SDQ_ERR_NULL: return "SDQ_ERR_NULL: a required pointer is NULL";
-    case SDQ_ERR_SHAPE: return "SDQ_ERR_SHAPE: M, N or K out of range or K not a multiple of 128";
+    case SDQ_ERR_SHAPE: return "SDQ_ERR_SHAPE: M, N or K out of range, or K not a multiple of 32 (or of a 64-K scale vector)";
     case SDQ_ERR_CONFIG: return "SDQ_ERR_CONFIG: malformed configuration";
     case SDQ_ERR_BUFFER_TOO_SMALL: return "SDQ_ERR_BUFFER_TOO_SMALL: output buffer too small";
     case SDQ_ERR_HIP: return "SDQ_ERR_HIP: a HIP call or kernel launch failed";
@@ -101,6 +109,7 @@ extern "C" sdq_status sdq_quantize_act(const sdq_config* cfg, const void* X, int
   if (M == 0) return SDQ_OK;
   if (!X || !Xq || !s_a) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq) % 16) return SDQ_ERR_SHAPE;
+  drop_pending_error();
   const hipError_t e = launch_act_quant(c, X, x_dtype, M, K, static_cast<uint8_t*>(Xq), s_a,
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
@@ -150,6 +159,7 @@ extern "C" sdq_status sdq_gemm_ex(const sdq_config* cfg, const void* Xq, const f
   const auto* xq = static_cast<const uint8_t*>(Xq);
   const auto* blob = static_cast<const uint8_t*>(packed);
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  drop_pending_error();
   hipError_t e;
   const char* name;
   if (c.mx) {
@@ -205,6 +215,7 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   const auto* xq = static_cast<const uint8_t*>(Xq);
   const auto* blob = static_cast<const uint8_t*>(packed);
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  drop_pending_error();
   const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense(c, xq, s_a, M, blob, N, K, Y, workspace, st)
                                               : launch_int_split(c, xq, s_a, M, blob, N, K, Y, workspace, st);
   if (log_enabled())
@@ -235,6 +246,7 @@ extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, con
   const auto* xq = static_cast<const uint8_t*>(Xq);
   const auto* blob = static_cast<const uint8_t*>(packed);
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  drop_pending_error();
   const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense_static(c, xq, s_a, M, blob, N, K, Y, st)
                                               : int_split_static(c, xq, s_a, M, blob, N, K, Y, st);
   if (log_enabled())
@@ -264,6 +276,7 @@ extern "C" sdq_status sdq_linear(const sdq_config* cfg, const void* X, int32_t x
     return SDQ_ERR_SHAPE;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (auto_path(c, M, K) == SDQ_PATH_DECODE && decode_fused_fits(M, K)) {
+    drop_pending_error();
     const hipError_t e = launch_int_decode_fused(c, X, x_dtype, M, static_cast<uint8_t*>(Xq), s_a,
                                                  static_cast<const uint8_t*>(packed), N, K, Y, st);
     if (log_enabled())
@@ -290,6 +303,7 @@ extern "C" sdq_status sdq_quantize_act_dual(const sdq_config* cfg, const void* X
   if (reinterpret_cast<uintptr_t>(X) % 16 || reinterpret_cast<uintptr_t>(Xq_o) % 16 ||
       reinterpret_cast<uintptr_t>(Xq_i) % 16)
     return SDQ_ERR_SHAPE;
+  drop_pending_error();
   const hipError_t e = launch_act_quant_dual(X, x_dtype, M, K, static_cast<uint8_t*>(Xq_o), s_a_o,
                                              static_cast<uint8_t*>(Xq_i), static_cast<uint8_t*>(e_a_i),
                                              static_cast<hipStream_t>(stream));
@@ -309,6 +323,7 @@ extern "C" sdq_status sdq_gemm_dual(const sdq_config* cfg, const void* Xq_o, con
   if (reinterpret_cast<uintptr_t>(Xq_o) % 16 || reinterpret_cast<uintptr_t>(Xq_i) % 16 ||
       reinterpret_cast<uintptr_t>(packed) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
+  drop_pending_error();
   const hipError_t e = launch_dual_mfma(c, static_cast<const uint8_t*>(Xq_o), s_a_o,
                                         static_cast<const uint8_t*>(Xq_i), static_cast<const uint8_t*>(e_a_i),
                                         M, static_cast<const uint8_t*>(packed), N, K, Y,

@@ -256,7 +256,7 @@ __global__ __launch_bounds__(NT) void act_quant_dual(const void* __restrict__ X,
                                                      uint8_t* __restrict__ Xi, uint8_t* __restrict__ Ea) {
   __shared__ float red[NT / 64];
   const int64_t m = blockIdx.x;
-  const int64_t P = K >> 3;  // pieces of 8 elements, a multiple of 16
+  const int64_t P = K >> 3;  // pieces of 8 elements, a multiple of 4 (K a multiple of 32)
   float amax = 0.f;
   for (int64_t p = threadIdx.x; p < P; p += NT) {
     float v[8];

@@ -57,6 +57,22 @@ __device__ __forceinline__ int ld8(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_
   return int(__builtin_amdgcn_raw_buffer_load_b8(r, v, s, 0));
 }
 
+// The four e8m0 scales of chunk cs of the A_i row at byte v of ea, block j
+// in byte j.  One dword when K is a multiple of 128.  Otherwise a row's K/32
+// bytes do not fill whole dwords, and a dword reaching past the end of the
+// buffer's range would read as 0 whole: four byte loads, and 127 (2^0) for
+// the blocks past K, whose weight codes are zero and add nothing whatever
+// their scale.
+__device__ __forceinline__ uint32_t ld_ea4(__amdgpu_buffer_rsrc_t ea, uint32_t v, uint32_t cs, uint32_t K) {
+  if ((K & 127u) == 0) return __builtin_amdgcn_raw_buffer_load_b32(ea, v, cs * 4, 0);
+  uint32_t e = 0;
+#pragma unroll
+  for (uint32_t j = 0; j < 4; ++j)
+    e |= (cs * 4 + j < K / 32 ? uint32_t(__builtin_amdgcn_raw_buffer_load_b8(ea, v + j, cs * 4, 0)) : 127u)
+         << (8 * j);
+  return e;
+}
+
 // Dense int8 bytes of two 8-groups from their half-words (bits 0-2 position,
 // bits 8-15 code): group i fills dwords 2i, 2i + 1.
 __device__ __forceinline__ v4i outlier_bytes(uint32_t hw2) {
@@ -122,7 +138,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
       if (BM * 4 % kDThreads == 0 || p < BM * 4)
         x.i[j] = ld16(xi, uint32_t(p >> 2) * (K / 2) + uint32_t(p & 3) * 16, cs * (kChunkK / 2));
     }
-    if (tid < BM) x.e = __builtin_amdgcn_raw_buffer_load_b32(ea, uint32_t(tid) * (K / 32), cs * 4, 0);
+    if (tid < BM) x.e = ld_ea4(ea, uint32_t(tid) * (K / 32), cs, K);
   };
   auto store_x = [&](int buf, const XRegs& x) __attribute__((always_inline)) {
 #pragma unroll
@@ -273,7 +289,7 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
       st.sb[s] = ld8(ws, uint32_t(s * 64 + lane), cs * kDualScaleBytesPerTC);
       st.ai[s] = ld16(xi, uint32_t(col) * (K / 2) + uint32_t(s * 32 + h * 16), cs * (kChunkK / 2));
     }
-    st.sa = __builtin_amdgcn_raw_buffer_load_b32(ea, uint32_t(col) * (K / 32), cs * 4, 0);
+    st.sa = ld_ea4(ea, uint32_t(col) * (K / 32), cs, K);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       st.hw[u] = __builtin_amdgcn_raw_buffer_load_b32(wo, uint32_t(u * 64 + lane) * 4u, cs * kDualOutBytesPerTC, 0);

@@ -228,7 +228,7 @@ int steps_for_dual(int64_t M, int64_t N, int64_t KC) {
 
 bool dual_decode_fits(int64_t M, int64_t N, int64_t K) {
   if (M < 1 || M > kDecTokensMax) return false;
-  return steps_for_dual(M, N, K / kChunkK) > 0;
+  return steps_for_dual(M, N, (K + kChunkK - 1) / kChunkK) > 0;
 }
 
 hipError_t launch_dual_decode(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,

@@ -404,9 +404,9 @@ __global__ __launch_bounds__(SPW * KS * 64) void int_decode_kernel(DecodeArgs a)
   }
 }
 
-// steps per wave for K (K is a multiple of 128) when KS waves share a slice
+// steps per wave for K (a partial last chunk counts whole) when KS waves share a slice
 int steps_for(int64_t K, int KS) {
-  const int64_t all_steps = (K / kChunkK + kStepChunks - 1) / kStepChunks;
+  const int64_t all_steps = ((K + kChunkK - 1) / kChunkK + kStepChunks - 1) / kStepChunks;
   return int((all_steps + KS - 1) / KS);
 }
 

@@ -71,14 +71,22 @@ __global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
   constexpr int kPieces = BM * 8;
   constexpr int kPerThread = (kPieces + kThreads - 1) / kThreads;
   uint4 xr[kPerThread];
+  // the block's rows through a buffer resource: rows past M, and the bytes of
+  // a last partial chunk past the end of the tensor, read 0
+  const __amdgpu_buffer_rsrc_t x_rsrc =
+      buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, BM)) * uint32_t(a.K));
   auto load_x = [&](int c) {
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
       const int pc = tid + i * kThreads;
       const int rr = pc >> 3, cp = pc & 7;
       xr[i] = make_uint4(0, 0, 0, 0);
-      if (pc < kPieces && m0 + rr < a.M)
-        xr[i] = *reinterpret_cast<const uint4*>(a.Xq + size_t(m0 + rr) * a.K + c * kChunkK + cp * 16);
+      if (pc < kPieces) {
+        typedef unsigned int u4_ __attribute__((ext_vector_type(4)));
+        const u4_ q = __builtin_bit_cast(u4_, __builtin_amdgcn_raw_buffer_load_b128(
+            x_rsrc, uint32_t(rr) * uint32_t(a.K) + uint32_t(cp) * 16u, uint32_t(c) * kChunkK, 0));
+        xr[i] = make_uint4(q[0], q[1], q[2], q[3]);
+      }
     }
   };
   auto store_x = [&](int buf) {

@@ -289,7 +289,7 @@ SplitShape split_shape(int64_t M, int64_t N, int64_t K) {
   s.MB = int((M + 32 * s.MS - 1) / (32 * s.MS));
   const int64_t tiles = (N + kTileN - 1) / kTileN;
   s.G = int((tiles + kSplitWaves - 1) / kSplitWaves);
-  const int64_t kc = K / kChunkK;
+  const int64_t kc = (K + kChunkK - 1) / kChunkK;
   const int64_t per_range = int64_t(kSplitWaves) * s.G * std::max(s.MB, 1);  // waves per K range
   int64_t S = (kSplitTargetWaves + per_range - 1) / per_range;
   S = std::min<int64_t>(S, std::max<int64_t>(1, kc / kSplitMinChunks));

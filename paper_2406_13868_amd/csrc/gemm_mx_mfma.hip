@@ -66,20 +66,28 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   // thread tid moves pieces p = tid & 7 of rows (tid >> 3) + 32 i; the
   // swizzle of those rows does not depend on i, so their LDS offsets are one
   // register plus i * 32 rows
-  const uint8_t* xsrc[kPerThread];
+  // the block's rows through a buffer resource: rows past M (whose outputs
+  // are never stored) and the bytes of a last partial chunk past the end of
+  // the tensor read 0
+  const __amdgpu_buffer_rsrc_t x_rsrc =
+      buffer_rsrc(a.Xq + size_t(m0) * a.K, uint32_t(min(a.M - m0, BM)) * uint32_t(a.K));
+  uint32_t xsrc[kPerThread];
   const uint32_t xdst0 = uint32_t((tid >> 3) * kChunkK + (((tid & 7) ^ lds_swizzle(tid >> 3)) << 4));
 #pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int rr = (tid >> 3) + i * 32;
-    // rows past M re-read row M-1 (their outputs are never stored)
-    xsrc[i] = a.Xq + size_t(min(m0 + rr, a.M - 1)) * a.K + (tid & 7) * 16;
-  }
+  for (int i = 0; i < kPerThread; ++i)
+    xsrc[i] = uint32_t((tid >> 3) + i * 32) * uint32_t(a.K) + uint32_t(tid & 7) * 16u;
+  auto ld_x = [&](uint32_t voff, int c) __attribute__((always_inline)) {
+    typedef unsigned int u4_ __attribute__((ext_vector_type(4)));
+    const u4_ q = __builtin_bit_cast(
+        u4_, __builtin_amdgcn_raw_buffer_load_b128(x_rsrc, voff, uint32_t(c) * kChunkK, 0));
+    return make_uint4(q[0], q[1], q[2], q[3]);
+  };
   // activations of one chunk on their way to LDS, as named registers (the
   // compiler keeps a local array of them in scratch across the products)
   static_assert(kPerThread == 1 || kPerThread == 2 || kPerThread == 4 || kPerThread == 8,
                 "1, 2, 4 or 8 pieces per thread");
   uint4 xr0, xr1, xr2, xr3, xr4, xr5, xr6, xr7;
-#define SDQ_XLD(i, c) *reinterpret_cast<const uint4*>(xsrc[i] + size_t(c) * kChunkK)
+#define SDQ_XLD(i, c) ld_x(xsrc[i], c)
 #define SDQ_LOAD_X(c)                                        \
   {                                                          \
     xr0 = SDQ_XLD(0, c);                                     \

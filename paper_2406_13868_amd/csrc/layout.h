@@ -91,7 +91,7 @@ struct Layout {
 inline Layout make_layout(bool mx, int64_t N, int64_t K, bool sc8 = false, int qv = 16, int sb = 2) {
   Layout L;
   L.n_tiles = (N + kTileN - 1) / kTileN;
-  L.n_chunks = K / kChunkK;
+  L.n_chunks = (K + kChunkK - 1) / kChunkK;  // a last, partial chunk holds zeros past K
   L.scale_bytes_per_tc = mx ? kMxScaleBytesPerTC : kTileN * (kChunkK / qv) * sb;
   L.words_off = 0;
   L.scales_off = L.n_tiles * L.n_chunks * kWordBytesPerTC;
@@ -113,7 +113,7 @@ struct DualLayout {
 inline DualLayout make_dual_layout(int64_t N, int64_t K) {
   DualLayout L;
   L.n_tiles = (N + kTileN - 1) / kTileN;
-  L.n_chunks = K / kChunkK;
+  L.n_chunks = (K + kChunkK - 1) / kChunkK;
   const int64_t tc = L.n_tiles * L.n_chunks;
   L.nib_off = 0;
   L.out_off = tc * kDualNibBytesPerTC;

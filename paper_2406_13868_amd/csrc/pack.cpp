@@ -20,6 +20,7 @@
 // contiguous row ranges, so the output does not depend on the thread count.
 #include <atomic>
 #include <cmath>
+#include <algorithm>
 #include <cstring>
 #include <thread>
 #include <vector>
@@ -704,16 +705,17 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
         const int64_t tc = t * dl.n_chunks + ch;
         const uint8_t* nib = blob + dl.nib_off + tc * kDualNibBytesPerTC;
         const uint16_t* hw = reinterpret_cast<const uint16_t*>(blob + dl.out_off + tc * kDualOutBytesPerTC);
-        for (int k = 0; k < kChunkK; ++k) {
+        const int kend = int(std::min<int64_t>(kChunkK, K - ch * kChunkK));  // a last chunk may be partial
+        for (int k = 0; k < kend; ++k) {
           const int64_t kk = n * K + ch * kChunkK + k;
           code_i_dense[kk] = uint8_t((nib[dual_nib_byte(k, r)] >> ((k & 1) * 4)) & 0xFu);
           code_o_dense[kk] = 0;
         }
-        for (int g = 0; g < 16; ++g) {
+        for (int g = 0; g < kend / 8; ++g) {
           const uint16_t v = hw[dual_out_halfword(g, r)];
           if (v >> 8) code_o_dense[n * K + ch * kChunkK + g * 8 + (v & 7)] = uint8_t(v >> 8);
         }
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < kend / 32; ++b)
           static_cast<uint8_t*>(scale_i)[n * (K / 32) + ch * 4 + b] =
               blob[dl.scale_off + tc * kDualScaleBytesPerTC + dual_scale_byte(b, r)];
       }
@@ -732,7 +734,8 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
       const uint32_t* words = reinterpret_cast<const uint32_t*>(blob + lay.words_off) +
                               (t * lay.n_chunks + ch) * kWordsPerTC;
       const uint8_t* sc = blob + lay.scales_off + (t * lay.n_chunks + ch) * lay.scale_bytes_per_tc;
-      for (int g = 0; g < 16; ++g) {
+      const int kend = int(std::min<int64_t>(kChunkK, K - ch * kChunkK));  // a last chunk may be partial
+      for (int g = 0; g < kend / 8; ++g) {
         const uint32_t word = words[c.mx ? mx_word_index(g, r) : int_word_index(g, r)];
         const int64_t kbase = n * K + ch * kChunkK + g * 8;
         for (int j = 0; j < 3; ++j) {
@@ -748,14 +751,14 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
         }
       }
       if (c.mx) {
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < kend / 32; ++b) {
           const int64_t bi = n * (K / 32) + ch * 4 + b;
           static_cast<uint8_t*>(scale_o)[bi] = sc[mx_scale_byte(b, r, 0)];
           static_cast<uint8_t*>(scale_i)[bi] = sc[mx_scale_byte(b, r, 1)];
         }
       } else {
         const int nb = kChunkK / c.qv;
-        for (int kb = 0; kb < nb; ++kb) {
+        for (int kb = 0; kb < kend / c.qv; ++kb) {
           if (c.scale_bytes() == 1) {
             static_cast<uint8_t*>(scale_i)[n * (K / c.qv) + ch * nb + kb] = sc[int_scale_off(kb, r, c.qv, 1)];
           } else {

@@ -72,7 +72,11 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
     if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
   }
   // upper bounds keep every per-block offset of the kernels in 32 bits
-  if (N <= 0 || K <= 0 || K % 128 != 0 || N > (int64_t(1) << 21) || K > (int64_t(1) << 22))
+  // K: whole 32-K blocks (the e8m0 block of the MX and dual families, two
+  // 16-K inlier blocks of the INT family) and whole Q-Vectors
+  const int qv_eff = c->qv_i ? c->qv_i : 16;
+  if (N <= 0 || K <= 0 || K % 32 != 0 || K % qv_eff != 0 || N > (int64_t(1) << 21) ||
+      K > (int64_t(1) << 22))
     return SDQ_ERR_SHAPE;
   if (N > (int64_t(1) << 31) || K > (int64_t(1) << 24)) return SDQ_ERR_SHAPE;
   if (out) {

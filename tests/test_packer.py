@@ -6,6 +6,7 @@ codes, scales) must agree exactly, and the kernel layout must decode back to
 the oracle's dense codes.
 """
 import ctypes as C
+import dataclasses
 import os
 import re
 
@@ -62,7 +63,7 @@ def _compare_logical(Lg, Lo, cfg_o):
 
 
 @pytest.mark.parametrize("c", CONFIGS, ids=_ids)
-@pytest.mark.parametrize("shape", [(256, 256), (50, 384), (33, 128)])
+@pytest.mark.parametrize("shape", [(256, 256), (50, 384), (33, 128), (40, 160), (33, 1056), (9, 32)])
 def test_logical_pack_matches_oracle(c, shape):
     cfg, cfg_o = _cfgs(*c)
     N, K = shape
@@ -73,9 +74,13 @@ def test_logical_pack_matches_oracle(c, shape):
 
 
 @pytest.mark.parametrize("c", CONFIGS, ids=_ids)
-def test_kernel_layout_roundtrip(c):
+@pytest.mark.parametrize("K", [512, 160, 288, 4128])
+def test_kernel_layout_roundtrip(c, K):
+    """Blob -> dense codes and scales, against the oracle's decisions: a ragged
+    last tile of 32 rows, and K that leaves a last partial 128-K chunk (which
+    the blob pads with zero codes and scales)."""
     cfg, cfg_o = _cfgs(*c)
-    N, K = 70, 512  # ragged last tile of 32 rows
+    N = 70  # ragged last tile of 32 rows
     W = synth.make_w(5, 0, N, K)
     blob = sdq.pack(W, cfg)
     U = sdq.unpack_dense(blob, cfg, N, K)
@@ -174,7 +179,12 @@ def test_error_paths():
     L = _lib.lib()
     n = C.c_size_t()
     assert L.sdq_pack_size(None, 32, 128, C.byref(n)) == -1
-    assert L.sdq_pack_size(C.byref(cfg), 32, 100, C.byref(n)) == -2       # K % 128
+    assert L.sdq_pack_size(C.byref(cfg), 32, 100, C.byref(n)) == -2       # K % 32
+    assert L.sdq_pack_size(C.byref(cfg), 32, 48, C.byref(n)) == -2        # K % 32
+    assert L.sdq_pack_size(C.byref(cfg), 32, 160, C.byref(n)) == 0        # a partial last 128-K chunk
+    assert n.value == sdq.pack_size(sdq.Config.int_family(), 32, 256)     # padded to whole chunks
+    cq = dataclasses.replace(sdq.Config.int_family(), qv_i=64)
+    assert L.sdq_pack_size(C.byref(cq.c()), 32, 160, C.byref(n)) == -2   # K % qv
     assert L.sdq_pack_size(C.byref(cfg), 0, 128, C.byref(n)) == -2
     bad = sdq.Config("int", 1, 8, "e2m1", 3).c()
     assert L.sdq_pack_size(C.byref(bad), 32, 128, C.byref(n)) == -3
@@ -212,7 +222,7 @@ def test_error_paths():
     dual = sdq.Config.dual_family().c()
     p16 = C.c_void_p(16)
     assert L.sdq_gemm_dual(C.byref(dual), p16, p16, p16, p16, 1, p16, 32, 128, C.c_void_p(18), None) == -2
-    assert L.sdq_gemm_dual(C.byref(dual), p16, p16, p16, p16, 1, p16, 32, 120, p16, None) == -2  # K % 128
+    assert L.sdq_gemm_dual(C.byref(dual), p16, p16, p16, p16, 1, p16, 32, 120, p16, None) == -2  # K % 32
     assert L.sdq_gemm_dual(C.byref(dual), None, p16, p16, p16, 1, p16, 32, 128, p16, None) == -1
     assert L.sdq_gemm_dual(C.byref(cfg), p16, p16, p16, p16, 1, p16, 32, 128, p16, None) == -3  # INT config
     for s in list(_lib.STATUS) + [123]:
@@ -235,6 +245,19 @@ def test_library_exports_every_header_symbol():
     L = _lib.lib()
     for name in declared:
         assert hasattr(L, name), name
+
+
+def test_library_shares_the_hip_runtime_torch_uses():
+    """Loaded before torch is imported, the library must still end up on the
+    same HIP runtime as torch: one libamdhip64 mapped in the process (two would
+    leave the library's launches without a device)."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, sys.argv[1]); from paper_2406_13868_amd import _lib; "
+            "_lib.lib(); import torch; r = _lib._hip_runtimes(); assert len(r) == 1, r; print('ok')")
+    p = subprocess.run([sys.executable, "-c", code, os.path.dirname(HERE)], capture_output=True, text=True,
+                       timeout=300)
+    assert p.returncode == 0 and p.stdout.strip() == "ok", p.stderr[-2000:]
 
 
 def test_gemm_path_choice():
@@ -424,8 +447,9 @@ def test_e4m3_scales_sizes_and_validation():
 @pytest.mark.parametrize("n_o,n_i,metric,decomp", [(1, 6, "magnitude", "same"), (1, 6, "product", "error"),
                                                    (1, 7, "magnitude", "same"), (1, 3, "product", "same"),
                                                    (0, 8, "magnitude", "same"), (0, 5, "magnitude", "same")])
-def test_dual_pack_matches_oracle(n_o, n_i, metric, decomp):
-    N, K = 40, 384
+@pytest.mark.parametrize("K", [384, 160])
+def test_dual_pack_matches_oracle(n_o, n_i, metric, decomp, K):
+    N = 40
     W = synth.make_w(2, 0, N, K)
     W[4, :] = 0.0
     W[6, :40] *= np.float32(1e-6)
