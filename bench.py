@@ -51,7 +51,9 @@ WORKLOADS = {
     "llama7b-mlp-prefill": (3, [0, 1, 2], 2048),
     "opt6.7b-ffn-decode": (4, [0, 1], 64),
     "tiny": (1, [0], 16),
-    # the paper's SDQ-W7:8-1:8int8-6:8fp4 (dual activations) on the LLaMA-7B block
+    # the paper's dual configurations (int8 outliers against int8 activations,
+    # fp4 inliers against MXFP4 activations) on the LLaMA-7B block; --fmt 0:
+    # 1:8 + 6:8 (7:8 in all), 1: 2:8 + 4:8 (6:8), 2: 1:8 + 7:8 (8:8)
     "llama7b-block-dual": (6, [0, 1, 2, 3, 4, 5, 6], 4096),
 }
 
@@ -80,7 +82,9 @@ def parse():
     p.add_argument("--layer", type=int, default=0, help="block-sweep layer index (0..6)")
     p.add_argument("--M", type=int, default=0,
                    help="token count: block sweep (default 1) or the dual block workload (default 4096)")
-    p.add_argument("--fmt", type=int, default=0, help="block-sweep format index")
+    p.add_argument("--fmt", type=int, default=0,
+                   help="format index of the block sweep, or of llama7b-block-dual (0: 1:8 int8 + 6:8 fp4, "
+                        "1: 2:8 int8 + 4:8 fp4, 2: 1:8 int8 + 7:8 fp4)")
     p.add_argument("--inlier-scale", default="", choices=["", "e4m3", "ue6m2"],
                    help="INT family: two-level e4m3 or ufp8-e6m2 inlier scales instead of the workload's "
                         "fp16 (the quantized scale formats of the paper's Section 6.4 study)")
@@ -239,10 +243,10 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
         wid, layers, M = WORKLOADS[workload]
         if M_arg and wid == 6:
             M = M_arg
-        fmt = synth.WORKLOADS[wid].formats[0]
+        fmt = synth.WORKLOADS[wid].formats[a.fmt if wid == 6 else 0]
         wl_name = synth.WORKLOADS[wid].name
         if wid == 6:
-            wl_name += f" M={M}"
+            wl_name += f" M={M} {fmt.n_o}:8 int8 + {fmt.n_i}:8 fp4"
     W_def = synth.WORKLOADS[wid]
     cfg = sdq.Config.of(fmt)
     sfmt, qv = scale
@@ -404,6 +408,8 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
     paths = [] if dual else sorted({sdq.gemm_path(cfg, M, L.N, L.K, workspace=True) for L in Ls})
     hbm_bound = cfg.family == "int" and M <= 64 or (cfg.family != "int" and M < 256)
     tkey = workload if workload != "sweep" else f"sweep_l{a.layer}_m{M}_f{a.fmt}"
+    if wid == 6 and a.fmt:
+        tkey += f"_f{a.fmt}"
     if sfmt or qv:
         tkey += f"_{sfmt or 'f16'}_qv{cfg.qv}_scales"
     gemm_s = gemm_us * 1e-6

@@ -70,12 +70,15 @@ typedef enum {
  *  SDQ_FAMILY_MX: activations fp8-e4m3 per token (fp32 scale); outliers
  *    fp8-e4m3 and inliers fp4-e2m1, each branch with one e8m0 (power of two)
  *    scale per 32 consecutive K positions of a row (OCP MX shared exponents).
- *  SDQ_FAMILY_DUAL (Section 5.1's worked configuration, e.g. 1:8 int8 +
- *    6:8 fp4): outliers int8 with one fp32 scale per row against int8
+ *  SDQ_FAMILY_DUAL (Section 5.1's worked configuration, and the dual
+ *    configurations whose perplexity Section 6.2 reports: 7:8 kept as 1:8
+ *    int8 + 6:8 fp4, 6:8 as 2:8 int8 + 4:8 fp4, 8:8 as 1:8 int8 + 7:8
+ *    fp4): outliers int8
+ *    with one fp32 scale per row against int8
  *    activations A_o (fp32 scale per token); inliers fp4-e2m1 with an e8m0
  *    scale per 32 K against fp4-e2m1 activations A_i (MXFP4: an e8m0 scale
  *    per 32 K per token).  fmt_o INT8, fmt_i E2M1, fmt_a INT8 (A_o; A_i is
- *    implied); n_o in {0, 1} with m_o = 8, any n_i with n_o + n_i <= 8.
+ *    implied); n_o in {0, 1, 2} with m_o = 8, any n_i with n_o + n_i <= 8.
  *    Quantize with sdq_quantize_act_dual and multiply with sdq_gemm_dual.
  */
 enum { SDQ_FAMILY_INT = 0, SDQ_FAMILY_MX = 1, SDQ_FAMILY_DUAL = 2 };
@@ -155,8 +158,9 @@ typedef struct {
 const char* sdq_status_string(sdq_status s);
 
 /* Validate a configuration for a W of shape [N, K].  K must be a positive
- * multiple of 32 (and of qv_i when that is 64) up to 2^22 and N positive up
- * to 2^21.  The kernels take K in chunks of 128: when K is not a multiple of
+ * multiple of 32 (and of qv_i when that is 64) up to 2^22 (2^19 with int8
+ * outliers, whose products with int8 activations are summed exactly in
+ * int32) and N positive up to 2^21.  The kernels take K in chunks of 128: when K is not a multiple of
  * 128 the blob pads the last chunk with zero codes and scales.  Returns SDQ_ERR_CONFIG / SDQ_ERR_SHAPE /
  * SDQ_ERR_UNSUPPORTED without touching anything else. */
 sdq_status sdq_check(const sdq_config* cfg, int64_t N, int64_t K);

@@ -11,7 +11,9 @@
 //     exactly the operand order, so the B fragment is one 16-byte load per
 //     lane and needs no expansion;
 //   * outliers: v_mfma_i32_32x32x32_i8, exact in int32.  Each lane expands
-//     its two groups' (position, code) half-words into 16 dense bytes.
+//     its two groups' (position, code) half-words into 16 dense bytes; with
+//     2:8 outliers the second plane's half-words scatter into the same bytes
+//     (the two positions of a group differ).
 //     Lane half h covers K [16h, 16h + 16) of the 32-K step for both
 //     operands (the K order inside the instruction is free as long as A and B
 //     agree).
@@ -83,12 +85,24 @@ __device__ __forceinline__ v4i outlier_bytes(uint32_t hw2) {
   return r;
 }
 
+// Outlier bytes per (tile, chunk) with NP half-word planes.
+template <int NP>
+constexpr uint32_t out_bytes_tc() { return uint32_t(NP) * kDualOutBytesPerTC; }
+
+// Dense int8 outlier bytes of two groups from NP planes of half-word pairs.
+template <int NP>
+__device__ __forceinline__ v4i outlier_bytes_np(const uint32_t (&hw)[NP]) {
+  v4i b = outlier_bytes(hw[0]);
+  if constexpr (NP == 2) b |= outlier_bytes(hw[1]);
+  return b;
+}
+
 // LDS rows of one 128-K chunk of activations, padded so that the 16-byte
 // fragment reads of 8 consecutive rows fall on distinct banks.
 constexpr int kRowO = kChunkK + 16;      // int8 codes of A_o: 144 bytes
 constexpr int kRowI = kChunkK / 2 + 16;  // fp4 codes of A_i: 80 bytes
 
-template <int MS>
+template <int MS, int NP>
 __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(DualArgs a) {
   constexpr int BM = 32 * MS;
   // one chunk of the workgroup's activations, two buffers
@@ -114,8 +128,8 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
   // the wave's tile: dense inlier nibbles, outlier half-words, inlier scales
   const __amdgpu_buffer_rsrc_t wn =
       buffer_rsrc(a.blob + size_t(tile) * KC * kDualNibBytesPerTC, uint32_t(KC) * kDualNibBytesPerTC);
-  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(tile) * KC * kDualOutBytesPerTC,
-                                                uint32_t(KC) * kDualOutBytesPerTC);
+  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(tile) * KC * out_bytes_tc<NP>(),
+                                                uint32_t(KC) * out_bytes_tc<NP>());
   const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.blob + a.scale_off + size_t(tile) * KC * kDualScaleBytesPerTC,
                                                 uint32_t(KC) * kDualScaleBytesPerTC);
 
@@ -159,7 +173,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
   struct BRegs {
     v4i bi[2];       // fp4 inlier fragments of the two 64-K steps
     int sb[2];       // their e8m0 scales (block 2s + h of row col)
-    uint32_t hw[4];  // outlier half-word pairs of the four 32-K steps
+    uint32_t hw[4][NP];  // outlier half-word pairs of the four 32-K steps, per plane
   };
   auto load_b = [&](int c, BRegs& st) __attribute__((always_inline)) {
     const uint32_t cs = uint32_t(c);
@@ -170,7 +184,10 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      st.hw[u] = __builtin_amdgcn_raw_buffer_load_b32(wo, uint32_t(u * 64 + lane) * 4u, cs * kDualOutBytesPerTC, 0);
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+        st.hw[u][p] = __builtin_amdgcn_raw_buffer_load_b32(
+            wo, uint32_t(p * kDualOutBytesPerTC) + uint32_t(u * 64 + lane) * 4u, cs * out_bytes_tc<NP>(), 0);
   };
 
   v16f acc[MS];
@@ -196,7 +213,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const v4i bo = outlier_bytes(st.hw[u]);
+      const v4i bo = outlier_bytes_np<NP>(st.hw[u]);
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms) {
         const v4i ao = *reinterpret_cast<const v4i*>(&xo_s[buf][(ms * 32 + col) * kRowO + u * 32 + h * 16]);
@@ -250,7 +267,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
 // accumulators are summed through LDS in a fixed-order tree.  This keeps
 // n_tiles * NW waves streaming weights where the tiled form above would run
 // only n_tiles / 4 workgroups.
-template <int NW>
+template <int NW, int NP>
 __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
   __shared__ float red[NW / 2][2][16][64];
 
@@ -268,15 +285,15 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
   const __amdgpu_buffer_rsrc_t ea = buffer_rsrc(a.Ea + size_t(m0) * (K / 32), rows * (K / 32));
   const __amdgpu_buffer_rsrc_t wn =
       buffer_rsrc(a.blob + size_t(tile) * KC * kDualNibBytesPerTC, uint32_t(KC) * kDualNibBytesPerTC);
-  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(tile) * KC * kDualOutBytesPerTC,
-                                                uint32_t(KC) * kDualOutBytesPerTC);
+  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(tile) * KC * out_bytes_tc<NP>(),
+                                                uint32_t(KC) * out_bytes_tc<NP>());
   const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.blob + a.scale_off + size_t(tile) * KC * kDualScaleBytesPerTC,
                                                 uint32_t(KC) * kDualScaleBytesPerTC);
 
   struct Stage {
     v4i bi[2];
     int sb[2];
-    uint32_t hw[4];
+    uint32_t hw[4][NP];
     v4i ai[2];
     uint32_t sa;  // the chunk's four e8m0 bytes of token row col
     v4i ao[4];
@@ -292,7 +309,10 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
     st.sa = ld_ea4(ea, uint32_t(col) * (K / 32), cs, K);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      st.hw[u] = __builtin_amdgcn_raw_buffer_load_b32(wo, uint32_t(u * 64 + lane) * 4u, cs * kDualOutBytesPerTC, 0);
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+        st.hw[u][p] = __builtin_amdgcn_raw_buffer_load_b32(
+            wo, uint32_t(p * kDualOutBytesPerTC) + uint32_t(u * 64 + lane) * 4u, cs * out_bytes_tc<NP>(), 0);
       st.ao[u] = ld16(xo, uint32_t(col) * K + uint32_t(u * 32 + h * 16), cs * kChunkK);
     }
   };
@@ -311,7 +331,8 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
       acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, b, acc, 4, 4, 0, sa, 0, st.sb[s]);
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acco = __builtin_amdgcn_mfma_i32_32x32x32_i8(st.ao[u], outlier_bytes(st.hw[u]), acco, 0, 0, 0);
+    for (int u = 0; u < 4; ++u)
+      acco = __builtin_amdgcn_mfma_i32_32x32x32_i8(st.ao[u], outlier_bytes_np<NP>(st.hw[u]), acco, 0, 0, 0);
   };
 
   // wave w takes chunks w, w + NW, ...; stage s0 its even-numbered ones and s1
@@ -361,26 +382,19 @@ __global__ __launch_bounds__(NW * 64, 2) void dual_splitk_kernel(DualArgs a) {
   for (int e = 0; e < 16; ++e) store_out(yr, a.N, n, 0, e, h, fmaf(rs.v[0][e], so * float(acco[e]), acc[e]));
 }
 
-template <int MS>
+template <int MS, int NP>
 hipError_t launch_ms(const DualArgs& a, hipStream_t st) {
   const dim3 grid(unsigned((a.n_tiles + kDWaves - 1) / kDWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
-  hipLaunchKernelGGL((dual_mfma_kernel<MS>), grid, dim3(kDThreads), 0, st, a);
+  hipLaunchKernelGGL((dual_mfma_kernel<MS, NP>), grid, dim3(kDThreads), 0, st, a);
   return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
-                            const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
-                            void* Y, hipStream_t st) {
-  const DualLayout L = make_dual_layout(N, K);
-  DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
-             L.out_off, L.scale_off, L.rows_off};
-  a.y_bf16 = c.y_bf16;
-  if (dual_decode_fits(M, N, K)) return launch_dual_decode(c, Xo, s_a, Xi, Ea, M, blob, N, K, Y, st);
-  if (M <= 32) {
+// The split-K or tiled form, by the number of tokens (NP outlier planes).
+template <int NP>
+hipError_t launch_np(const DualArgs& a, hipStream_t st) {
+  if (a.M <= 32) {
     const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 31) / 32));
-    hipLaunchKernelGGL((dual_splitk_kernel<4>), grid, dim3(4 * 64), 0, st, a);
+    hipLaunchKernelGGL((dual_splitk_kernel<4, NP>), grid, dim3(4 * 64), 0, st, a);
     return hipGetLastError();
   }
   // Tokens per workgroup: 32, 64 or 128 (one, two or four sub-tiles per
@@ -390,9 +404,23 @@ hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, c
   // with 32-token blocks against 31/32 us with 128; 11008x4096 at M = 512
   // takes 60 us with 64-token blocks against 73 us with 128.
   const int64_t groups = (a.n_tiles + kDWaves - 1) / kDWaves;
-  if (groups * ((M + 31) / 32) <= 256) return launch_ms<1>(a, st);
-  if (groups * ((M + 63) / 64) <= 1024 && groups * ((M + 127) / 128) < 512) return launch_ms<2>(a, st);
-  return launch_ms<4>(a, st);
+  const int64_t M = a.M;
+  if (groups * ((M + 31) / 32) <= 256) return launch_ms<1, NP>(a, st);
+  if (groups * ((M + 63) / 64) <= 1024 && groups * ((M + 127) / 128) < 512) return launch_ms<2, NP>(a, st);
+  return launch_ms<4, NP>(a, st);
+}
+
+}  // namespace
+
+hipError_t launch_dual_mfma(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
+                            const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
+                            void* Y, hipStream_t st) {
+  const DualLayout L = make_dual_layout(N, K, c.n_o);
+  DualArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
+             L.out_off, L.scale_off, L.rows_off};
+  a.y_bf16 = c.y_bf16;
+  if (dual_decode_fits(M, N, K)) return launch_dual_decode(c, Xo, s_a, Xi, Ea, M, blob, N, K, Y, st);
+  return L.out_planes == 2 ? launch_np<2>(a, st) : launch_np<1>(a, st);
 }
 
 }  // namespace sdq

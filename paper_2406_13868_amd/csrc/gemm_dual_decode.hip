@@ -16,7 +16,8 @@
 //     the fp32 accumulator;
 //   * outliers: each (position, code) half-word becomes a v_perm selector that
 //     picks the group's int8 activation, and v_dot4 multiplies it by the
-//     code into an exact int32 accumulator;
+//     code into an exact int32 accumulator (with 2:8 outliers, once for each
+//     of the two half-word planes);
 //   * the eight lanes of a row are summed by three fixed butterfly steps and
 //     the K parts in a fixed order through LDS, so the result does not depend
 //     on timing.
@@ -87,9 +88,10 @@ __device__ __forceinline__ int outlier_dot(uint32_t hw, uint32_t lo, uint32_t hi
   return __builtin_amdgcn_sdot4(int(a), int((hw >> 8) & 0xFFu), acc, false);
 }
 
-// MT tokens, S two-chunk steps per wave.
-template <int MT, int S>
+// MT tokens, S two-chunk steps per wave, NP outlier half-word planes.
+template <int MT, int S, int NP>
 __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(DualDecArgs a) {
+  constexpr uint32_t kOutTC = uint32_t(NP) * kDualOutBytesPerTC;  // outlier bytes per (tile, chunk)
   __shared__ float part[max_parts(MT, S)][MT][kSliceRowsD][2];
 
   const int lane = threadIdx.x & 63;
@@ -102,8 +104,7 @@ __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(Dual
 
   const __amdgpu_buffer_rsrc_t wn = buffer_rsrc(a.blob + size_t(t) * KC * kDualNibBytesPerTC,
                                                 uint32_t(KC) * kDualNibBytesPerTC);
-  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(t) * KC * kDualOutBytesPerTC,
-                                                uint32_t(KC) * kDualOutBytesPerTC);
+  const __amdgpu_buffer_rsrc_t wo = buffer_rsrc(a.blob + a.out_off + size_t(t) * KC * kOutTC, uint32_t(KC) * kOutTC);
   const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(a.blob + a.scale_off + size_t(t) * KC * kDualScaleBytesPerTC,
                                                 uint32_t(KC) * kDualScaleBytesPerTC);
   const uint32_t rows = uint32_t(a.M);
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(Dual
 
   // ---- every load of the wave first: weights, then activations (chunks
   //      past K re-read the last one and are multiplied by zero activations)
-  struct W { v4i nib; uint32_t hw[2]; uint32_t e; };
+  struct W { v4i nib; uint32_t hw[NP][2]; uint32_t e; };
   struct X { v4i ai; v4i ao[2]; uint32_t e; };
   W w[S];
   X x[S][MT];
@@ -125,8 +126,10 @@ __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(Dual
     const uint32_t ce = uint32_t(min(c, KC - 1));
     w[d].nib = ld16(wn, ce * kDualNibBytesPerTC + uint32_t(b * 32 + r) * 16u);
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-      w[d].hw[hh] = ld32(wo, ce * kDualOutBytesPerTC + uint32_t((b * 2 + hh) * 32 + r) * 4u);
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+        w[d].hw[p][hh] = ld32(wo, ce * kOutTC + uint32_t(p * kDualOutBytesPerTC) + uint32_t((b * 2 + hh) * 32 + r) * 4u);
     w[d].e = ld8(ws, ce * kDualScaleBytesPerTC + uint32_t(b * 32 + r));
   }
 #pragma unroll
@@ -157,11 +160,13 @@ __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(Dual
       acc[m] += __builtin_ldexpf(p, int(xv.e + w[d].e) - 254);
       if (live[d]) {
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const uint32_t h2w = w[d].hw[hh];
-          acco[m] = outlier_dot(h2w & 0xFFFFu, uint32_t(xv.ao[hh][0]), uint32_t(xv.ao[hh][1]), acco[m]);
-          acco[m] = outlier_dot(h2w >> 16, uint32_t(xv.ao[hh][2]), uint32_t(xv.ao[hh][3]), acco[m]);
-        }
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t h2w = w[d].hw[p][hh];
+            acco[m] = outlier_dot(h2w & 0xFFFFu, uint32_t(xv.ao[hh][0]), uint32_t(xv.ao[hh][1]), acco[m]);
+            acco[m] = outlier_dot(h2w >> 16, uint32_t(xv.ao[hh][2]), uint32_t(xv.ao[hh][3]), acco[m]);
+          }
       }
     }
   }
@@ -198,8 +203,11 @@ __global__ __launch_bounds__(max_parts(MT, S) * 64) void dual_decode_kernel(Dual
 }
 
 template <int MT, int S>
-hipError_t launch_s(const DualDecArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((dual_decode_kernel<MT, S>), dim3(unsigned(a.n_slices)), dim3(unsigned(a.parts * 64)), 0, st, a);
+hipError_t launch_s(const DualDecArgs& a, int planes, hipStream_t st) {
+  if (planes == 2)
+    hipLaunchKernelGGL((dual_decode_kernel<MT, S, 2>), dim3(unsigned(a.n_slices)), dim3(unsigned(a.parts * 64)), 0, st, a);
+  else
+    hipLaunchKernelGGL((dual_decode_kernel<MT, S, 1>), dim3(unsigned(a.n_slices)), dim3(unsigned(a.parts * 64)), 0, st, a);
   return hipGetLastError();
 }
 
@@ -234,19 +242,20 @@ bool dual_decode_fits(int64_t M, int64_t N, int64_t K) {
 hipError_t launch_dual_decode(const Cfg& c, const uint8_t* Xo, const float* s_a, const uint8_t* Xi,
                               const uint8_t* Ea, int64_t M, const uint8_t* blob, int64_t N, int64_t K,
                               void* Y, hipStream_t st) {
-  const DualLayout L = make_dual_layout(N, K);
+  const DualLayout L = make_dual_layout(N, K, c.n_o);
   const int S = steps_for_dual(M, N, L.n_chunks);
+  const int np = L.out_planes;
   DualDecArgs a{Xo, s_a, Xi, Ea, blob, Y, int(M), int(N), int(K), int(L.n_chunks),
                 int(L.n_tiles * (kTileN / kSliceRowsD)), int((L.n_chunks + 2 * S - 1) / (2 * S)),
                 L.out_off, L.scale_off, L.rows_off, c.y_bf16};
   if (M == 1) {
-    if (S == 1) return launch_s<1, 1>(a, st);
-    if (S == 2) return launch_s<1, 2>(a, st);
-    if (S == 4) return launch_s<1, 4>(a, st);
-    return launch_s<1, 8>(a, st);
+    if (S == 1) return launch_s<1, 1>(a, np, st);
+    if (S == 2) return launch_s<1, 2>(a, np, st);
+    if (S == 4) return launch_s<1, 4>(a, np, st);
+    return launch_s<1, 8>(a, np, st);
   }
-  if (S == 1) return launch_s<2, 1>(a, st);
-  return launch_s<2, 2>(a, st);
+  if (S == 1) return launch_s<2, 1>(a, np, st);
+  return launch_s<2, 2>(a, np, st);
 }
 
 }  // namespace sdq

@@ -58,10 +58,12 @@
 //              piece ((s*2 + h)*32 + r) of 16 bytes holds K 64s + 32h .. +32
 //              of row r (64-K step s), byte j = K 2j (low nibble), 2j + 1
 //              (high nibble): the fp4 operand of lane h*32 + r as loaded
-//   section B  outlier half-words         1024 B  [t][c]
-//              group g = 4u + 2h + i (32-K step u, half h, i in {0,1}) of
-//              row r at half-word ((u*2 + h)*32 + r)*2 + i: bits 0-2 the
-//              position, bits 8-15 the int8 code (0: no outlier)
+//   section B  outlier half-words, P = max(1, n_o) planes of 1024 B
+//              [t][c][plane]: plane p holds each group's p-th outlier in
+//              ascending position order; group g = 4u + 2h + i (32-K step
+//              u, half h, i in {0,1}) of row r at half-word
+//              ((u*2 + h)*32 + r)*2 + i of the plane: bits 0-2 the position,
+//              bits 8-15 the int8 code (0: no such outlier)
 //   section C  inlier e8m0 scales          128 B  [t][c]
 //              32-K block b = 2s + h of row r at byte b*32 + r
 //   section D  outlier row scales, fp32 [t][32]
@@ -108,16 +110,20 @@ constexpr int kDualScaleBytesPerTC = kTileN * (kChunkK / 32);   // 128
 struct DualLayout {
   int64_t n_tiles = 0, n_chunks = 0;
   int64_t nib_off = 0, out_off = 0, scale_off = 0, rows_off = 0, total = 0;
+  int out_planes = 1;                          // outlier half-word planes: max(1, n_o)
+  int64_t out_bytes_per_tc = kDualOutBytesPerTC;  // out_planes * 1024
 };
 
-inline DualLayout make_dual_layout(int64_t N, int64_t K) {
+inline DualLayout make_dual_layout(int64_t N, int64_t K, int n_o) {
   DualLayout L;
   L.n_tiles = (N + kTileN - 1) / kTileN;
   L.n_chunks = (K + kChunkK - 1) / kChunkK;
+  L.out_planes = n_o > 1 ? n_o : 1;
+  L.out_bytes_per_tc = int64_t(L.out_planes) * kDualOutBytesPerTC;
   const int64_t tc = L.n_tiles * L.n_chunks;
   L.nib_off = 0;
   L.out_off = tc * kDualNibBytesPerTC;
-  L.scale_off = L.out_off + tc * kDualOutBytesPerTC;
+  L.scale_off = L.out_off + tc * L.out_bytes_per_tc;
   L.rows_off = L.scale_off + tc * kDualScaleBytesPerTC;
   L.total = L.rows_off + L.n_tiles * kTileN * 4;
   return L;

@@ -517,16 +517,21 @@ sdq_status pack_row(const Cfg& c, const float* w, const float* act_norm, int64_t
       const int64_t ch = k0 / kChunkK;
       const int64_t tc = t * out.dlay->n_chunks + ch;
       uint8_t* nib = out.blob + out.dlay->nib_off + tc * kDualNibBytesPerTC;
-      uint16_t* hw = reinterpret_cast<uint16_t*>(out.blob + out.dlay->out_off + tc * kDualOutBytesPerTC);
+      uint16_t* hw = reinterpret_cast<uint16_t*>(out.blob + out.dlay->out_off + tc * out.dlay->out_bytes_per_tc);
       for (int kk = 0; kk < 32; ++kk) {
         const int k = int(k0 % kChunkK) + kk;
         nib[dual_nib_byte(k, int(r))] |= uint8_t((icode[kk] & 0xFu) << ((k & 1) * 4));
       }
+      // the j-th outlier of a group (ascending position) in plane j; a plane
+      // without one keeps the zero half-word
       for (int gg = 0; gg < 4; ++gg) {
-        uint16_t v = 0;
+        int j = 0;
         for (int p = 0; p < 8; ++p)
-          if ((om[gg] >> p) & 1u) v = uint16_t(p | (ocode[8 * gg + p] << 8));
-        hw[dual_out_halfword(int((k0 % kChunkK) / 8) + gg, int(r))] = v;
+          if ((om[gg] >> p) & 1u) {
+            hw[j * (kDualOutBytesPerTC / 2) + dual_out_halfword(int((k0 % kChunkK) / 8) + gg, int(r))] =
+                uint16_t(p | (ocode[8 * gg + p] << 8));
+            ++j;
+          }
       }
     } else if (out.blob) {
       const int64_t ch = k0 / kChunkK;
@@ -619,7 +624,7 @@ extern "C" sdq_status sdq_pack_size(const sdq_config* cfg, int64_t N, int64_t K,
   const sdq_status s = check_config(cfg, N, K, &c);
   if (s != SDQ_OK) return s;
   if (!bytes) return SDQ_ERR_NULL;
-  *bytes = size_t(c.dual ? make_dual_layout(N, K).total : layout_for(c, N, K).total);
+  *bytes = size_t(c.dual ? make_dual_layout(N, K, c.n_o).total : layout_for(c, N, K).total);
   return SDQ_OK;
 }
 
@@ -655,7 +660,7 @@ extern "C" sdq_status sdq_pack(const sdq_config* cfg, const float* W, int64_t N,
   if (s != SDQ_OK) return s;
   if (!W || !packed) return SDQ_ERR_NULL;
   const Layout lay = layout_for(c, N, K);
-  const DualLayout dlay = make_dual_layout(N, K);
+  const DualLayout dlay = make_dual_layout(N, K, c.n_o);
   const size_t total = size_t(c.dual ? dlay.total : lay.total);
   if (bytes < total) return SDQ_ERR_BUFFER_TOO_SMALL;
   if ((s = check_act_norm(c, act_norm, K)) != SDQ_OK) return s;
@@ -696,7 +701,7 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
   const Layout lay = layout_for(c, N, K);
   const uint8_t* blob = static_cast<const uint8_t*>(packed);
   if (c.dual) {
-    const DualLayout dl = make_dual_layout(N, K);
+    const DualLayout dl = make_dual_layout(N, K, c.n_o);
     if (bytes < size_t(dl.total)) return SDQ_ERR_BUFFER_TOO_SMALL;
     for (int64_t n = 0; n < N; ++n) {
       const int64_t t = n / kTileN;
@@ -704,17 +709,18 @@ extern "C" sdq_status sdq_unpack_dense(const sdq_config* cfg, const void* packed
       for (int64_t ch = 0; ch < dl.n_chunks; ++ch) {
         const int64_t tc = t * dl.n_chunks + ch;
         const uint8_t* nib = blob + dl.nib_off + tc * kDualNibBytesPerTC;
-        const uint16_t* hw = reinterpret_cast<const uint16_t*>(blob + dl.out_off + tc * kDualOutBytesPerTC);
+        const uint16_t* hw = reinterpret_cast<const uint16_t*>(blob + dl.out_off + tc * dl.out_bytes_per_tc);
         const int kend = int(std::min<int64_t>(kChunkK, K - ch * kChunkK));  // a last chunk may be partial
         for (int k = 0; k < kend; ++k) {
           const int64_t kk = n * K + ch * kChunkK + k;
           code_i_dense[kk] = uint8_t((nib[dual_nib_byte(k, r)] >> ((k & 1) * 4)) & 0xFu);
           code_o_dense[kk] = 0;
         }
-        for (int g = 0; g < kend / 8; ++g) {
-          const uint16_t v = hw[dual_out_halfword(g, r)];
-          if (v >> 8) code_o_dense[n * K + ch * kChunkK + g * 8 + (v & 7)] = uint8_t(v >> 8);
-        }
+        for (int pl = 0; pl < dl.out_planes; ++pl)
+          for (int g = 0; g < kend / 8; ++g) {
+            const uint16_t v = hw[pl * (kDualOutBytesPerTC / 2) + dual_out_halfword(g, r)];
+            if (v >> 8) code_o_dense[n * K + ch * kChunkK + g * 8 + (v & 7)] = uint8_t(v >> 8);
+          }
         for (int b = 0; b < kend / 32; ++b)
           static_cast<uint8_t*>(scale_i)[n * (K / 32) + ch * 4 + b] =
               blob[dl.scale_off + tc * kDualScaleBytesPerTC + dual_scale_byte(b, r)];

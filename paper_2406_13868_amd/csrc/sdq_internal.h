@@ -65,8 +65,8 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
   // What the kernels implement.
   if (c->m_i != 8) return SDQ_ERR_UNSUPPORTED;
   if (dual) {
-    // dense fp4 inliers: any n_i with n_o + n_i <= 8; 1:8 outliers
-    if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8) || c->n_o + c->n_i > 8) return SDQ_ERR_UNSUPPORTED;
+    // dense fp4 inliers: any n_i with n_o + n_i <= 8; 1:8 or 2:8 outliers
+    if (c->n_o > 2 || (c->n_o > 0 && c->m_o != 8) || c->n_o + c->n_i > 8) return SDQ_ERR_UNSUPPORTED;
   } else {
     if (c->n_i > 3) return SDQ_ERR_UNSUPPORTED;
     if (c->n_o > 1 || (c->n_o == 1 && c->m_o != 8 && c->m_o != 16)) return SDQ_ERR_UNSUPPORTED;
@@ -79,6 +79,10 @@ inline sdq_status check_config(const sdq_config* c, int64_t N, int64_t K, Cfg* o
       K > (int64_t(1) << 22))
     return SDQ_ERR_SHAPE;
   if (N > (int64_t(1) << 31) || K > (int64_t(1) << 24)) return SDQ_ERR_SHAPE;
+  // int8 outliers against int8 activations accumulate in int32: K n_o / m_o
+  // products of at most 127^2 each stay below 2^31 for K <= 2^19 (n_o / m_o
+  // <= 1/4)
+  if (c->fmt_o == SDQ_FMT_INT8 && c->n_o > 0 && K > (int64_t(1) << 19)) return SDQ_ERR_SHAPE;
   if (out) {
     out->mx = mx;
     out->dual = dual;

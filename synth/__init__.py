@@ -136,8 +136,11 @@ WORKLOADS: Dict[int, Workload] = {
                 + tuple(mx_formats(1, mo, ni, 8) for mo in (8, 16) for ni in (2, 3)),
                 "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
     # The paper's headline SDQ-W7:8-1:8int8-6:8fp4 on the LLaMA-7B block shapes.
-    6: Workload(6, "llama7b block, dual 1:8 int8 + 6:8 fp4", LLAMA7B_LAYERS, (1, 16, 256, 4096),
-                (dual_formats(1, 6),), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
+    # the paper's three evaluated dual configurations: 7:8 = 1:8 int8 + 6:8
+    # fp4, 6:8 = 2:8 int8 + 4:8 fp4, 8:8 = 1:8 int8 + 7:8 fp4
+    6: Workload(6, "llama7b block, dual int8 outliers + fp4 inliers", LLAMA7B_LAYERS, (1, 16, 256, 4096),
+                (dual_formats(1, 6), dual_formats(2, 4), dual_formats(1, 7)), "bf16", 0.001, 0, 30.0, 0.02,
+                0.002, "t3"),
     # LLaMA-7B q, k and v projections stacked along N (one weight of 12288 rows,
     # the attention recipe), single-token decode: one launch for three layers.
     7: Workload(7, "llama7b qkv-concatenated decode M=1 12288x4096", (Layer("qkv_proj", 12288, 4096),),

@@ -84,7 +84,7 @@ def test_act_quant_dual_bit_exact(M, K, bf16):
     assert np.array_equal(Ea.cpu().numpy(), Ea_r)
 
 
-@pytest.mark.parametrize("n_o,n_i", [(1, 6), (1, 3), (0, 7), (1, 7)])
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (1, 3), (0, 7), (1, 7), (2, 4), (2, 6), (2, 1)])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 256), (5, 96, 384), (33, 160, 256), (64, 256, 2048),
                                    (100, 70, 256), (130, 129, 384), (300, 544, 128)])
 def test_gemm_dual_matches_oracle(n_o, n_i, M, N, K):
@@ -96,13 +96,15 @@ def test_gemm_dual_matches_oracle(n_o, n_i, M, N, K):
     _check(Y, X, W, cfg_o, f"dual {n_o}:8+{n_i}:8 M={M} N={N} K={K}")
 
 
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (2, 4)])
 @pytest.mark.parametrize("M", [1, 2])
 @pytest.mark.parametrize("N,K", [(256, 128), (70, 256), (544, 1152), (96, 4096), (40, 11008), (96, 6144)])
-def test_gemm_dual_decode_matches_oracle(M, N, K):
+def test_gemm_dual_decode_matches_oracle(M, N, K, n_o, n_i):
     """One and two tokens (the vector decode kernel; two tokens at K = 11008
     exceed its register budget and take the matrix kernel): one chunk of K
-    (half the lanes idle), ragged N, parts of K from one to eight."""
-    cfg, cfg_o = _cfgs(1, 6)
+    (half the lanes idle), ragged N, parts of K from one to eight; 1:8 and
+    2:8 outliers."""
+    cfg, cfg_o = _cfgs(n_o, n_i)
     X = synth.make_x(2, M, K)
     W = synth.make_w(2, 0, N, K)
     say("gemm dual decode", M, N, K)
@@ -143,10 +145,11 @@ def _tokens_per_block(M, N):
 @pytest.mark.parametrize("M,N,K,block", [(100, 256, 512, 32), (300, 16384, 256, 64),
                                          (1100, 4096, 128, 64), (300, 32768, 128, 128),
                                          (2100, 4096, 128, 128)])
-def test_gemm_dual_every_token_block(M, N, K, block):
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (2, 4)])
+def test_gemm_dual_every_token_block(M, N, K, block, n_o, n_i):
     """Shapes that take each token block of the tiled kernel, with ragged M."""
     assert _tokens_per_block(M, N) == block
-    cfg, cfg_o = _cfgs(1, 6)
+    cfg, cfg_o = _cfgs(n_o, n_i)
     X = synth.make_x(2, M, K)
     W = synth.make_w(2, 0, N, K)
     say("gemm dual block", block, M, N, K)
@@ -165,11 +168,14 @@ def test_gemm_dual_llama_layer(M):
     _check(Y, X, W, cfg_o, f"dual llama M={M}")
 
 
-def test_gemm_dual_integer_grid_is_exact():
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (2, 4)])
+@pytest.mark.parametrize("M", [1, 2, 20, 64])
+def test_gemm_dual_integer_grid_is_exact(M, n_o, n_i):
     """Inputs on which every scale is 1 and every product and partial sum is
-    representable: the output must equal the oracle exactly."""
+    representable: the output must equal the oracle exactly, on every form
+    (decode, split-K, tiled) and with one or two outliers per group."""
     rng = np.random.default_rng(9)
-    M, N, K = 64, 64, 512
+    N, K = 64, 512
     # activations: amax 127 per token (s_a = 1 for A_o); every 32-K block's amax
     # 4 would give A_i codes of x itself, but a token has one amax: use blocks
     # whose values are e2m1 grid points times 2^E with E = floor(log2 amax) - 2
@@ -178,11 +184,14 @@ def test_gemm_dual_integer_grid_is_exact():
     X[:, 1:32] = rng.choice([-64.0, -32.0, 0.0, 32.0, 64.0, 96.0], (M, 31))  # block 0: E = 4, x/16 on the grid
     W = rng.choice([-6.0, -3.0, -1.0, 1.0, 2.0, 4.0, 6.0], (N, K)).astype(np.float32)
     W[:, ::8] = 127.0 * rng.choice([-1.0, 1.0], (N, K // 8))   # outliers: row amax 127, s_o = 1
+    if n_o == 2:
+        W[:, 5::8] = rng.choice([-100.0, -9.0, 8.0, 77.0], (N, K // 8))  # the second outlier of a group
     W[:, 1::32] = 6.0                                # every inlier block amax 6: E = 0
-    cfg, cfg_o = _cfgs(1, 6)
+    cfg, cfg_o = _cfgs(n_o, n_i)
     Yref, _, (s_ao, Ea), L = S.reference(X, W, cfg_o)
     assert (s_ao == 1).all() and (L["scale_o"] == 1).all()
-    say("gemm dual grid")
+    assert (L["mask_o"].reshape(N, -1, 8).sum(-1) == n_o).all()
+    say("gemm dual grid", M, n_o)
     Y, _ = _run(X, W, cfg)
     assert np.array_equal(Y.astype(np.float64), Yref)
 
@@ -241,17 +250,18 @@ def test_dual_hip_graph_replays_match_eager(M, y_dtype):
         torch.cuda.synchronize()
 
 
-def test_gemm_dual_decode_eight_steps_per_wave():
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (2, 4)])
+def test_gemm_dual_decode_eight_steps_per_wave(n_o, n_i):
     """A wide layer whose K parts take eight steps per wave at one token
     (8192 x 14464: 1024 slices x 113 chunks), checked on a seeded sample of
     rows (rows are independent, so the oracle packs only those)."""
     torch = torch_cuda()
-    cfg, cfg_o = _cfgs()
+    cfg, cfg_o = _cfgs(n_o, n_i)
     N, K = 8192, 14464
     W = synth.make_w(2, 3, N, K)
     X = synth.make_x(2, 1, K)
     blob = torch.from_numpy(sdq.pack(W, cfg)).cuda()
-    say("dual decode S=8", N, K)
+    say("dual decode S=8", N, K, n_o)
     Xo, s_a, Xi, Ea = sdq.quantize_act_dual(torch.from_numpy(X).cuda(), cfg)
     Y = sdq.gemm_dual(Xo, s_a, Xi, Ea, blob, N, K, cfg)
     torch.cuda.synchronize()

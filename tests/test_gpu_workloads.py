@@ -116,13 +116,14 @@ def test_block_sweep_layer(li):
         _check_sampled(W, Xs[M], Y, Xq, s_a, fmt, seed=li * 100 + M, what=f"{L.name} M={M} {fmt.label}")
 
 
-def test_dual_block_gate_prefill_every_output():
-    """The paper's own configuration (1:8 int8 outliers against int8
-    activations, 6:8 fp4 inliers against MXFP4 activations) on the LLaMA-7B
-    gate projection at 4096 tokens, every output."""
+@pytest.mark.parametrize("fi", [0, 1], ids=["1:8+6:8", "2:8+4:8"])
+def test_dual_block_gate_prefill_every_output(fi):
+    """The paper's own configurations (1:8 or 2:8 int8 outliers against int8
+    activations, 6:8 or 4:8 fp4 inliers against MXFP4 activations) on the
+    LLaMA-7B gate projection at 4096 tokens, every output."""
     torch = torch_cuda()
     w = synth.WORKLOADS[6]
-    fmt, L = w.formats[0], w.layers[4]
+    fmt, L = w.formats[fi], w.layers[4]
     cfg, cfg_o = sdq.Config.of(fmt), S.config_from(fmt)
     W = synth.make_w(6, 4, L.N, L.K)
     X = synth.make_x(6, 4096, L.K)

@@ -6,7 +6,8 @@ What pins it: hand-computed MXFP4 activation codes and exponents (the OCP MX
 rule, saturation, round-half-to-even, an all-zero block); A_o equal to the
 int8 per-token quantizer pinned elsewhere; the pure-Python loops over the
 stored slots of both SpMMs against the dense fp64 product; the branch
-structure of 7:8 = 1:8 + 6:8; a weight matrix with no outliers or no inliers
+structure of 7:8 = 1:8 + 6:8 and of 6:8 = 2:8 + 4:8 (the paper's other
+evaluated configuration); a weight matrix with no outliers or no inliers
 reducing the product to the other branch alone.
 """
 import numpy as np
@@ -57,9 +58,9 @@ def test_act_o_is_the_int8_quantizer():
     assert np.array_equal(Ao, Xq) and np.array_equal(s_ao, s_a)
 
 
-@pytest.mark.parametrize("n_i", [6, 3])
-def test_slot_loops_equal_dense_product(n_i):
-    cfg = S.Config("dual", 1, 8, "int8", n_i, 8, "e2m1", "int8+e2m1")
+@pytest.mark.parametrize("n_o,n_i", [(1, 6), (1, 3), (2, 4), (2, 6)])
+def test_slot_loops_equal_dense_product(n_o, n_i):
+    cfg = S.Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8+e2m1")
     W = synth.make_w(2, 0, 12, 128)
     X = synth.make_x(2, 3, 128)
     Ao, s_ao, Ai, Ea = S.quantize_act_dual(X)
@@ -82,6 +83,25 @@ def test_seven_of_eight_structure():
     # int8 outliers with one fp32 scale per row: the row's largest outlier is code 127
     codes = L["code_o_dense"].view(np.int8)
     assert (np.abs(codes).max(axis=1) == 127).all()
+
+
+def test_six_of_eight_structure():
+    """The paper's 6:8 configuration with two int8 outliers and four fp4
+    inliers per group of 8: exactly that many of each, disjoint, the outliers
+    the two largest magnitudes of the group and the pruned two the smallest."""
+    cfg = S.Config("dual", 2, 8, "int8", 4, 8, "e2m1", "int8+e2m1")
+    W = synth.make_w(2, 1, 16, 256)
+    L = S.pack_logical(W, cfg)
+    mo, mi = L["mask_o"].reshape(16, -1, 8), L["mask_i"].reshape(16, -1, 8)
+    assert (mo.sum(-1) == 2).all() and (mi.sum(-1) == 4).all()
+    assert not (mo & mi).any()
+    A = np.abs(W).reshape(16, -1, 8)
+    pruned = ~(mo | mi)
+    assert (np.where(mo, A, np.inf).min(-1) >= np.where(mi, A, -np.inf).max(-1)).all()
+    assert (np.where(mi, A, np.inf).min(-1) >= np.where(pruned, A, -np.inf).max(-1)).all()
+    codes = L["code_o_dense"].view(np.int8)
+    assert (np.abs(codes).max(axis=1) == 127).all()
+    assert (L["pos_o"][..., 0] < L["pos_o"][..., 1]).all()  # slots in ascending position
 
 
 def test_branches_alone():

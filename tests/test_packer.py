@@ -446,7 +446,9 @@ def test_e4m3_scales_sizes_and_validation():
 # ---- the dual family (Section 5.1's int8 A_o / fp4 A_i configuration)
 @pytest.mark.parametrize("n_o,n_i,metric,decomp", [(1, 6, "magnitude", "same"), (1, 6, "product", "error"),
                                                    (1, 7, "magnitude", "same"), (1, 3, "product", "same"),
-                                                   (0, 8, "magnitude", "same"), (0, 5, "magnitude", "same")])
+                                                   (0, 8, "magnitude", "same"), (0, 5, "magnitude", "same"),
+                                                   (2, 4, "magnitude", "same"), (2, 4, "product", "error"),
+                                                   (2, 6, "magnitude", "same"), (2, 1, "product", "same")])
 @pytest.mark.parametrize("K", [384, 160])
 def test_dual_pack_matches_oracle(n_o, n_i, metric, decomp, K):
     N = 40
@@ -483,6 +485,20 @@ def test_dual_sizes_and_validation():
     assert n.value == (N * (K // 8 * 11 + K // 8 * 42 + K // 32 * 8 + 32) + 7) // 8
     assert L.sdq_pack_size(C.byref(sdq.Config("dual", 1, 16, "int8", 6, 8, "e2m1", "int8").c()), 32, 128,
                            C.byref(n)) == -6      # 1:16 outliers not built for this family
+    # 2:8 outliers: a second plane of half-words (2 more bits per weight)
+    two = sdq.Config("dual", 2, 8, "int8", 4, 8, "e2m1", "int8")
+    assert L.sdq_pack_size(C.byref(two.c()), N, K, C.byref(n)) == 0
+    assert n.value == N * K // 2 + 2 * (N * K // 4) + N * K // 32 + N * 4
+    assert L.sdq_logical_bytes(C.byref(two.c()), N, K, C.byref(n)) == 0
+    assert n.value == (N * (K // 8 * 22 + K // 8 * 28 + K // 32 * 8 + 32) + 7) // 8
+    for bad in (sdq.Config("dual", 3, 8, "int8", 4, 8, "e2m1", "int8"),
+                sdq.Config("dual", 2, 8, "int8", 7, 8, "e2m1", "int8")):
+        assert L.sdq_pack_size(C.byref(bad.c()), 32, 128, C.byref(n)) in (-3, -6)
+    # int8 outliers sum exactly in int32 up to K = 2^19
+    for c8 in (two, dual, sdq.Config.int_family(1, 8, "int8", 3)):
+        assert L.sdq_check(C.byref(c8.c()), 32, 1 << 19) == 0
+        assert L.sdq_check(C.byref(c8.c()), 32, (1 << 19) + 32) == -2
+    assert L.sdq_check(C.byref(sdq.Config.int_family().c()), 32, (1 << 19) + 32) == 0  # e4m3 outliers
     assert L.sdq_pack_size(C.byref(sdq.Config("dual", 1, 8, "e4m3", 6, 8, "e2m1", "int8").c()), 32, 128,
                            C.byref(n)) == -3
     cfg = dual.c()
