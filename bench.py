@@ -308,16 +308,25 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
             quant(r, j)
     torch.cuda.synchronize()
 
-    def gemm_one(r, j, L):
+    def gemm_one(r, j, L, q=None):
+        q = j if q is None else q  # whose quantized activations
         if dual:
-            sdq.gemm_dual(Xq[r][j], sa[r][j], Xi[r][j], Ea[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j])
+            sdq.gemm_dual(Xq[r][q], sa[r][q], Xi[r][q], Ea[r][q], blobs[r][j], L.N, L.K, cfg, out=Y[r][j])
         else:
-            sdq.gemm(Xq[r][j], sa[r][j], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], workspace=ws)
+            sdq.gemm(Xq[r][q], sa[r][q], blobs[r][j], L.N, L.K, cfg, out=Y[r][j], workspace=ws)
+
+    # A layer that reads an earlier layer's input tensor (k and v read q's,
+    # up reads gate's) multiplies that layer's quantized activations: the
+    # tensor is quantized once per step, as the model computes it.
+    shared = {j: [jj for jj in range(j) if Ls[jj].name == L.input_of][0]
+              for j, L in enumerate(Ls) if L.input_of and any(P.name == L.input_of for P in Ls[:j])}
 
     def step(i):
         r = i % R
         for j, L in enumerate(Ls):
-            if dual:  # quantize into this copy's buffers, then multiply
+            if j in shared:
+                gemm_one(r, j, L, shared[j])
+            elif dual:  # quantize into this copy's buffers, then multiply
                 quant(r, j)
                 gemm_one(r, j, L)
             else:
@@ -482,6 +491,7 @@ def measure(a, torch, sdq, workload, M_arg, full, scale=("", 0)):
                    "formats": fmt.label,
                    "gemm_path": "dual mfma" if dual else ", ".join(
                        ["decode", "mfma", "dense (two passes)", "split-K (two passes)"][p - 1] for p in paths),
+                   "activations_quantized": [L.name for j, L in enumerate(Ls) if j not in shared],
                    "parallelism": "none (one GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,

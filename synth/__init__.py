@@ -88,6 +88,7 @@ class Layer:
     name: str
     N: int  # output features (rows of W)
     K: int  # input features (reduction)
+    input_of: str = ""  # an earlier layer whose input tensor this layer reads too
 
 
 @dataclasses.dataclass(frozen=True)
@@ -109,9 +110,9 @@ class Workload:
 
 
 LLAMA7B_LAYERS = (
-    Layer("q_proj", 4096, 4096), Layer("k_proj", 4096, 4096),
-    Layer("v_proj", 4096, 4096), Layer("o_proj", 4096, 4096),
-    Layer("gate_proj", 11008, 4096), Layer("up_proj", 11008, 4096),
+    Layer("q_proj", 4096, 4096), Layer("k_proj", 4096, 4096, "q_proj"),
+    Layer("v_proj", 4096, 4096, "q_proj"), Layer("o_proj", 4096, 4096),
+    Layer("gate_proj", 11008, 4096), Layer("up_proj", 11008, 4096, "gate_proj"),
     Layer("down_proj", 4096, 11008),
 )
 
@@ -124,7 +125,7 @@ WORKLOADS: Dict[int, Workload] = {
                 (1,), (INT_1x8_E4M3_3x8,), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
     # LLaMA-7B MLP prefill, 2048 tokens, MX formats.
     3: Workload(3, "llama7b mlp prefill M=2048", (Layer("gate_proj", 11008, 4096),
-                Layer("up_proj", 11008, 4096), Layer("down_proj", 4096, 11008)),
+                Layer("up_proj", 11008, 4096, "gate_proj"), Layer("down_proj", 4096, 11008)),
                 (2048,), (mx_formats(1, 8, 2, 8),), "bf16", 0.001, 0, 30.0, 0.02, 0.002, "t3"),
     # OPT-6.7B FFN, batched decode of 64 tokens, int8 outliers.
     4: Workload(4, "opt6.7b ffn batched decode M=64", (Layer("fc1", 16384, 4096),
