@@ -344,6 +344,28 @@ sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, 
                        const void* packed, int64_t N, int64_t K, void* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);
 
+/* The two passes of SDQ_PATH_DENSE as separate calls (the MX family with
+ * outliers; Section 5.1's product, with the weight unpack of Section 5 done
+ * ahead of it).  The first pass needs only the packed weights, so a caller
+ * can unpack the next layer's weights on another stream while this layer's
+ * product runs, and order each product after its own unpack with an event.
+ *   sdq_unpack_weights: writes the expanded B operands of the blob into
+ *     workspace (device, 16-byte aligned, ws_bytes at least
+ *     sdq_gemm_workspace_size(cfg, M, N, K, SDQ_PATH_DENSE) =
+ *     32 * ceil(N / 32) * K, else SDQ_ERR_BUFFER_TOO_SMALL).
+ *   sdq_gemm_unpacked: Y = the product, reading that workspace and the scale
+ *     words of the same blob (packed); arguments otherwise as sdq_gemm_ws.
+ *     The result equals sdq_gemm_ws with SDQ_PATH_DENSE bit for bit.
+ * The workspace must hold the unpack of this packed, N and K, and no other
+ * call may write it before sdq_gemm_unpacked has run (on its stream); a
+ * workspace that holds anything else gives wrong results, not an error.
+ * SDQ_ERR_UNSUPPORTED outside the MX family with outliers. */
+sdq_status sdq_unpack_weights(const sdq_config* cfg, const void* packed, int64_t N, int64_t K,
+                              void* workspace, size_t ws_bytes, void* stream);
+sdq_status sdq_gemm_unpacked(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                             const void* packed, int64_t N, int64_t K, const void* workspace,
+                             size_t ws_bytes, void* Y, void* stream);
+
 /* For callers that cannot allocate device memory: code under HIP graph
  * capture that may not call hipMalloc, tight serving loops, harnesses that
  * forbid allocation.  sdq_gemm_ws without a workspace argument: where the path

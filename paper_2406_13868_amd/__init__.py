@@ -29,7 +29,7 @@ from ._lib import (DTYPE_BF16, DTYPE_F32, FAMILY_DUAL, FAMILY_INT, FAMILY_MX, FM
 __all__ = ["Config", "pack", "pack_logical", "unpack_dense", "pack_size", "logical_bytes",
            "quantize_act", "gemm", "linear", "gemm_path", "SDQError", "PATH_AUTO", "PATH_DECODE",
            "PATH_MFMA", "PATH_DENSE", "PATH_SPLITK", "gemm_workspace_size", "check", "quantize_act_dual", "gemm_dual",
-           "gemm_static"]
+           "gemm_static", "unpack_weights", "gemm_unpacked"]
 
 _FMT = {"int8": FMT_INT8, "int4": FMT_INT4, "e4m3": FMT_E4M3, "e2m1": FMT_E2M1}
 
@@ -349,6 +349,44 @@ def gemm(Xq, s_a, packed, N: int, K: int, cfg: Config, out=None, path: int = PAT
                                       _dev(packed, "packed"), N, K, _dev(Y, "Y"),
                                       _dev(ws, "workspace"), ws.numel() * ws.element_size(),
                                       _stream(stream), path), "sdq_gemm_ws")
+    return Y
+
+
+def unpack_weights(packed, N: int, K: int, cfg: Config, workspace=None, stream=None):
+    """Pass 1 of the two-pass MX path on its own (sdq_unpack_weights): the blob's
+    expanded B operands in `workspace` (a uint8 CUDA tensor of at least
+    gemm_workspace_size(cfg, M, N, K, PATH_DENSE) bytes, or a fresh one),
+    which is returned for gemm_unpacked."""
+    import torch
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
+    nb = gemm_workspace_size(cfg, 0, N, K, PATH_DENSE)
+    ws = workspace if workspace is not None else torch.empty(nb, dtype=torch.uint8, device=packed.device)
+    _need_bytes(ws, nb, "workspace")
+    _same_device(packed, ws)
+    _lib.check(_lib.lib().sdq_unpack_weights(C.byref(cfg.c()), _dev(packed, "packed"), N, K,
+                                             _dev(ws, "workspace"), ws.numel() * ws.element_size(),
+                                             _stream(stream)), "sdq_unpack_weights")
+    return ws
+
+
+def gemm_unpacked(Xq, s_a, packed, N: int, K: int, cfg: Config, workspace, out=None, stream=None):
+    """Pass 2 of the two-pass MX path (sdq_gemm_unpacked): Y from the operands
+    unpack_weights wrote into `workspace` for the same packed, N and K; equal
+    to gemm(..., path=PATH_DENSE) bit for bit."""
+    import torch
+    if Xq.dim() != 2:
+        raise ValueError("Xq must be [M, K]")
+    M = Xq.shape[0]
+    _need(Xq, (M, K), torch.uint8, "Xq")
+    _need(s_a, (M,), torch.float32, "s_a")
+    _need_bytes(packed, pack_size(cfg, N, K), "packed")
+    _need_bytes(workspace, gemm_workspace_size(cfg, M, N, K, PATH_DENSE), "workspace")
+    Y = _out(out, M, N, cfg, Xq.device)
+    _same_device(Xq, s_a, packed, Y, workspace)
+    _lib.check(_lib.lib().sdq_gemm_unpacked(C.byref(cfg.c()), _dev(Xq, "Xq"), _dev(s_a, "s_a"), M,
+                                            _dev(packed, "packed"), N, K, _dev(workspace, "workspace"),
+                                            workspace.numel() * workspace.element_size(), _dev(Y, "Y"),
+                                            _stream(stream)), "sdq_gemm_unpacked")
     return Y
 
 

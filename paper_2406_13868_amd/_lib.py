@@ -28,6 +28,7 @@ EXPORTS = (
     "sdq_pack_logical", "sdq_unpack_dense", "sdq_quantize_act", "sdq_gemm", "sdq_gemm_ex",
     "sdq_gemm_path", "sdq_linear", "sdq_gemm_workspace_size", "sdq_gemm_ws",
     "sdq_quantize_act_dual", "sdq_gemm_dual", "sdq_gemm_static", "sdq_gemm_path_ws",
+    "sdq_unpack_weights", "sdq_gemm_unpacked",
 )
 STATIC_SCRATCH_BYTES = 48 * 1024 * 1024
 
@@ -114,6 +115,8 @@ def lib() -> C.CDLL:
             "sdq_quantize_act_dual": (C.c_int, [cfgp, vp, C.c_int32, i64, i64, vp, vp, vp, vp, vp]),
             "sdq_gemm_dual": (C.c_int, [cfgp, vp, vp, vp, vp, i64, vp, i64, i64, vp, vp]),
             "sdq_gemm_static": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, vp, C.c_int32]),
+            "sdq_unpack_weights": (C.c_int, [cfgp, vp, i64, i64, vp, C.c_size_t, vp]),
+            "sdq_gemm_unpacked": (C.c_int, [cfgp, vp, vp, i64, vp, i64, i64, vp, C.c_size_t, vp, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)

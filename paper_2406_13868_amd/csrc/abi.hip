@@ -224,6 +224,43 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 
+extern "C" sdq_status sdq_unpack_weights(const sdq_config* cfg, const void* packed, int64_t N, int64_t K,
+                                         void* workspace, size_t ws_bytes, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (!path_serves(c, SDQ_PATH_DENSE)) return SDQ_ERR_UNSUPPORTED;  // the MX family with outliers
+  if (!packed || !workspace) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(packed) % 16 || reinterpret_cast<uintptr_t>(workspace) % 16)
+    return SDQ_ERR_SHAPE;
+  if (ws_bytes < mx_dense_workspace_bytes(N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  drop_pending_error();
+  const hipError_t e = launch_mx_densify(c, static_cast<const uint8_t*>(packed), N, K, workspace,
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
+extern "C" sdq_status sdq_gemm_unpacked(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
+                                        const void* packed, int64_t N, int64_t K, const void* workspace,
+                                        size_t ws_bytes, void* Y, void* stream) {
+  Cfg c;
+  const sdq_status s = check_config(cfg, N, K, &c);
+  if (s != SDQ_OK) return s;
+  if (M < 0 || M > (int64_t(1) << 31) || M * N > (int64_t(1) << 40)) return SDQ_ERR_SHAPE;
+  if (!path_serves(c, SDQ_PATH_DENSE)) return SDQ_ERR_UNSUPPORTED;
+  if (M == 0) return SDQ_OK;
+  if (!Xq || !s_a || !packed || !workspace || !Y) return SDQ_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
+      reinterpret_cast<uintptr_t>(workspace) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
+    return SDQ_ERR_SHAPE;
+  if (ws_bytes < mx_dense_workspace_bytes(N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  drop_pending_error();
+  const hipError_t e = launch_mx_dense_pass(c, static_cast<const uint8_t*>(Xq), s_a, M,
+                                            static_cast<const uint8_t*>(packed), N, K, Y, workspace,
+                                            static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
+}
+
 extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, const float* s_a,
                                       int64_t M, const void* packed, int64_t N, int64_t K, void* Y,
                                       void* stream, int32_t path) {

@@ -358,12 +358,17 @@ __global__ __launch_bounds__(kDThreads, 2) void mx_dense2_kernel(DenseArgs a) {
 }
 
 template <int NI>
-hipError_t launch_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8_t* blob,
-                     const Layout& L, int64_t N, int64_t K, void* Y, bool y_bf16, uint4* frag,
-                     hipStream_t st) {
+hipError_t densify_ni(const uint8_t* blob, const Layout& L, uint4* frag, hipStream_t st) {
   const int n_units = int(L.n_tiles * L.n_chunks);
   hipLaunchKernelGGL((mx_densify_kernel<NI>), dim3(unsigned((n_units + 3) / 4)), dim3(256), 0, st,
                      blob, L.scales_off, n_units, frag);
+  return hipGetLastError();
+}
+
+template <int NI>
+hipError_t dense_ni(const uint8_t* Xq, const float* s_a, int64_t M, const uint8_t* blob,
+                    const Layout& L, int64_t N, int64_t K, void* Y, bool y_bf16, const uint4* frag,
+                    hipStream_t st) {
   DenseArgs a{Xq, s_a, blob, frag, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
               L.scales_off, int((M + kDBM - 1) / kDBM)};
   const int groups = int((L.n_tiles + kDTiles - 1) / kDTiles);
@@ -382,14 +387,31 @@ size_t mx_dense_workspace_bytes(int64_t N, int64_t K) {
   return size_t(L.n_tiles) * size_t(L.n_chunks) * kUnitPieces * sizeof(uint4);
 }
 
+hipError_t launch_mx_densify(const Cfg& c, const uint8_t* blob, int64_t N, int64_t K, void* workspace,
+                             hipStream_t st) {
+  const Layout L = make_layout(true, N, K);
+  uint4* frag = static_cast<uint4*>(workspace);
+  if (c.n_i == 1) return densify_ni<1>(blob, L, frag, st);
+  if (c.n_i == 2) return densify_ni<2>(blob, L, frag, st);
+  return densify_ni<3>(blob, L, frag, st);
+}
+
+hipError_t launch_mx_dense_pass(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                                const uint8_t* blob, int64_t N, int64_t K, void* Y, const void* workspace,
+                                hipStream_t st) {
+  const Layout L = make_layout(true, N, K);
+  const uint4* frag = static_cast<const uint4*>(workspace);
+  if (c.n_i == 1) return dense_ni<1>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+  if (c.n_i == 2) return dense_ni<2>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+  return dense_ni<3>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+}
+
 hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                            hipStream_t st) {
-  const Layout L = make_layout(true, N, K);
-  uint4* frag = static_cast<uint4*>(workspace);
-  if (c.n_i == 1) return launch_ni<1>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
-  if (c.n_i == 2) return launch_ni<2>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
-  return launch_ni<3>(Xq, s_a, M, blob, L, N, K, Y, c.y_bf16, frag, st);
+  const hipError_t e = launch_mx_densify(c, blob, N, K, workspace, st);
+  if (e != hipSuccess) return e;
+  return launch_mx_dense_pass(c, Xq, s_a, M, blob, N, K, Y, workspace, st);
 }
 
 }  // namespace sdq

@@ -95,6 +95,14 @@ size_t mx_dense_workspace_bytes(int64_t N, int64_t K);
 hipError_t launch_mx_dense(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                            hipStream_t st);
+// The two passes one at a time: pass 1 writes the expanded weights of the
+// blob into `workspace`; pass 2 multiplies them (with the blob's scale words)
+// whenever the caller orders it after pass 1.
+hipError_t launch_mx_densify(const Cfg& c, const uint8_t* blob, int64_t N, int64_t K, void* workspace,
+                             hipStream_t st);
+hipError_t launch_mx_dense_pass(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                                const uint8_t* blob, int64_t N, int64_t K, void* Y, const void* workspace,
+                                hipStream_t st);
 // The same two passes with the library's static scratch array as the
 // workspace (at most kStaticScratchBytes; the caller checks the size).
 constexpr size_t kStaticScratchBytes = size_t(48) << 20;

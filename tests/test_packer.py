@@ -260,6 +260,30 @@ def test_library_shares_the_hip_runtime_torch_uses():
     assert p.returncode == 0 and p.stdout.strip() == "ok", p.stderr[-2000:]
 
 
+def test_unpacked_entry_points_validate():
+    """sdq_unpack_weights / sdq_gemm_unpacked: argument errors before any GPU work."""
+    L = _lib.lib()
+    mx = sdq.Config.mx_family().c()
+    p16 = C.c_void_p(16)
+    N, K = 64, 256
+    need = 32 * 2 * K
+    assert L.sdq_unpack_weights(C.byref(sdq.Config.int_family().c()), p16, N, K, p16, need, None) == -6
+    assert L.sdq_unpack_weights(C.byref(sdq.Config.mx_family(n_o=0).c()), p16, N, K, p16, need, None) == -6
+    assert L.sdq_unpack_weights(C.byref(mx), None, N, K, p16, need, None) == -1
+    assert L.sdq_unpack_weights(C.byref(mx), p16, N, K, None, need, None) == -1
+    assert L.sdq_unpack_weights(C.byref(mx), p16, N, K, p16, need - 1, None) == -4
+    assert L.sdq_unpack_weights(C.byref(mx), C.c_void_p(8), N, K, p16, need, None) == -2
+    assert L.sdq_unpack_weights(C.byref(mx), p16, N, 120, p16, need, None) == -2
+    assert L.sdq_gemm_unpacked(C.byref(mx), p16, p16, 0, p16, N, K, p16, need, p16, None) == 0  # M = 0
+    assert L.sdq_gemm_unpacked(C.byref(mx), p16, p16, 4, p16, N, K, p16, need - 16, p16, None) == -4
+    assert L.sdq_gemm_unpacked(C.byref(mx), None, p16, 4, p16, N, K, p16, need, p16, None) == -1
+    assert L.sdq_gemm_unpacked(C.byref(mx), p16, p16, 4, p16, N, K, p16, need, C.c_void_p(18), None) == -2
+    assert L.sdq_gemm_unpacked(C.byref(sdq.Config.int_family().c()), p16, p16, 4, p16, N, K, p16, need, p16,
+                               None) == -6
+    n = C.c_size_t()
+    assert L.sdq_gemm_workspace_size(C.byref(mx), 4, N, K, sdq.PATH_DENSE, C.byref(n)) == 0 and n.value == need
+
+
 def test_gemm_path_choice():
     cfg = sdq.Config.int_family()
     assert sdq.gemm_path(cfg, 1, 4096, 4096) == sdq.PATH_DECODE
