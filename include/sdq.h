@@ -301,11 +301,13 @@ sdq_status sdq_gemm_path_ws(const sdq_config* cfg, int64_t M, int64_t N, int64_t
 
 /* Device workspace that sdq_gemm_ws needs (the product is sdq_gemm's,
  * Section 5.1).  Two paths take one.
- * SDQ_PATH_SPLITK, the INT family's matrix-core path for 9 to 256 tokens,
- * splits K into ranges of 128-K chunks handled by different workgroups, each
- * of which converts its activations to the matrix instruction's f16 once for
- * four row tiles; the partial sums of the ranges go to the workspace and a
- * second kernel adds them in range order.  SDQ_PATH_DENSE, the two-pass matrix-core path of the MX
+ * SDQ_PATH_SPLITK splits K into ranges of 128-K chunks handled by different
+ * workgroups; the partial sums of the ranges go to the workspace and a
+ * second kernel adds them in range order and scales by s_a.  In the INT
+ * family (9 to 256 tokens) each workgroup converts its activations to the
+ * matrix instruction's f16 once for four row tiles; in the MX family (from
+ * one token up to a few hundred) it is the one-pass scaled-MFMA kernel over
+ * a range of K, so that a small grid still fills the GPU.  SDQ_PATH_DENSE, the two-pass matrix-core path of the MX
  * family with outliers, first expands every packed weight once into the dense
  * fp8 B operand of the matrix instruction (both branches of a 32-K block
  * merged into one e4m3 value per position under the outlier's e8m0 scale,
@@ -314,16 +316,18 @@ sdq_status sdq_gemm_path_ws(const sdq_config* cfg, int64_t M, int64_t N, int64_t
  * 128 tokens (at 512 tokens and more the two passes take less time).
  *   path   SDQ_PATH_AUTO (what sdq_gemm_ws takes: SDQ_PATH_DENSE for the MX
  *          family with outliers when M >= 512 and ceil(N/256) * ceil(M/128)
- *          >= 160; SDQ_PATH_SPLITK for the INT family up to 256 tokens
- *          where sdq_gemm would take the matrix cores and K >= 8192, or
- *          M >= 64 and N >= 8192, or M = 256; else what sdq_gemm takes), or
- *          SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE / SDQ_PATH_SPLITK
+ *          >= 160; SDQ_PATH_SPLITK for the MX family when K >= 1024 and
+ *          ceil(N/128) * ceil(M/128) <= 128, and for the INT family up to
+ *          256 tokens where sdq_gemm would take the matrix cores and K >=
+ *          8192, or M >= 64 and N >= 8192, or M = 256; else what sdq_gemm
+ *          takes), or SDQ_PATH_DECODE / SDQ_PATH_MFMA / SDQ_PATH_DENSE /
+ *          SDQ_PATH_SPLITK
  *   bytes  32 * ceil(N / 32) * K for SDQ_PATH_DENSE; 4 * S * M * N for
- *          SDQ_PATH_SPLITK, with S (the number of K ranges, at most K / 512)
- *          chosen from M, N and K so that about 2048 waves run; 0 for the
- *          other paths
+ *          SDQ_PATH_SPLITK, with S (the number of K ranges, at most
+ *          ceil(K / 128) / 4) chosen from M, N and K so that about 2048
+ *          waves (INT) or 512 workgroups (MX) run; 0 for the other paths
  * Returns SDQ_ERR_UNSUPPORTED for SDQ_PATH_DENSE outside the MX family with
- * outliers and for SDQ_PATH_SPLITK outside the INT family. */
+ * outliers and for SDQ_PATH_SPLITK in the dual family. */
 sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, int64_t K,
                                    int32_t path, size_t* bytes);
 
@@ -337,9 +341,9 @@ sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, int64_t N, 
  * matrix instructions in the same order); the inliers of blocks that did not
  * merge are added after the last chunk instead of within their chunk, a
  * different fp32 rounding order.  SDQ_PATH_SPLITK adds the fp32 partial
- * sums s_o * acc_o + acc of its K ranges in range order before scaling by
- * s_a, another fixed rounding order than SDQ_PATH_MFMA's (its products are
- * as exact; integer-grid inputs give the same results). */
+ * sums of its K ranges (INT: s_o * acc_o + acc) in range order before
+ * scaling by s_a, another fixed rounding order than SDQ_PATH_MFMA's (its
+ * products are as exact; integer-grid inputs give the same results). */
 sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const float* s_a, int64_t M,
                        const void* packed, int64_t N, int64_t K, void* Y, void* workspace,
                        size_t ws_bytes, void* stream, int32_t path);

@@ -46,26 +46,38 @@ bool split_wins(int64_t M, int64_t N, int64_t K) {
   return K >= 8192 || (M >= 64 && N >= 8192) || M >= 256;
 }
 
+// The MX family's split-K path where the one-pass grid of 128 outputs x 128
+// tokens per workgroup would hold at most 128 workgroups (half the CUs):
+// measured on the LLaMA-7B shapes, 4096x4096 takes 9.1 / 14.3 / 20.8 us at M
+// = 1 / 64 / 128 against 25.9 / 29.8 / 26.5 in one pass, and 28.6 against 30.8
+// at 512; 4096x11008 14.1 / 19.7 / 34.8 / 51.4 at M = 1 / 64 / 256 / 512
+// against 63.1 / 72.4 / 64.7 / 73.9.  It loses on fuller grids (11008x4096
+// at M = 256: 40.5 against 39.6; 4096x4096 at M = 768: 41.5 against 38.6),
+// and needs K for at least two ranges.
+bool mx_split_wins(int64_t M, int64_t N, int64_t K) {
+  return K >= 2 * kMxSplitMinChunks * kChunkK && (N + 127) / 128 * ((M + 127) / 128) <= 128;
+}
+
 int32_t auto_path_ws(const Cfg& c, int64_t M, int64_t N, int64_t K) {
   const int64_t wgs = (N + 255) / 256 * ((M + 127) / 128);
   if (c.mx && c.n_o > 0 && M >= kDenseMinM && wgs >= 160) return SDQ_PATH_DENSE;
+  if (c.mx && mx_split_wins(M, N, K)) return SDQ_PATH_SPLITK;
   const int32_t p = auto_path(c, M, K);
   if (!c.mx && p == SDQ_PATH_MFMA && split_wins(M, N, K)) return SDQ_PATH_SPLITK;
   return p;
 }
 
 // Workspace bytes of a path that takes one (0 for the others).
-size_t path_workspace_bytes(int32_t path, int64_t M, int64_t N, int64_t K) {
+size_t path_workspace_bytes(const Cfg& c, int32_t path, int64_t M, int64_t N, int64_t K) {
   if (path == SDQ_PATH_DENSE) return mx_dense_workspace_bytes(N, K);
-  if (path == SDQ_PATH_SPLITK) return int_split_workspace_bytes(M, N, K);
+  if (path == SDQ_PATH_SPLITK) return c.mx ? mx_split_workspace_bytes(M, N, K) : int_split_workspace_bytes(M, N, K);
   return 0;
 }
 
 // Whether a workspace path serves the configuration.
 bool path_serves(const Cfg& c, int32_t path) {
   if (path == SDQ_PATH_DENSE) return c.mx && c.n_o > 0;
-  if (path == SDQ_PATH_SPLITK) return !c.mx;
-  return true;
+  return true;  // SDQ_PATH_SPLITK: the INT and the MX family
 }
 
 // The launchers report a failed launch through hipGetLastError, which also
@@ -189,7 +201,7 @@ extern "C" sdq_status sdq_gemm_workspace_size(const sdq_config* cfg, int64_t M, 
   if (c.dual) return SDQ_ERR_UNSUPPORTED;
   if (path == SDQ_PATH_AUTO) path = auto_path_ws(c, M, N, K);
   if (!path_serves(c, path)) return SDQ_ERR_UNSUPPORTED;
-  *bytes = path_workspace_bytes(path, M, N, K);
+  *bytes = path_workspace_bytes(c, path, M, N, K);
   return SDQ_OK;
 }
 
@@ -211,16 +223,17 @@ extern "C" sdq_status sdq_gemm_ws(const sdq_config* cfg, const void* Xq, const f
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
       reinterpret_cast<uintptr_t>(workspace) % 16 || reinterpret_cast<uintptr_t>(Y) % 4)
     return SDQ_ERR_SHAPE;
-  if (ws_bytes < path_workspace_bytes(path, M, N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
+  if (ws_bytes < path_workspace_bytes(c, path, M, N, K)) return SDQ_ERR_BUFFER_TOO_SMALL;
   const auto* xq = static_cast<const uint8_t*>(Xq);
   const auto* blob = static_cast<const uint8_t*>(packed);
   const hipStream_t st = static_cast<hipStream_t>(stream);
   drop_pending_error();
   const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense(c, xq, s_a, M, blob, N, K, Y, workspace, st)
-                                              : launch_int_split(c, xq, s_a, M, blob, N, K, Y, workspace, st);
+                       : c.mx                  ? launch_mx_split(c, xq, s_a, M, blob, N, K, Y, workspace, st)
+                                               : launch_int_split(c, xq, s_a, M, blob, N, K, Y, workspace, st);
   if (log_enabled())
     std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s\n", (long long)M, (long long)N,
-                 (long long)K, path == SDQ_PATH_DENSE ? "mx_dense (two passes)" : "int_split (K ranges)");
+                 (long long)K, path == SDQ_PATH_DENSE ? "mx_dense (two passes)" : c.mx ? "mx_split (K ranges)" : "int_split (K ranges)");
   return e == hipSuccess ? SDQ_OK : SDQ_ERR_HIP;
 }
 
@@ -274,7 +287,7 @@ extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, con
   if (path != SDQ_PATH_DENSE && path != SDQ_PATH_SPLITK)
     return sdq_gemm_ex(cfg, Xq, s_a, M, packed, N, K, Y, stream, path);
   if (!path_serves(c, path)) return SDQ_ERR_UNSUPPORTED;
-  if (path_workspace_bytes(path, M, N, K) > kStaticScratchBytes) return SDQ_ERR_TOO_LARGE;
+  if (path_workspace_bytes(c, path, M, N, K) > kStaticScratchBytes) return SDQ_ERR_TOO_LARGE;
   if (M == 0) return SDQ_OK;
   if (!Xq || !s_a || !packed || !Y) return SDQ_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(Xq) % 16 || reinterpret_cast<uintptr_t>(packed) % 16 ||
@@ -285,7 +298,7 @@ extern "C" sdq_status sdq_gemm_static(const sdq_config* cfg, const void* Xq, con
   const hipStream_t st = static_cast<hipStream_t>(stream);
   drop_pending_error();
   const hipError_t e = path == SDQ_PATH_DENSE ? launch_mx_dense_static(c, xq, s_a, M, blob, N, K, Y, st)
-                                              : int_split_static(c, xq, s_a, M, blob, N, K, Y, st);
+                                              : split_static(c, xq, s_a, M, blob, N, K, Y, st);
   if (log_enabled())
     std::fprintf(stderr, "[sdq] gemm M=%lld N=%lld K=%lld -> %s, static scratch\n", (long long)M,
                  (long long)N, (long long)K, path == SDQ_PATH_DENSE ? "mx_dense (two passes)" : "int_split");

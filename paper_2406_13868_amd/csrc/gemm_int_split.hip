@@ -243,7 +243,7 @@ __global__ __launch_bounds__(kSplitThreads) void int_split_kernel(SplitArgs a) {
 // partial sums of up to 16 ranges are requested together before any is
 // added (one memory round trip instead of one per range).
 template <bool V4>
-__global__ __launch_bounds__(256) void int_split_reduce(const float* part, const float* s_a, void* Y, int M,
+__global__ __launch_bounds__(256) void split_reduce(const float* part, const float* s_a, void* Y, int M,
                                                         int N, int S, bool y_bf16) {
   const size_t MN = size_t(M) * size_t(N);
   const size_t i0 = (size_t(blockIdx.x) * 256 + threadIdx.x) * 4;
@@ -338,12 +338,17 @@ hipError_t launch_int_split(const Cfg& c, const uint8_t* Xq, const float* s_a, i
               c.qv == 64 ? 2 : c.qv == 32 ? 1 : 0, int((kChunkK / c.qv) * c.scale_bytes())};
   const hipError_t e = sh.MS == 1 ? launch_split_ms<1>(c, a, st) : launch_split_ms<2>(c, a, st);
   if (e != hipSuccess) return e;
+  return launch_split_reduce(a.part, s_a, Y, M, N, sh.S, c.y_bf16, st);
+}
+
+hipError_t launch_split_reduce(const float* part, const float* s_a, void* Y, int64_t M, int64_t N, int S,
+                               bool y_bf16, hipStream_t st) {
   const size_t MN = size_t(M) * size_t(N);
   const dim3 grid(unsigned((MN + 1023) / 1024)), block(256);
   if (N % 4 == 0)
-    hipLaunchKernelGGL(int_split_reduce<true>, grid, block, 0, st, a.part, s_a, Y, int(M), int(N), sh.S, c.y_bf16);
+    hipLaunchKernelGGL(split_reduce<true>, grid, block, 0, st, part, s_a, Y, int(M), int(N), S, y_bf16);
   else
-    hipLaunchKernelGGL(int_split_reduce<false>, grid, block, 0, st, a.part, s_a, Y, int(M), int(N), sh.S, c.y_bf16);
+    hipLaunchKernelGGL(split_reduce<false>, grid, block, 0, st, part, s_a, Y, int(M), int(N), S, y_bf16);
   return hipGetLastError();
 }
 

@@ -452,13 +452,15 @@ hipError_t static_scratch(void** out) {
 
 }  // namespace
 
-hipError_t int_split_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                            const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {
-  if (int_split_workspace_bytes(M, N, K) > kStaticScratchBytes) return hipErrorInvalidValue;
+hipError_t split_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                        const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {
+  const size_t need = c.mx ? mx_split_workspace_bytes(M, N, K) : int_split_workspace_bytes(M, N, K);
+  if (need > kStaticScratchBytes) return hipErrorInvalidValue;
   void* ws = nullptr;
   const hipError_t e = static_scratch(&ws);
   if (e != hipSuccess) return e;
-  return launch_int_split(c, Xq, s_a, M, blob, N, K, Y, ws, st);
+  return c.mx ? launch_mx_split(c, Xq, s_a, M, blob, N, K, Y, ws, st)
+              : launch_int_split(c, Xq, s_a, M, blob, N, K, Y, ws, st);
 }
 
 hipError_t launch_mx_dense_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,

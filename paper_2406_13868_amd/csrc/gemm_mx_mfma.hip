@@ -18,7 +18,15 @@
 // buffered, XOR-swizzled) and shared by the 4 waves; weights stream from HBM
 // into registers and are expanded there into dense fp8 / fp4 fragments.
 // Weights and activations are requested two chunks before they are used.
+//
+// Split-K form (a caller-owned workspace): the grid also runs over ranges of
+// the 128-K chunks; each workgroup writes the raw fp32 sums of its range to
+// the workspace, and a second kernel adds the ranges in order and scales by
+// s_a.  For tens to hundreds of tokens, where the one-pass grid alone leaves
+// CUs idle or runs one workgroup per CU through every chunk.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "kernels.h"
 #include "mx_frag.h"
@@ -39,8 +47,11 @@ struct MxArgs {
   void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
-  int m_blocks;  // workgroups along M; the grid is 1-D over (tile group, M block)
+  int m_blocks;  // workgroups along M; the grid is 1-D over (K range, tile group, M block)
   bool y_bf16 = false;  // Y as bf16
+  int k_ranges = 1;     // ranges of chunks the grid splits K into
+  int kc_range = 0;     // chunks per range (the last may hold fewer)
+  float* part = nullptr;  // split-K: [k_ranges][M][N] raw sums; null: Y = s_a * acc
 };
 
 template <int MS, int NI, bool HAS_O>
@@ -54,11 +65,14 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: chunk offsets stay scalar
   const int col = lane & 31, h = lane >> 5;
   int group, mblock;
-  tile_work(blockIdx.x, gridDim.x / a.m_blocks, a.m_blocks, group, mblock);
+  const int items = int(gridDim.x) / a.k_ranges;  // (tile group, M block) items per K range
+  const int range = int(blockIdx.x) / items;
+  tile_work(int(blockIdx.x) - range * items, items / a.m_blocks, a.m_blocks, group, mblock);
   const int m0 = mblock * BM;
   const int tile = min(group * kWaves + wave, a.n_tiles - 1);  // spare waves recompute the last tile
   const bool tile_ok = group * kWaves + wave < a.n_tiles;
   const int KC = a.n_chunks;
+  const int cb = range * a.kc_range, ce = min(KC, cb + a.kc_range);  // this workgroup's chunks
 
   // ---- activation staging: every thread moves kPerThread 16-byte pieces
   constexpr int kPerThread = BM * 8 / kThreads;
@@ -205,16 +219,16 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   //      past the last chunk re-read it (in bounds, never used), so that no
   //      load is conditional.  A register set is refilled right after its
   //      last expansion, never copied (a copy would wait for the load).
-  const int last = KC - 1;
-  WRegs wA, wB;     // weights of the even / odd chunks
-  SDQ_LOAD_X(0)
-  load_w(0, wA);
-  load_w(min(1, last), wB);
+  const int last = ce - 1;
+  WRegs wA, wB;     // weights of the even / odd chunks (counted from cb)
+  SDQ_LOAD_X(cb)
+  load_w(cb, wA);
+  load_w(min(cb + 1, last), wB);
   SDQ_STORE_X(0)
-  SDQ_LOAD_X(min(1, last))
+  SDQ_LOAD_X(min(cb + 1, last))
   BFrag fE = expand(wA, 0), fO;  // first step of the next even / odd chunk
   __syncthreads();
-  for (int c = 0; c < KC; c += 2) {
+  for (int c = cb; c < ce; c += 2) {
     {
       const BFrag f1 = expand(wA, 1);
       load_w(min(c + 2, last), wA);
@@ -225,7 +239,7 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
       SDQ_LOAD_X(min(c + 2, last))
       __syncthreads();
     }
-    if (c + 1 >= KC) break;
+    if (c + 1 >= ce) break;
     {
       const BFrag f1 = expand(wB, 1);
       load_w(min(c + 3, last), wB);
@@ -245,6 +259,14 @@ __global__ __launch_bounds__(kThreads, MS >= 8 ? 1 : 2) void mx_mfma_kernel(MxAr
   if (!tile_ok) return;
   const int n = tile * kTileN + col;
   if (n >= a.N) return;
+  if (a.part) {  // split-K: this range's raw sums
+    const OutRows pr = out_rows(a.part + size_t(range) * size_t(a.M) * size_t(a.N), false, a.M, a.N, m0, BM);
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) store_out(pr, a.N, n, ms, e, h, acc[ms][e]);
+    return;
+  }
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
   const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, BM);
 #pragma unroll
@@ -257,7 +279,7 @@ template <int MS, int NI>
 hipError_t launch_ms_ni(const Cfg& c, const MxArgs& a, hipStream_t st) {
   MxArgs b = a;
   b.m_blocks = int((a.M + 32 * MS - 1) / (32 * MS));
-  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves * b.m_blocks));
+  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves * b.m_blocks * b.k_ranges));
   const dim3 block(kThreads);
   if (c.n_o)
     hipLaunchKernelGGL((mx_mfma_kernel<MS, NI, true>), grid, block, 0, st, b);
@@ -280,6 +302,7 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
   const Layout L = make_layout(true, N, K);
   MxArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles), L.scales_off};
   a.y_bf16 = c.y_bf16;
+  a.kc_range = int(L.n_chunks);
   if (M <= 32) return launch_ms<1>(c, a, st);
   if (M <= 64) return launch_ms<2>(c, a, st);
   // More tokens: the largest token block that still gives a full round of
@@ -290,6 +313,47 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
   if (groups * ((M + 31) / 32) <= kCUs) return launch_ms<1>(c, a, st);
   if (groups * ((M + 63) / 64) <= kCUs) return launch_ms<2>(c, a, st);
   return launch_ms<4>(c, a, st);
+}
+
+// Split-K shape: the one-pass kernel's token block for M (as above), then K
+// ranges of at least kMxSplitMinChunks chunks until about kMxSplitTarget
+// workgroups run (two per CU).
+constexpr int kMxSplitTarget = 512;
+
+struct MxSplitShape {
+  int MS, S, kc_range;
+};
+
+MxSplitShape mx_split_shape(int64_t M, int64_t N, int64_t K) {
+  MxSplitShape s;
+  const int64_t tiles = (N + kTileN - 1) / kTileN, groups = (tiles + kWaves - 1) / kWaves;
+  const int64_t kc = (K + kChunkK - 1) / kChunkK;
+  s.MS = M <= 32 ? 1 : M <= 64 ? 2 : 4;
+  const int64_t items = groups * std::max<int64_t>(1, (M + 32 * s.MS - 1) / (32 * s.MS));
+  int64_t S = (kMxSplitTarget + items - 1) / items;
+  S = std::max<int64_t>(1, std::min<int64_t>(S, kc / kMxSplitMinChunks));
+  s.kc_range = int((kc + S - 1) / S);
+  s.S = int((kc + s.kc_range - 1) / s.kc_range);  // no empty range
+  return s;
+}
+
+size_t mx_split_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  return size_t(mx_split_shape(M, N, K).S) * size_t(M) * size_t(N) * sizeof(float);
+}
+
+hipError_t launch_mx_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
+                           hipStream_t st) {
+  const Layout L = make_layout(true, N, K);
+  const MxSplitShape sh = mx_split_shape(M, N, K);
+  MxArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles), L.scales_off};
+  a.k_ranges = sh.S;
+  a.kc_range = sh.kc_range;
+  a.part = static_cast<float*>(workspace);
+  const hipError_t e = sh.MS == 1 ? launch_ms<1>(c, a, st) : sh.MS == 2 ? launch_ms<2>(c, a, st)
+                                                                        : launch_ms<4>(c, a, st);
+  if (e != hipSuccess) return e;
+  return launch_split_reduce(a.part, s_a, Y, M, N, sh.S, c.y_bf16, st);
 }
 
 }  // namespace sdq

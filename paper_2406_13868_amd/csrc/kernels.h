@@ -86,6 +86,19 @@ hipError_t launch_int_split(const Cfg& c, const uint8_t* Xq, const float* s_a, i
 // MX family, scaled matrix-core kernel (any M).
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                           const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
+// The same kernel with K split across workgroups: raw partial sums of the K
+// ranges in `workspace` (mx_split_workspace_bytes(M, N, K) bytes, 16-byte
+// aligned), then the split-K reduction below.
+constexpr int kMxSplitMinChunks = 4;  // 128-K chunks per K range, at least
+size_t mx_split_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_mx_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                           const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
+                           hipStream_t st);
+
+// Y[m, n] = s_a[m] * (part[0][m, n] + ... + part[S-1][m, n]), the ranges added
+// in order (part: [S][M][N] fp32, 16-byte aligned); fp32 or bf16 Y.
+hipError_t launch_split_reduce(const float* part, const float* s_a, void* Y, int64_t M, int64_t N, int S,
+                               bool y_bf16, hipStream_t st);
 
 // MX family with outliers, two passes for many tokens: the blob is expanded
 // once into dense merged fp8 fragments in `workspace` (at least
@@ -109,9 +122,9 @@ constexpr size_t kStaticScratchBytes = size_t(48) << 20;
 hipError_t launch_mx_dense_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                                   const uint8_t* blob, int64_t N, int64_t K, void* Y,
                                   hipStream_t st);
-// launch_int_split with the same static array as the workspace (the caller
-// checks the size).
-hipError_t int_split_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
-                            const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
+// launch_int_split (INT) or launch_mx_split (MX) with the same static array
+// as the workspace (the caller checks the size).
+hipError_t split_static(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                        const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st);
 
 }  // namespace sdq

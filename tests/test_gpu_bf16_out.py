@@ -58,9 +58,9 @@ def test_gemm_bf16_is_rounded_fp32(cfg, M):
     X = torch.from_numpy(synth.make_x(2, M, K)).cuda()
     blob = torch.from_numpy(sdq.pack(synth.make_w(2, 0, N, K), cfg)).cuda()
     Xq, s_a = sdq.quantize_act(X, cfg)
-    paths = [sdq.PATH_MFMA]
+    paths = [sdq.PATH_MFMA, sdq.PATH_SPLITK]
     if cfg.family == "int":
-        paths = ([sdq.PATH_DECODE] if M <= 8 else []) + paths + [sdq.PATH_SPLITK]
+        paths = ([sdq.PATH_DECODE] if M <= 8 else []) + paths
     for path in paths:
         say("bf16 out", cfg.family, cfg.fmt_o, cfg.n_i, M, "path", path)
         Y32 = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=path)

@@ -64,8 +64,8 @@ def _paths(fam, M, n_o=1):
     if fam == "int":
         return ([sdq.PATH_DECODE] if M <= 8 else []) + [sdq.PATH_MFMA, sdq.PATH_SPLITK]
     if fam == "mx" and n_o:
-        return [sdq.PATH_MFMA, sdq.PATH_DENSE]
-    return [sdq.PATH_MFMA]
+        return [sdq.PATH_MFMA, sdq.PATH_DENSE, sdq.PATH_SPLITK]
+    return [sdq.PATH_MFMA, sdq.PATH_SPLITK]
 
 
 @pytest.mark.parametrize("c", INT_CFGS + MX_CFGS, ids=_ids)
@@ -370,14 +370,17 @@ def test_hip_graph_replays_match_eager(c):
         torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("which", ["mx-dense", "int-splitk"])
+@pytest.mark.parametrize("which", ["mx-dense", "int-splitk", "mx-splitk"])
 def test_hip_graph_replays_match_eager_two_pass(which):
-    """The workspace paths (two-pass MX, INT split-K; workspace allocated
-    before capture) replay like eager, whatever the workspace held."""
+    """The workspace paths (two-pass MX, INT and MX split-K; workspace
+    allocated before capture) replay like eager, whatever the workspace held."""
     torch = torch_cuda()
     if which == "mx-dense":
         cfg, _ = _cfgs(*MX_CFGS[1])
         N, K, M, path = 544, 640, 600, sdq.PATH_DENSE
+    elif which == "mx-splitk":
+        cfg, _ = _cfgs(*MX_CFGS[1])
+        N, K, M, path = 1000, 2304, 200, sdq.PATH_SPLITK
     else:
         cfg, _ = _cfgs(*INT_CFGS[1])
         N, K, M, path = 1000, 2304, 100, sdq.PATH_SPLITK
@@ -424,6 +427,21 @@ def test_split_k_ragged_shapes(c, M, N, K):
     check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} split-K")
 
 
+@pytest.mark.parametrize("c", [MX_CFGS[0], MX_CFGS[1], MX_CFGS[4]], ids=_ids)
+@pytest.mark.parametrize("M,N,K", [(9, 4128, 512), (33, 97, 4096), (64, 1000, 16384), (100, 544, 1152),
+                                   (129, 64, 8192), (256, 4096, 4096), (300, 2080, 640), (511, 33, 1024)])
+def test_mx_split_k_ragged_shapes(c, M, N, K):
+    """The MX family's split-K path on shapes that give 1 to 32 K ranges,
+    every token block and ragged tiles, against the oracle."""
+    cfg, cfg_o = _cfgs(*c)
+    X = synth.make_x(4, M, K)
+    W = synth.make_w(4, 4, N, K)
+    Yref, _, _, _ = S.reference(X, W, cfg_o)
+    say("mx split-K ragged", _ids(c), M, N, K)
+    Y, _, _, _ = run_gpu(X, W, cfg, sdq.PATH_SPLITK)
+    check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} mx split-K")
+
+
 def _split_case(kind, N, K, rng):
     """MX weights whose blocks cannot merge the inliers into the outliers' e4m3
     fragment (inlier/outlier exponent difference outside [-5, 6])."""
@@ -448,7 +466,7 @@ def _split_case(kind, N, K, rng):
 @pytest.mark.parametrize("kind", ["product", "zero_inliers", "huge_outliers"])
 @pytest.mark.parametrize("n_i", [2, 3])
 @pytest.mark.parametrize("M,N,K", [(64, 96, 512), (256, 64, 1024), (520, 96, 384)])
-@pytest.mark.parametrize("path", [sdq.PATH_MFMA, sdq.PATH_DENSE])
+@pytest.mark.parametrize("path", [sdq.PATH_MFMA, sdq.PATH_DENSE, sdq.PATH_SPLITK])
 def test_mx_unmergeable_blocks(kind, n_i, M, N, K, path):
     """The matrix kernel's correction path for blocks that stay split."""
     rng = np.random.default_rng(7)

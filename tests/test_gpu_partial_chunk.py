@@ -53,7 +53,7 @@ def test_mx_paths(c, M, N, K):
     X = synth.make_x(6, M, K)
     W = synth.make_w(6, 2, N, K)
     Yref, _, _, _ = S.reference(X, W, cfg_o)
-    paths = [sdq.PATH_MFMA] + ([sdq.PATH_DENSE] if c[1] else [])
+    paths = [sdq.PATH_MFMA, sdq.PATH_SPLITK] + ([sdq.PATH_DENSE] if c[1] else [])
     for path in paths:
         say("partial chunk mx", _ids(c), M, N, K, "path", path)
         Y, _, _, _ = run_gpu(X, W, cfg, path)

@@ -297,6 +297,13 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(cfg, 3, 4096, 11008) == sdq.PATH_MFMA
     # the two-pass MX path only on a grid of at least 160 workgroups
     mx = sdq.Config.mx_family()
+    # the MX split-K path where the one-pass grid of 128 x 128 holds at most 128 workgroups
+    for (M, N, K) in ((1, 4096, 4096), (64, 11008, 4096), (128, 11008, 4096), (256, 4096, 11008),
+                      (512, 4096, 4096), (16, 4096, 1024)):
+        assert sdq.gemm_path(mx, M, N, K, workspace=True) == sdq.PATH_SPLITK, (M, N, K)
+        assert sdq.gemm_path(mx, M, N, K) == sdq.PATH_MFMA  # without a workspace: one pass
+    for (M, N, K) in ((256, 11008, 4096), (768, 4096, 4096), (16, 4096, 896)):
+        assert sdq.gemm_path(mx, M, N, K, workspace=True) == sdq.PATH_MFMA, (M, N, K)
     assert sdq.gemm_path(mx, 512, 11008, 4096, workspace=True) == sdq.PATH_DENSE
     assert sdq.gemm_path(mx, 1024, 4096, 4096, workspace=True) == sdq.PATH_MFMA
     assert sdq.gemm_path(mx, 2048, 4096, 4096, workspace=True) == sdq.PATH_DENSE
@@ -318,8 +325,13 @@ def test_gemm_path_choice():
         b = sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK)
         S = b // max(4 * M * N, 1)
         assert b == 4 * S * M * N and 1 <= max(S, 1) <= max(1, K // 512), (M, N, K, S)
+    # the MX family's split-K path: S K ranges of at least 4 chunks, about 512 workgroups
+    for (M, N, K) in ((256, 4096, 4096), (128, 11008, 4096), (256, 4096, 11008), (64, 64, 288)):
+        b = sdq.gemm_workspace_size(mx, M, N, K, sdq.PATH_SPLITK)
+        S = b // (4 * M * N)
+        assert b == 4 * S * M * N and 1 <= S <= max(1, -(-K // 128) // 4), (M, N, K, S)
     with pytest.raises(sdq.SDQError):
-        sdq.gemm_workspace_size(mx, 64, 4096, 4096, sdq.PATH_SPLITK)
+        sdq.gemm_workspace_size(sdq.Config.dual_family(), 64, 4096, 4096, sdq.PATH_SPLITK)
 
 
 def test_gemm_workspace_size_and_validation():
@@ -330,7 +342,8 @@ def test_gemm_workspace_size_and_validation():
     it = sdq.Config.int_family()
     assert sdq.gemm_workspace_size(mx, 2048, 11008, 4096) == 11008 * 4096
     assert sdq.gemm_workspace_size(mx, 512, 11008, 4096) == 11008 * 4096  # 43 x 4 workgroups
-    assert sdq.gemm_workspace_size(mx, 512, 100, 384) == 0               # one pass on a small grid
+    assert sdq.gemm_workspace_size(mx, 512, 100, 384) == 0               # one pass: K holds one range
+    assert sdq.gemm_workspace_size(mx, 512, 100, 1024) == 2 * 4 * 512 * 100  # split-K: two ranges
     assert sdq.gemm_workspace_size(mx, 1024, 4096, 4096) == 0            # 16 x 8 workgroups
     assert sdq.gemm_workspace_size(mx, 511, 11008, 4096) == 0            # one pass below 512 tokens
     assert sdq.gemm_workspace_size(mx, 512, 100, 384, sdq.PATH_DENSE) == 128 * 384  # N padded to 32

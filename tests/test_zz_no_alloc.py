@@ -67,12 +67,13 @@ def test_static_entry_refuses_a_workspace_beyond_the_array():
     assert e.value.status == -8
 
 
-def test_static_entry_equals_workspace_entry_split_k():
-    """The INT family's split-K path (partial sums of K ranges in the scratch
-    array): two calls in a row, the second smaller, each bit for bit equal to
-    sdq_gemm_ws with a caller-owned workspace."""
+@pytest.mark.parametrize("fam", ["int", "mx"])
+def test_static_entry_equals_workspace_entry_split_k(fam):
+    """The split-K paths of the INT and MX families (partial sums of K ranges
+    in the scratch array): two calls in a row, the second smaller, each bit
+    for bit equal to sdq_gemm_ws with a caller-owned workspace."""
     torch = torch_cuda()
-    cfg = sdq.Config.int_family(1, 8, "int8", 3)
+    cfg = sdq.Config.int_family(1, 8, "int8", 3) if fam == "int" else CFG
     for (M, N, K, seed) in ((64, 4128, 16384, 1), (20, 1000, 2048, 2)):
         assert 0 < sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK) <= _lib.STATIC_SCRATCH_BYTES
         W = synth.make_w(4, 10 + seed, N, K)
@@ -80,7 +81,7 @@ def test_static_entry_equals_workspace_entry_split_k():
         Xq, s_a = sdq.quantize_act(torch.from_numpy(synth.make_x(4, M, K, seed=seed)).cuda(), cfg)
         ws = torch.full((sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK),), 0x7F,
                         dtype=torch.uint8, device="cuda")  # stale contents must not matter
-        say("static scratch split-K", M, N, K)
+        say("static scratch split-K", fam, M, N, K)
         Y_ws = sdq.gemm(Xq, s_a, blob, N, K, cfg, path=sdq.PATH_SPLITK, workspace=ws)
         Y_st = torch.full((M, N), float("nan"), device="cuda")
         st = _lib.lib().sdq_gemm_static(C.byref(cfg.c()), C.c_void_p(Xq.data_ptr()),
