@@ -261,7 +261,7 @@ __global__ __launch_bounds__(kDThreads, MS >= 4 ? 1 : 2) void dual_mfma_kernel(D
       store_out(yr, a.N, n, ms, e, h, fmaf(rs.v[ms][e], so * float(acco[ms][e]), acc[ms][e]));
 }
 
-// Split-K form for few tokens (M <= 32): one 32-row tile per workgroup, its
+// Split-K form for few tokens (up to 32, more on narrow layers): one 32-row tile per workgroup, its
 // NW waves take interleaved 128-K chunks (two in flight per wave) and read
 // their activations straight into registers; the wave partials of both
 // accumulators are summed through LDS in a fixed-order tree.  This keeps
@@ -389,10 +389,16 @@ hipError_t launch_ms(const DualArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// The split-K or tiled form, by the number of tokens (NP outlier planes).
+// The split-K form up to 32 tokens, and beyond while its grid (one tile x 32
+// tokens per workgroup) stays within one round, or two on long rows
+// (measured: 4096x4096 at M = 48 / 64 takes 11.9 / 12.0 us against 18.8 in
+// tiles, at 96 21.1 against 19.0; 4096x11008 at M = 64 / 96 / 128 takes 23.1
+// / 41.7 / 42.6 against 48.6 / 48.5 / 48.7; 11008x4096 at M = 48 27.4
+// against 22.6); else the tiled form (NP outlier planes).
 template <int NP>
 hipError_t launch_np(const DualArgs& a, hipStream_t st) {
-  if (a.M <= 32) {
+  const int64_t split_grid = int64_t(a.n_tiles) * ((a.M + 31) / 32);
+  if (a.M <= 32 || split_grid <= 256 || (a.K >= 8192 && split_grid <= 512)) {
     const dim3 grid(unsigned(a.n_tiles), unsigned((a.M + 31) / 32));
     hipLaunchKernelGGL((dual_splitk_kernel<4, NP>), grid, dim3(4 * 64), 0, st, a);
     return hipGetLastError();

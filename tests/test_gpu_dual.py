@@ -131,9 +131,14 @@ def test_gemm_dual_decode_grid_is_exact():
         assert np.array_equal(Y.astype(np.float64), Yref)
 
 
-def _tokens_per_block(M, N):
-    """The tiled kernel's token block for this shape (32, 64 or 128): the
-    smallest that keeps the GPU full, by workgroup count."""
+def _tokens_per_block(M, N, K=128):
+    """The matrix form for this shape (above two tokens): "split" (one tile and
+    32 tokens per workgroup, K over its waves) while its grid stays within a
+    round (two on rows of 8192 and more), else the tiled kernel's token block
+    (32, 64 or 128): the smallest that keeps the GPU full, by workgroup count."""
+    split_grid = -(-N // 32) * -(-M // 32)
+    if M <= 32 or split_grid <= 256 or (K >= 8192 and split_grid <= 512):
+        return "split"
     groups = -(-(-(-N // 32)) // 4)
     if groups * -(-M // 32) <= 256:
         return 32
@@ -142,13 +147,15 @@ def _tokens_per_block(M, N):
     return 128
 
 
-@pytest.mark.parametrize("M,N,K,block", [(100, 256, 512, 32), (300, 16384, 256, 64),
+@pytest.mark.parametrize("M,N,K,block", [(100, 4096, 512, 32), (300, 16384, 256, 64),
                                          (1100, 4096, 128, 64), (300, 32768, 128, 128),
-                                         (2100, 4096, 128, 128)])
+                                         (2100, 4096, 128, 128), (64, 4096, 4096, "split"),
+                                         (96, 4096, 11008, "split"), (100, 256, 512, "split")])
 @pytest.mark.parametrize("n_o,n_i", [(1, 6), (2, 4)])
 def test_gemm_dual_every_token_block(M, N, K, block, n_o, n_i):
-    """Shapes that take each token block of the tiled kernel, with ragged M."""
-    assert _tokens_per_block(M, N) == block
+    """Shapes that take each token block of the tiled kernel, and the split-K
+    form beyond 32 tokens, with ragged M."""
+    assert _tokens_per_block(M, N, K) == block
     cfg, cfg_o = _cfgs(n_o, n_i)
     X = synth.make_x(2, M, K)
     W = synth.make_w(2, 0, N, K)
