@@ -72,6 +72,43 @@ class Config:
         return Config("dual", n_o, 8, "int8", n_i, 8, "e2m1", "int8", metric)
 
     @property
+    def label(self) -> str:
+        """The formats as '{family}-{n_o}:{m_o}{fmt_o}-{n_i}:{m_i}{fmt_i}-A{fmt_a}', the
+        form Config.parse reads back (metric and the other options are not part of it)."""
+        return (f"{self.family}-{self.n_o}:{self.m_o}{self.fmt_o}-{self.n_i}:{self.m_i}{self.fmt_i}"
+                f"-A{self.fmt_a}")
+
+    @staticmethod
+    def parse(label: str) -> "Config":
+        """A configuration from a label: this library's form (Config.label, e.g.
+        'mx-1:8e4m3-2:8e2m1-Ae4m3'), or the paper's SDQ names (Section 6.2's
+        tables, e.g. 'SDQ-W7:8-1:8int8-6:8fp4': W for Wanda sparsification,
+        i.e. the weight-activation product metric; then the kept N:M, the
+        outliers' n:m and format, the inliers' n:m and format).  int8
+        outliers with fp4 inliers are the dual family, with int4 inliers the
+        INT family; the kept N must equal n_o + n_i.  Raises ValueError for
+        anything else (SparseGPT, 'SDQ-S...', is not built).  Whether the
+        kernels implement the result is for check() to say."""
+        import re
+        m = re.fullmatch(r"(int|mx|dual)-(\d+):(\d+)(e4m3|int8)-(\d+):(\d+)(int4|e2m1)-A(int8|e4m3)", label)
+        if m:
+            fam, n_o, m_o, fo, n_i, m_i, fi, fa = m.groups()
+            return Config(fam, int(n_o), int(m_o), fo, int(n_i), int(m_i), fi, fa)
+        m = re.fullmatch(r"SDQ-([A-Z])(\d+):(\d+)-(\d+):(\d+)(int8|fp8)-(\d+):(\d+)(fp4|int4)", label)
+        if not m:
+            raise ValueError(f"not a configuration label: {label!r}")
+        sp, kept, m_kept, n_o, m_o, fo, n_i, m_i, fi = m.groups()
+        if sp != "W":
+            raise ValueError(f"{label!r}: sparsifier {sp!r} is not built (W, the Wanda product metric, is)")
+        if int(kept) != int(n_o) + int(n_i) or not (int(m_kept) == int(m_o) == int(m_i)):
+            raise ValueError(f"{label!r}: kept {kept}:{m_kept} is not outliers {n_o}:{m_o} + inliers {n_i}:{m_i}")
+        if fo != "int8":
+            raise ValueError(f"{label!r}: {fo} outliers with {fi} inliers is not a configuration of this library")
+        if fi == "fp4":
+            return Config("dual", int(n_o), int(m_o), "int8", int(n_i), int(m_i), "e2m1", "int8", "product")
+        return Config("int", int(n_o), int(m_o), "int8", int(n_i), int(m_i), "int4", "int8", "product")
+
+    @property
     def mx(self) -> bool:
         return self.family == "mx"
 

@@ -47,7 +47,7 @@ struct MxArgs {
   void* Y;
   int M, N, K, n_chunks, n_tiles;
   int64_t scales_off;
-  int m_blocks;  // workgroups along M; the grid is 1-D over (K range, tile group, M block)
+  int m_blocks = 1;  // workgroups along M; the grid is 1-D over (K range, tile group, M block)
   bool y_bf16 = false;  // Y as bf16
   int k_ranges = 1;     // ranges of chunks the grid splits K into
   int kc_range = 0;     // chunks per range (the last may hold fewer)
