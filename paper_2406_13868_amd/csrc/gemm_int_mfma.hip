@@ -400,9 +400,11 @@ hipError_t launch_splitk(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int MS, int NI, int SF>
+// TILED: the tiled kernel even for MS <= 2 (which otherwise takes the
+// split-K form).
+template <int MS, int NI, int SF, bool TILED>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if constexpr (MS <= 2) {
+  if constexpr (MS <= 2 && !TILED) {
     // few tokens: split K inside the workgroup so that about 2048+ waves run
     const int64_t waves4 = int64_t(a.n_tiles) * 4 * ((a.M + 32 * MS - 1) / (32 * MS));
     if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SF>(c, a, st);
@@ -417,18 +419,18 @@ hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int MS, int SF>
+template <int MS, int SF, bool TILED>
 hipError_t launch_ms_sc(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.n_i == 1) return launch_ms_ni<MS, 1, SF>(c, a, st);
-  if (c.n_i == 2) return launch_ms_ni<MS, 2, SF>(c, a, st);
-  return launch_ms_ni<MS, 3, SF>(c, a, st);
+  if (c.n_i == 1) return launch_ms_ni<MS, 1, SF, TILED>(c, a, st);
+  if (c.n_i == 2) return launch_ms_ni<MS, 2, SF, TILED>(c, a, st);
+  return launch_ms_ni<MS, 3, SF, TILED>(c, a, st);
 }
 
-template <int MS>
+template <int MS, bool TILED = false>
 hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.sc8) return launch_ms_sc<MS, kScaleE4M3>(c, a, st);
-  if (c.e6m2) return launch_ms_sc<MS, kScaleE6M2>(c, a, st);
-  return launch_ms_sc<MS, kScaleF16>(c, a, st);
+  if (c.sc8) return launch_ms_sc<MS, kScaleE4M3, TILED>(c, a, st);
+  if (c.e6m2) return launch_ms_sc<MS, kScaleE6M2, TILED>(c, a, st);
+  return launch_ms_sc<MS, kScaleF16, TILED>(c, a, st);
 }
 
 }  // namespace
@@ -452,9 +454,18 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   // runs when its last round of workgroups is at least 3/4 full.  Measured
   // on 4096x4096: M = 128/256/512 take 24/37/70 us split-K against 104/106/111
   // tiled (32 to 128 workgroups); 11008x4096 at M = 512 takes 179 against 216.
-  const int64_t w4 = int64_t((L.n_tiles + kWaves - 1) / kWaves) * ((M + 127) / 128);
+  const int64_t groups = (L.n_tiles + kWaves - 1) / kWaves;
+  const int64_t w4 = groups * ((M + 127) / 128);
   const int64_t rounds = (w4 + kCUs - 1) / kCUs;
   if (4 * w4 < 3 * kCUs * rounds) return launch_ms<2>(c, a, st);
+  // The tiled kernel with 64-token blocks (three workgroups per CU, each
+  // weight expanded twice as often) once its grid fills three workgroups per
+  // CU, else 128-token blocks (one per CU).  Measured, 128 -> 64: 4096x4096
+  // at M = 2048 / 4096 206 -> 186 / 409 -> 348 us; 11008x4096 at M = 1024 /
+  // 2048 / 4096 308 -> 265 / 612 -> 478 / 1121 -> 945; 4096x11008 at 2048 /
+  // 4096 535 -> 487 / 1066 -> 915; on smaller grids 4096x4096 and 4096x11008
+  // at M = 1024 take 105 / 270 with 128 against 107 / 278 with 64.
+  if (groups * ((M + 63) / 64) >= 3 * kCUs) return launch_ms<2, true>(c, a, st);
   return launch_ms<4>(c, a, st);
 }
 

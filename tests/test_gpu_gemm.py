@@ -239,13 +239,16 @@ def _kernel_for(fam, M, N):
     """Which matrix-core kernel the launcher picks above 64 tokens (the rule
     the kernels' launchers state): INT "tiled" when its grid of
     ceil(N/128) x ceil(M/128) workgroups fills its last round of 256 to at
-    least 3/4, else "split-K"; MX token blocks of 32, 64 or 128 (the largest
-    whose grid stays within one round of 256 workgroups)."""
+    least 3/4 ("tiled64", 64-token blocks, when ceil(N/128) x ceil(M/64) is
+    at least 768), else "split-K"; MX token blocks of 32, 64 or 128 (the
+    largest whose grid stays within one round of 256 workgroups)."""
     groups = -(-N // 128)
     if fam == "int":
         w4 = groups * -(-M // 128)
         rounds = -(-w4 // 256)
-        return "split-K" if 4 * w4 < 3 * 256 * rounds else "tiled"
+        if 4 * w4 < 3 * 256 * rounds:
+            return "split-K"
+        return "tiled64" if groups * -(-M // 64) >= 768 else "tiled"
     if groups * -(-M // 32) <= 256:
         return "block32"
     if groups * -(-M // 64) <= 256:
@@ -255,6 +258,7 @@ def _kernel_for(fam, M, N):
 
 @pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 100, 70, 256, "split-K"), ("int", 384, 8192, 256, "tiled"),
                                               ("int", 400, 8192, 128, "tiled"), ("int", 700, 2048, 128, "split-K"),
+                                              ("int", 1000, 8192, 128, "tiled64"), ("int", 770, 16384, 256, "tiled64"),
                                               ("mx", 100, 70, 256, "block32"), ("mx", 200, 8192, 256, "block64"),
                                               ("mx", 300, 8192, 128, "block128")])
 def test_every_matrix_kernel_above_64_tokens(fam, M, N, K, kernel):

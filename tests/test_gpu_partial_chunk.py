@@ -33,6 +33,7 @@ def test_int_paths(c, M, N, K):
 
 
 @pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 384, 8192, 160, "tiled"), ("int", 700, 2048, 288, "split-K"),
+                                              ("int", 1000, 8192, 160, "tiled64"),
                                               ("mx", 100, 70, 160, "block32"), ("mx", 200, 8192, 288, "block64"),
                                               ("mx", 300, 8192, 160, "block128")])
 def test_every_matrix_kernel(fam, M, N, K, kernel):
