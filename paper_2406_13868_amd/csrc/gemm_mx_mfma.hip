@@ -315,9 +315,10 @@ hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int
   return launch_ms<4>(c, a, st);
 }
 
-// Split-K shape: the one-pass kernel's token block for M (as above), then K
-// ranges of at least kMxSplitMinChunks chunks until about kMxSplitTarget
-// workgroups run (two per CU).
+// Split-K shape: token blocks of 32 tokens up to 32, 64 up to 64, else 128
+// (the K split, not the token block, fills the GPU), then K ranges of at
+// least kMxSplitMinChunks chunks until about kMxSplitTarget workgroups run
+// (two per CU).
 constexpr int kMxSplitTarget = 512;
 
 struct MxSplitShape {
