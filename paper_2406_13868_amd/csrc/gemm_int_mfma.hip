@@ -14,7 +14,9 @@
 //   Y = s_a * (acc + s_o * acc_o)
 //
 // Tiling: a workgroup of 4 waves owns 4 row tiles of W (128 outputs) and BM
-// = 32*MS tokens.  Each 128-K chunk of activations is converted from int8 to
+// = 32*MS = 128 tokens, two workgroups per CU (the register budget of two
+// waves per SIMD holds the eight 32x32 accumulators of a wave without
+// spilling).  Each 128-K chunk of activations is converted from int8 to
 // fp16 and staged in LDS (double buffered) for all 4 waves; each wave streams
 // its own tile's group words (32 bytes per lane per chunk) and
 // expands them in registers into dense fp16 B fragments: lane l holds column
@@ -51,7 +53,7 @@ struct MfmaArgs {
 };
 
 template <int MS, int NI, bool OUT_INT8, int SF>
-__global__ __launch_bounds__(kThreads) void int_mfma_kernel(MfmaArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
   constexpr bool SC8 = SF == kScaleE4M3;       // two-level: a power of two per row
   constexpr bool ONE = SF != kScaleF16;        // q * s exact in one fp16 fragment
   const int kSB = kTileN * a.srow;             // inlier scale bytes per (tile, chunk)
@@ -400,37 +402,38 @@ hipError_t launch_splitk(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// TILED: the tiled kernel even for MS <= 2 (which otherwise takes the
-// split-K form).
-template <int MS, int NI, int SF, bool TILED>
+// MS <= 2 (32 or 64 tokens per block): the split-K form; MS = 4: the tiled
+// kernel.
+template <int MS, int NI, int SF>
 hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if constexpr (MS <= 2 && !TILED) {
-    // few tokens: split K inside the workgroup so that about 2048+ waves run
+  if constexpr (MS <= 2) {
+    // split K inside the workgroup so that about 2048+ waves run
     const int64_t waves4 = int64_t(a.n_tiles) * 4 * ((a.M + 32 * MS - 1) / (32 * MS));
     if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SF>(c, a, st);
     return launch_splitk<MS, NI, 8, SF>(c, a, st);
+  } else {
+    const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
+    const dim3 block(kThreads);
+    if (c.fmt_o == SDQ_FMT_INT8)
+      hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SF>), grid, block, 0, st, a);
+    else
+      hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false, SF>), grid, block, 0, st, a);
+    return hipGetLastError();
   }
-  const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
-  const dim3 block(kThreads);
-  if (c.fmt_o == SDQ_FMT_INT8)
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SF>), grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL((int_mfma_kernel<MS, NI, false, SF>), grid, block, 0, st, a);
-  return hipGetLastError();
 }
 
-template <int MS, int SF, bool TILED>
+template <int MS, int SF>
 hipError_t launch_ms_sc(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.n_i == 1) return launch_ms_ni<MS, 1, SF, TILED>(c, a, st);
-  if (c.n_i == 2) return launch_ms_ni<MS, 2, SF, TILED>(c, a, st);
-  return launch_ms_ni<MS, 3, SF, TILED>(c, a, st);
+  if (c.n_i == 1) return launch_ms_ni<MS, 1, SF>(c, a, st);
+  if (c.n_i == 2) return launch_ms_ni<MS, 2, SF>(c, a, st);
+  return launch_ms_ni<MS, 3, SF>(c, a, st);
 }
 
-template <int MS, bool TILED = false>
+template <int MS>
 hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
-  if (c.sc8) return launch_ms_sc<MS, kScaleE4M3, TILED>(c, a, st);
-  if (c.e6m2) return launch_ms_sc<MS, kScaleE6M2, TILED>(c, a, st);
-  return launch_ms_sc<MS, kScaleF16, TILED>(c, a, st);
+  if (c.sc8) return launch_ms_sc<MS, kScaleE4M3>(c, a, st);
+  if (c.e6m2) return launch_ms_sc<MS, kScaleE6M2>(c, a, st);
+  return launch_ms_sc<MS, kScaleF16>(c, a, st);
 }
 
 }  // namespace
@@ -448,24 +451,23 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   // leaves fewer workgroups than compute units, two 32-token blocks fill the
   // GPU instead (each weight is then expanded twice)
   if (M <= 64) return L.n_tiles < kCUs ? launch_ms<1>(c, a, st) : launch_ms<2>(c, a, st);
-  // More tokens: the tiled kernel (four tiles x 128 tokens per workgroup,
-  // one workgroup per compute unit) does about 1.3x the work per unit of time
-  // of the split-K kernel over 64-token blocks, but only on a full grid: it
-  // runs when its last round of workgroups is at least 3/4 full.  Measured
-  // on 4096x4096: M = 128/256/512 take 24/37/70 us split-K against 104/106/111
-  // tiled (32 to 128 workgroups); 11008x4096 at M = 512 takes 179 against 216.
+  // More tokens: the tiled kernel (four row tiles x 128 tokens per
+  // workgroup, two workgroups per CU) or the split-K form over 64-token
+  // blocks, whichever this cost model says is faster.  A tiled workgroup
+  // alone on a CU takes one unit of time and two sharing a CU take 1.45
+  // units (4096x4096: 103 us at 256 workgroups, 145 at 384, 155 at 512), so
+  // a grid of w4 workgroups takes 1.45 units per full round of two per CU
+  // plus 1 or 1.45 for a last partial round.  The split-K form costs about
+  // 1/220 unit per workgroup's worth of work (4096x4096 at M = 512: 58 us),
+  // with no rounds.  Measured, split-K against tiled: 4096x4096 at M = 768 /
+  // 1024 / 1536: 81 / 106 / 156 against 102 / 103 / 145 us; 11008x4096 at
+  // M = 512 / 768 / 1024: 151 / 220 / 283 against 146 / 227 / 230;
+  // 4096x11008 at M = 512 / 1024: 139 / 258 against 262 / 263.
   const int64_t groups = (L.n_tiles + kWaves - 1) / kWaves;
   const int64_t w4 = groups * ((M + 127) / 128);
-  const int64_t rounds = (w4 + kCUs - 1) / kCUs;
-  if (4 * w4 < 3 * kCUs * rounds) return launch_ms<2>(c, a, st);
-  // The tiled kernel with 64-token blocks (three workgroups per CU, each
-  // weight expanded twice as often) once its grid fills three workgroups per
-  // CU, else 128-token blocks (one per CU).  Measured, 128 -> 64: 4096x4096
-  // at M = 2048 / 4096 206 -> 186 / 409 -> 348 us; 11008x4096 at M = 1024 /
-  // 2048 / 4096 308 -> 265 / 612 -> 478 / 1121 -> 945; 4096x11008 at 2048 /
-  // 4096 535 -> 487 / 1066 -> 915; on smaller grids 4096x4096 and 4096x11008
-  // at M = 1024 take 105 / 270 with 128 against 107 / 278 with 64.
-  if (groups * ((M + 63) / 64) >= 3 * kCUs) return launch_ms<2, true>(c, a, st);
+  const int64_t full = w4 / (2 * kCUs), rem = w4 % (2 * kCUs);
+  const int64_t tiled20 = 29 * full + (rem == 0 ? 0 : rem <= kCUs ? 20 : 29);  // tiled time x 20
+  if (w4 < 11 * tiled20) return launch_ms<2>(c, a, st);                     // w4 / 220 units < tiled
   return launch_ms<4>(c, a, st);
 }
 

@@ -142,7 +142,8 @@ def _int_grid(rng, M, N, K, outlier_fmt):
 
 
 @pytest.mark.parametrize("fmt_o", ["int8", "e4m3"])
-@pytest.mark.parametrize("M,N,K", [(1, 64, 4096), (2, 32, 1024), (16, 96, 1024), (64, 64, 4096)])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 4096), (2, 32, 1024), (16, 96, 1024), (64, 64, 4096),
+                                   (400, 8192, 128)])
 def test_integer_grid_is_exact(fmt_o, M, N, K):
     cfg, cfg_o = _cfgs("int", 1, 8, fmt_o, 3)
     rng = np.random.default_rng(M * 7 + N)
@@ -236,19 +237,19 @@ def test_quantized_activations_feed_gemm_like_oracle():
 
 
 def _kernel_for(fam, M, N):
-    """Which matrix-core kernel the launcher picks above 64 tokens (the rule
-    the kernels' launchers state): INT "tiled" when its grid of
-    ceil(N/128) x ceil(M/128) workgroups fills its last round of 256 to at
-    least 3/4 ("tiled64", 64-token blocks, when ceil(N/128) x ceil(M/64) is
-    at least 768), else "split-K"; MX token blocks of 32, 64 or 128 (the
-    largest whose grid stays within one round of 256 workgroups)."""
+    """Which matrix-core kernel the launcher picks above 64 tokens (the cost
+    model the kernels' launchers state): INT "tiled" (128-token blocks, two
+    workgroups per CU) when its grid of w4 = ceil(N/128) x ceil(M/128)
+    workgroups, at 1.45 units of time per full round of 512 plus 1 (up to 256
+    left) or 1.45 for a partial one, is faster than the split-K form at w4/220
+    units, else "split-K"; MX token blocks of 32, 64 or 128 (the largest whose
+    grid stays within one round of 256 workgroups)."""
     groups = -(-N // 128)
     if fam == "int":
         w4 = groups * -(-M // 128)
-        rounds = -(-w4 // 256)
-        if 4 * w4 < 3 * 256 * rounds:
-            return "split-K"
-        return "tiled64" if groups * -(-M // 64) >= 768 else "tiled"
+        full, rem = divmod(w4, 512)
+        tiled20 = 29 * full + (0 if rem == 0 else 20 if rem <= 256 else 29)
+        return "split-K" if w4 < 11 * tiled20 else "tiled"
     if groups * -(-M // 32) <= 256:
         return "block32"
     if groups * -(-M // 64) <= 256:
@@ -256,9 +257,10 @@ def _kernel_for(fam, M, N):
     return "block128"
 
 
-@pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 100, 70, 256, "split-K"), ("int", 384, 8192, 256, "tiled"),
+@pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 100, 70, 256, "split-K"), ("int", 384, 8192, 256, "split-K"),
                                               ("int", 400, 8192, 128, "tiled"), ("int", 700, 2048, 128, "split-K"),
-                                              ("int", 1000, 8192, 128, "tiled64"), ("int", 770, 16384, 256, "tiled64"),
+                                              ("int", 1000, 8192, 128, "tiled"), ("int", 770, 16384, 256, "tiled"),
+                                              ("int", 1300, 8192, 128, "tiled"),
                                               ("mx", 100, 70, 256, "block32"), ("mx", 200, 8192, 256, "block64"),
                                               ("mx", 300, 8192, 128, "block128")])
 def test_every_matrix_kernel_above_64_tokens(fam, M, N, K, kernel):

@@ -32,8 +32,8 @@ def test_int_paths(c, M, N, K):
         check(Y, Yref, X, W, cfg_o, f"{_ids(c)} M={M} N={N} K={K} path={path}")
 
 
-@pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 384, 8192, 160, "tiled"), ("int", 700, 2048, 288, "split-K"),
-                                              ("int", 1000, 8192, 160, "tiled64"),
+@pytest.mark.parametrize("fam,M,N,K,kernel", [("int", 400, 8192, 160, "tiled"), ("int", 700, 2048, 288, "split-K"),
+                                              ("int", 1000, 8192, 160, "tiled"),
                                               ("mx", 100, 70, 160, "block32"), ("mx", 200, 8192, 288, "block64"),
                                               ("mx", 300, 8192, 160, "block128")])
 def test_every_matrix_kernel(fam, M, N, K, kernel):
