@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
     const uint32_t wv[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
     const uint32_t sv[4] = {sr.x, sr.y, sr.z, sr.w};
     if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
-#pragma unroll 2
+#pragma unroll
     for (int kb = 0; kb < 8; ++kb) {
       const _Float16 s = block_scale<SF>(sv, kb, a.qs);
       h8 bh, bl;
@@ -454,20 +454,21 @@ hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, in
   // More tokens: the tiled kernel (four row tiles x 128 tokens per
   // workgroup, two workgroups per CU) or the split-K form over 64-token
   // blocks, whichever this cost model says is faster.  A tiled workgroup
-  // alone on a CU takes one unit of time and two sharing a CU take 1.45
-  // units (4096x4096: 103 us at 256 workgroups, 145 at 384, 155 at 512), so
-  // a grid of w4 workgroups takes 1.45 units per full round of two per CU
-  // plus 1 or 1.45 for a last partial round.  The split-K form costs about
-  // 1/220 unit per workgroup's worth of work (4096x4096 at M = 512: 58 us),
-  // with no rounds.  Measured, split-K against tiled: 4096x4096 at M = 768 /
-  // 1024 / 1536: 81 / 106 / 156 against 102 / 103 / 145 us; 11008x4096 at
-  // M = 512 / 768 / 1024: 151 / 220 / 283 against 146 / 227 / 230;
-  // 4096x11008 at M = 512 / 1024: 139 / 258 against 262 / 263.
+  // alone on a CU takes one unit of time and two sharing a CU take 1.7 units
+  // (4096x4096: 85 us at 256 workgroups, 144 at 512), so a grid of w4
+  // workgroups takes 1.7 units per full round of two per CU, plus 1.7 for a
+  // last round of more than one per CU, or for at most one per CU 1 unit
+  // alone and 0.65 after a full round (its workgroups start as the CUs of
+  // the full round drain: 11008x4096 at M = 768, 512 + 4 workgroups, 200
+  // us).  The split-K form costs about 1/200 unit per workgroup's worth of
+  // work, with no rounds (4096x4096 at M = 768 / 1024 / 1536: 83 / 109 /
+  // 158 us; tiled 84 / 85 / 132).
   const int64_t groups = (L.n_tiles + kWaves - 1) / kWaves;
   const int64_t w4 = groups * ((M + 127) / 128);
   const int64_t full = w4 / (2 * kCUs), rem = w4 % (2 * kCUs);
-  const int64_t tiled20 = 29 * full + (rem == 0 ? 0 : rem <= kCUs ? 20 : 29);  // tiled time x 20
-  if (w4 < 11 * tiled20) return launch_ms<2>(c, a, st);                     // w4 / 220 units < tiled
+  const int64_t tail20 = rem == 0 ? 0 : rem > kCUs ? 34 : full > 0 ? 13 : 20;
+  const int64_t tiled20 = 34 * full + tail20;            // tiled time x 20
+  if (w4 < 10 * tiled20) return launch_ms<2>(c, a, st);  // w4 / 200 units < tiled
   return launch_ms<4>(c, a, st);
 }
 

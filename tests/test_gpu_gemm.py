@@ -240,16 +240,17 @@ def _kernel_for(fam, M, N):
     """Which matrix-core kernel the launcher picks above 64 tokens (the cost
     model the kernels' launchers state): INT "tiled" (128-token blocks, two
     workgroups per CU) when its grid of w4 = ceil(N/128) x ceil(M/128)
-    workgroups, at 1.45 units of time per full round of 512 plus 1 (up to 256
-    left) or 1.45 for a partial one, is faster than the split-K form at w4/220
-    units, else "split-K"; MX token blocks of 32, 64 or 128 (the largest whose
-    grid stays within one round of 256 workgroups)."""
+    workgroups, at 1.7 units of time per full round of 512 plus 1.7 for a
+    last round of more than 256, or for at most 256 1 unit alone and 0.65
+    after a full round, is faster than the split-K form at w4/200 units, else
+    "split-K"; MX token blocks of 32, 64 or 128 (the largest whose grid stays
+    within one round of 256 workgroups)."""
     groups = -(-N // 128)
     if fam == "int":
         w4 = groups * -(-M // 128)
         full, rem = divmod(w4, 512)
-        tiled20 = 29 * full + (0 if rem == 0 else 20 if rem <= 256 else 29)
-        return "split-K" if w4 < 11 * tiled20 else "tiled"
+        tail20 = 0 if rem == 0 else 34 if rem > 256 else 13 if full else 20
+        return "split-K" if w4 < 10 * (34 * full + tail20) else "tiled"
     if groups * -(-M // 32) <= 256:
         return "block32"
     if groups * -(-M // 64) <= 256:
