@@ -111,19 +111,21 @@ __device__ __forceinline__ void scaled_hi_lo(h8 q, _Float16 s, h8& hi, h8& lo) {
   lo = __builtin_elementwise_fma(q, sv, -hi);
 }
 
-// Dense fp16 outlier fragment of one group word (one non-zero at most).
+// Dense fp16 outlier fragment of one group word (one non-zero at most).  The
+// position bits gather as in outlier_i8, here into 16 * position (bits 20-23
+// of the product are zero too); one 64-bit shift places the fp16 value in
+// its half of the fragment and the position's top bit picks the half.
 template <bool OUT_INT8>
 __device__ __forceinline__ h8 outlier_f16(uint32_t w) {
   float f;
   if constexpr (OUT_INT8) f = (float)(int(w) >> 24);
   else f = __builtin_amdgcn_cvt_f32_fp8(int(w), 3);
   const uint32_t hb = uint32_t(__builtin_bit_cast(unsigned short, (_Float16)f));
-  const uint32_t pos = (__umul24(w & 0x00080808u, kOutPosMagic) >> 24) & 7u;
-  const uint32_t val = hb << ((pos & 1u) << 4);
-  const uint32_t d = pos >> 1;
-  u4v out;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) out[v] = d == uint32_t(v) ? val : 0u;
+  const uint32_t p16 = __builtin_amdgcn_ubfe(__umul24(w & 0x00080808u, kOutPosMagic), 20, 7);
+  const uint64_t v = uint64_t(hb) << (p16 & 63u);
+  const bool upper = (p16 & 64u) != 0;
+  const uint32_t vlo = uint32_t(v), vhi = uint32_t(v >> 32);
+  const u4v out = {upper ? 0u : vlo, upper ? 0u : vhi, upper ? vlo : 0u, upper ? vhi : 0u};
   return __builtin_bit_cast(h8, out);
 }
 
