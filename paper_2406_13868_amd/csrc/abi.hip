@@ -41,8 +41,16 @@ int32_t auto_path(const Cfg& c, int64_t M, int64_t K) {
 // sums costs more than the fuller GPU saves (4096x4096 at M = 64 and 128:
 // 18.9 and 24.4 against 15.6 and 22.2; 16384x4096 at M = 16: 25.4 against
 // 22.2).
+//
+// Above 256 tokens the split-K path runs the tiled kernel over K ranges. It
+// wins over the matrix-core path where that kernel's own grid of ceil(N/128)
+// x ceil(M/128) workgroups would leave the GPU under-filled (under 384):
+// 4096x4096 at M = 512 / 768 / 1024: 47.8 / 78.5 / 80.8 us against 58.9 /
+// 81.1 / 86.1; 4096x11008 at M = 512 / 1024: 108 / 192 against 138 / 218;
+// 11008x4096 at M = 512 (344 workgroups): 118 against 135.  On fuller grids
+// it loses (11008x4096 at M = 640 / 768: 147 / 208 against 140 / 200).
 bool split_wins(int64_t M, int64_t N, int64_t K) {
-  if (M > kSplitMaxM) return false;
+  if (M > kSplitMaxM) return K >= 1024 && (N + 127) / 128 * ((M + 127) / 128) < 384;
   return K >= 8192 || (M >= 64 && N >= 8192) || M >= 256;
 }
 

@@ -23,6 +23,7 @@
 // l%32 and the 8-group 2*kb + l/32 of every 16-K block kb.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "int_frag.h"
@@ -50,6 +51,10 @@ struct MfmaArgs {
   bool y_bf16 = false;  // Y as bf16
   int qs = 0;           // log2(qv / 16): 16-K blocks per inlier scale = 1 << qs
   int srow = 16;        // bytes of one row's inlier scales in a chunk: (128 / qv) * (2 or 1)
+  // tiled kernel over K ranges (grid z): chunks [z * kc_range, (z + 1) *
+  // kc_range) of every tile, raw partial sums to part[z][M][N]
+  int k_ranges = 1, kc_range = 0;
+  float* part = nullptr;
 };
 
 template <int MS, int NI, bool OUT_INT8, int SF>
@@ -67,6 +72,8 @@ __global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
   const int tile = blockIdx.x * kWaves + wave;
   const bool tile_ok = tile < a.n_tiles;
   const int KC = a.n_chunks;
+  const int cb = int(blockIdx.z) * a.kc_range;                   // this workgroup's chunks [cb, ce)
+  const int ce = a.k_ranges > 1 ? min(KC, cb + a.kc_range) : KC;
 
   // ---- activation staging: BM rows x 128 int8 -> fp16 in LDS
   // thread -> (row, 16-byte column piece): 8 pieces per row
@@ -129,16 +136,16 @@ __global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { acc[s][e] = 0.f; acco[s][e] = 0.f; }
 
-  load_x(0);
-  load_w(0);
+  load_x(cb);
+  load_w(cb);
   store_x(0);
   __syncthreads();
 
-  for (int c = 0; c < KC; ++c) {
-    const int buf = c & 1;
+  for (int c = cb; c < ce; ++c) {
+    const int buf = (c - cb) & 1;
     const uint32_t wv[8] = {wr0.x, wr0.y, wr0.z, wr0.w, wr1.x, wr1.y, wr1.z, wr1.w};
     const uint32_t sv[4] = {sr.x, sr.y, sr.z, sr.w};
-    if (c + 1 < KC) { load_x(c + 1); load_w(c + 1); }
+    if (c + 1 < ce) { load_x(c + 1); load_w(c + 1); }
 #pragma unroll
     for (int kb = 0; kb < 8; ++kb) {
       const _Float16 s = block_scale<SF>(sv, kb, a.qs);
@@ -165,7 +172,7 @@ __global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
         for (int ms = 0; ms < MS; ++ms) acc[ms] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[ms], bl, acc[ms], 0, 0, 0);
       }
     }
-    if (c + 1 < KC) {
+    if (c + 1 < ce) {
       store_x(buf ^ 1);
       __syncthreads();
     }
@@ -177,6 +184,17 @@ __global__ __launch_bounds__(kThreads, 2) void int_mfma_kernel(MfmaArgs a) {
   const float so = reinterpret_cast<const float*>(a.blob + a.rows_off)[n];
   // the inlier row scale of two-level e4m3 scales (a power of two: exact)
   const float gi = SC8 ? reinterpret_cast<const float*>(a.blob + a.irow_off)[n] : 1.f;
+  if (a.part) {
+    // this K range's partial sums; split_reduce adds the ranges in order and
+    // scales by s_a
+    const OutRows pr = out_rows(a.part + size_t(blockIdx.z) * size_t(a.M) * size_t(a.N), false, a.M, a.N, m0,
+                                32 * MS);
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) store_out(pr, a.N, n, ms, e, h, fmaf(so, acco[ms][e], gi * acc[ms][e]));
+    return;
+  }
   const RowScales<MS> rs = load_row_scales<MS>(a.s_a, a.M, m0, h);
   const OutRows yr = out_rows(a.Y, a.y_bf16, a.M, a.N, m0, 32 * MS);
 #pragma unroll
@@ -412,7 +430,8 @@ hipError_t launch_ms_ni(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
     if (waves4 >= 2048 || a.n_chunks < 16) return launch_splitk<MS, NI, 4, SF>(c, a, st);
     return launch_splitk<MS, NI, 8, SF>(c, a, st);
   } else {
-    const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)));
+    const dim3 grid(unsigned((a.n_tiles + kWaves - 1) / kWaves), unsigned((a.M + 32 * MS - 1) / (32 * MS)),
+                    unsigned(a.k_ranges));
     const dim3 block(kThreads);
     if (c.fmt_o == SDQ_FMT_INT8)
       hipLaunchKernelGGL((int_mfma_kernel<MS, NI, true, SF>), grid, block, 0, st, a);
@@ -436,7 +455,48 @@ hipError_t launch_ms(const Cfg& c, const MfmaArgs& a, hipStream_t st) {
   return launch_ms_sc<MS, kScaleF16>(c, a, st);
 }
 
+// The tiled kernel over K ranges: S ranges of at least kSplitMinChunksTiled
+// chunks, S chosen for about 512 workgroups (two per CU).
+struct TiledSplit {
+  int64_t groups, m_blocks, S, kc_range;
+};
+constexpr int64_t kSplitMinChunksTiled = 4;
+
+TiledSplit tiled_split_shape(int64_t M, int64_t N, int64_t K) {
+  TiledSplit t;
+  t.groups = ((N + kTileN - 1) / kTileN + kWaves - 1) / kWaves;
+  t.m_blocks = (M + 127) / 128;
+  const int64_t kc = (K + kChunkK - 1) / kChunkK;
+  const int64_t items = t.groups * t.m_blocks;
+  int64_t S = (2 * kCUs + items - 1) / items;
+  S = std::max<int64_t>(1, std::min<int64_t>(S, kc / kSplitMinChunksTiled));
+  t.kc_range = (kc + S - 1) / S;
+  t.S = (kc + t.kc_range - 1) / t.kc_range;  // no empty range
+  return t;
+}
+
 }  // namespace
+
+size_t int_tiled_split_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  return size_t(tiled_split_shape(M, N, K).S) * size_t(M) * size_t(N) * sizeof(float);
+}
+
+hipError_t launch_int_tiled_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                                  const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
+                                  hipStream_t st) {
+  const Layout L = layout_for(c, N, K);
+  const TiledSplit t = tiled_split_shape(M, N, K);
+  MfmaArgs a{Xq, s_a, blob, Y, int(M), int(N), int(K), int(L.n_chunks), int(L.n_tiles),
+             L.scales_off, L.rows_off, L.irow_off};
+  a.qs = c.qv == 64 ? 2 : c.qv == 32 ? 1 : 0;
+  a.srow = (kChunkK / c.qv) * c.scale_bytes();
+  a.k_ranges = int(t.S);
+  a.kc_range = int(t.kc_range);
+  a.part = static_cast<float*>(workspace);
+  const hipError_t e = launch_ms<4>(c, a, st);
+  if (e != hipSuccess) return e;
+  return launch_split_reduce(a.part, s_a, Y, M, N, int(t.S), c.y_bf16, st);
+}
 
 hipError_t launch_int_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                            const uint8_t* blob, int64_t N, int64_t K, void* Y, hipStream_t st) {

@@ -323,7 +323,22 @@ hipError_t launch_split_ms(const Cfg& c, const SplitArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// The tiled kernel's 128-token blocks expand every weight once per 128
+// tokens where this kernel's 64-token blocks expand it twice, but give half
+// as many workgroups per K range, so more ranges and partial sums.  Measured
+// (tiled over K ranges against this kernel): it wins on long rows and wide
+// layers (4096x11008 at M = 256: 64.7 against 71.5 us; 16384x4096 at M =
+// 256: 86.5 against 94.2; 11008x4096 at M = 128: 43.0 against 50.7) and
+// above 256 tokens (4096x4096 at M = 384 / 512: 42.5 / 47.8 against 46.9 /
+// 51.9), and loses on 4096x4096 at M = 256 (35.4 against 31.2) and on
+// 11008x4096 at M = 192 / 256 (76.6 / 78.7 against 69.6 / 75.2).
+bool int_split_tiled(int64_t M, int64_t N, int64_t K) {
+  if (M <= 64) return false;
+  return M > kSplitMaxM || K >= 8192 || N >= 16384 || (M <= 128 && N >= 8192);
+}
+
 size_t int_split_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (int_split_tiled(M, N, K)) return int_tiled_split_workspace_bytes(M, N, K);
   const SplitShape s = split_shape(M, N, K);
   return size_t(s.S) * size_t(M) * size_t(N) * sizeof(float);
 }
@@ -331,6 +346,7 @@ size_t int_split_workspace_bytes(int64_t M, int64_t N, int64_t K) {
 hipError_t launch_int_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                             const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                             hipStream_t st) {
+  if (int_split_tiled(M, N, K)) return launch_int_tiled_split(c, Xq, s_a, M, blob, N, K, Y, workspace, st);
   const Layout L = layout_for(c, N, K);
   const SplitShape sh = split_shape(M, N, K);
   SplitArgs a{Xq, blob, static_cast<float*>(workspace), int(M), int(N), int(K), int(L.n_chunks),

@@ -82,6 +82,14 @@ size_t int_split_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_int_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
                             const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
                             hipStream_t st);
+// Whether the split-K path takes the tiled matrix-core kernel (128-token
+// blocks) over K ranges instead: partial sums in `workspace` (at least
+// int_tiled_split_workspace_bytes(M, N, K) bytes), the same second kernel.
+bool int_split_tiled(int64_t M, int64_t N, int64_t K);
+size_t int_tiled_split_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_int_tiled_split(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,
+                                  const uint8_t* blob, int64_t N, int64_t K, void* Y, void* workspace,
+                                  hipStream_t st);
 
 // MX family, scaled matrix-core kernel (any M).
 hipError_t launch_mx_mfma(const Cfg& c, const uint8_t* Xq, const float* s_a, int64_t M,

@@ -420,11 +420,15 @@ def test_hip_graph_replays_match_eager_two_pass(which):
 
 @pytest.mark.parametrize("c", [INT_CFGS[0], INT_CFGS[1], INT_CFGS[3], INT_CFGS[5]], ids=_ids)
 @pytest.mark.parametrize("M,N,K", [(9, 4128, 512), (31, 300, 2560), (33, 97, 4096), (64, 1000, 16384),
-                                   (100, 544, 1152), (129, 64, 8192), (200, 2080, 640), (256, 33, 128)])
+                                   (100, 544, 1152), (129, 64, 8192), (200, 2080, 640), (256, 33, 128),
+                                   (100, 8200, 384), (300, 544, 2560), (520, 200, 4160)])
 def test_split_k_ragged_shapes(c, M, N, K):
     """The split-K path on token counts around its 32- and 64-token blocks,
     row counts that leave a part of a 128-row group, K ranges from one chunk
-    to 128 (1 to 32 ranges), against the oracle."""
+    to 128 (1 to 32 ranges), against the oracle; and its tiled form over K
+    ranges (128-token blocks: 129 x 64 x 8192 in 16 ranges, 100 x 8200 x 384
+    in one, 300 x 544 x 2560 in 5, 520 x 200 x 4160 in 7 with a partial last
+    chunk)."""
     cfg, cfg_o = _cfgs(*c)
     X = synth.make_x(4, M, K)
     W = synth.make_w(4, 3, N, K)

@@ -309,11 +309,14 @@ def test_gemm_path_choice():
     assert sdq.gemm_path(mx, 2048, 4096, 4096, workspace=True) == sdq.PATH_DENSE
     # the INT split-K path where it measured faster than the matrix-core path
     for (M, N, K) in ((16, 4096, 16384), (64, 4096, 16384), (64, 11008, 4096), (64, 16384, 4096),
-                      (256, 4096, 4096), (256, 11008, 4096)):
+                      (256, 4096, 4096), (256, 11008, 4096),
+                      (257, 4096, 4096), (1024, 4096, 4096), (512, 11008, 4096), (1024, 4096, 11008)):
         assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_SPLITK, (M, N, K)
         assert sdq.gemm_workspace_size(cfg, M, N, K) > 0
+    # above 256 tokens only while the tiled grid of ceil(N/128) x ceil(M/128)
+    # workgroups stays under 384, and with K for two ranges
     for (M, N, K) in ((16, 16384, 4096), (32, 16384, 4096), (64, 4096, 4096), (128, 4096, 4096),
-                      (257, 4096, 4096),
+                      (1536, 4096, 4096), (640, 11008, 4096), (512, 4096, 896),
                       (4096, 4096, 4096)):
         assert sdq.gemm_path(cfg, M, N, K, workspace=True) == sdq.PATH_MFMA, (M, N, K)
         assert sdq.gemm_workspace_size(cfg, M, N, K) == 0
@@ -325,6 +328,11 @@ def test_gemm_path_choice():
         b = sdq.gemm_workspace_size(cfg, M, N, K, sdq.PATH_SPLITK)
         S = b // max(4 * M * N, 1)
         assert b == 4 * S * M * N and 1 <= max(S, 1) <= max(1, K // 512), (M, N, K, S)
+    # the tiled kernel over K ranges (long rows, wide layers, above 256 tokens):
+    # about 512 workgroups of 128 outputs x 128 tokens
+    assert sdq.gemm_workspace_size(cfg, 256, 4096, 11008, sdq.PATH_SPLITK) == 8 * 256 * 4096 * 4
+    assert sdq.gemm_workspace_size(cfg, 512, 4096, 4096, sdq.PATH_SPLITK) == 4 * 512 * 4096 * 4
+    assert sdq.gemm_workspace_size(cfg, 512, 11008, 4096, sdq.PATH_SPLITK) == 2 * 512 * 11008 * 4
     # the MX family's split-K path: S K ranges of at least 4 chunks, about 512 workgroups
     for (M, N, K) in ((256, 4096, 4096), (128, 11008, 4096), (256, 4096, 11008), (64, 64, 288)):
         b = sdq.gemm_workspace_size(mx, M, N, K, sdq.PATH_SPLITK)
